@@ -1,0 +1,209 @@
+#!/usr/bin/env python3
+"""Benchmark of one tree-verification step on one MI355X.
+
+A step is one dv_verify_step call: the draft tree goes through every decoder
+layer and the lm_head, then argmax and greedy acceptance; the call returns
+after the accept result is back on the host.  Inputs (weights, KV cache,
+tree) are seeded synthetic data resident in HBM before the timed region.
+
+Prints ONE JSON line: metric/value (draft tokens verified per second, one
+GPU), ms_per_step, the roofline of the dominant kernel class (the
+weight-streaming projections, timed with HIP events inside the timed region)
+and the CPU oracle timed on a bounded sample of the same workload.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+from dataclasses import replace
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import synth  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0
+
+
+def log(msg):
+    print("[bench] " + msg, file=sys.stderr, flush=True)
+
+
+def gemm_bytes(mc, m, esz):
+    """Algorithmic bytes of the projection kernels in one step: weights once,
+    fp32 activations in once, outputs written once (residual: read + write)."""
+    d, f, v, L = mc.d_model, mc.d_ffn, mc.vocab, mc.n_layers
+    w = esz * (L * (4 * d * d + 3 * d * f) + v * d)
+    per_layer = 4 * m * (d + d + 2 * d * esz / 4      # QKV: in, q out, k/v cache write
+                         + d + 2 * d                  # O: in, residual read+write
+                         + d + f                      # gate/up: in, h out
+                         + f + 2 * d)                 # down: in, residual read+write
+    head = 4 * m * d + 8 * m * (v // 32)              # lm_head: in, per-tile argmax partials
+    return w + L * per_layer + head, 4 * L + 1
+
+
+def step_bytes(mc, m, p, esz):
+    """Algorithmic HBM bytes of a whole step (no logits written)."""
+    d, L, H, hd = mc.d_model, mc.n_layers, mc.n_heads, mc.head_dim
+    g, _ = gemm_bytes(mc, m, esz)
+    kv_read = L * 2 * H * (p + m) * hd * esz
+    return g + kv_read + m * d * esz
+
+
+def cpu_baseline(wl, toks, par):
+    """The oracle as it stands (float64), timed on the host over a bounded
+    sample: the same tree, context and shapes with 1 and then 3 of the decoder
+    layers; per-layer time x n_layers + the rest gives the step estimate."""
+    import oracle.verify as ov
+    try:
+        import threadpoolctl
+        info = threadpoolctl.threadpool_info()
+        threads = max([i.get("num_threads", 1) for i in info] or [1])
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count()
+    mc, sd = wl.model, wl.seeds
+    lm = synth.lm_head(mc, sd["weights"])
+    fn = synth.final_norm(mc)
+    times = {}
+    for s in (1, 3):
+        layers = [synth.layer_weights(mc, sd["weights"], l) for l in range(s)]
+        raw_kv = [synth.kv_layer(mc, sd["kv"], l, wl.context) for l in range(s)]
+        kv_o = ov.kv_from_raw(raw_kv)
+        om = ov.OracleModel(replace(mc, n_layers=s), lambda l: layers[l],
+                            lambda ids: synth.embed_rows(mc, sd["weights"], ids), lm, fn)
+        t0 = time.perf_counter()
+        ov.verify_step(om, kv_o, toks, par)
+        times[s] = time.perf_counter() - t0
+        log("cpu oracle: %d layer(s) %.2f s" % (s, times[s]))
+        del layers, raw_kv, kv_o
+    per_layer = (times[3] - times[1]) / 2.0
+    rest = max(times[1] - per_layer, 0.0)
+    est = rest + mc.n_layers * per_layer
+    return {
+        "value": round(len(toks) / est, 4), "unit": "draft tokens/s", "cores": int(threads),
+        "kind": "oracle", "ms_per_step": round(est * 1e3, 1),
+        "sample": ("float64 numpy oracle, same %d-node tree and %d-token context, run with 1 "
+                   "and 3 of the %d decoder layers (%.1f s of CPU work); step = "
+                   "rest + %d x per-layer time" % (len(toks), wl.context, mc.n_layers,
+                                                    times[1] + times[3], mc.n_layers)),
+        "host_cpus": os.cpu_count(),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="llama13b-bf16-m16-ctx1024",
+                    help="one of %s, or sweep-M" % ", ".join(synth.WORKLOADS))
+    ap.add_argument("--cpu-baseline", choices=["on", "off"], default="on")
+    ap.add_argument("--roofline-events", choices=["inline", "off"], default="inline",
+                    help="HIP events around the projection kernels inside the timed region")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: the verification step is not split across "
+              "GPUs in this build (requested --gpus %d)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    if args.workload.startswith("sweep-"):
+        wl = synth.sweep_workload(int(args.workload.split("-")[1]))
+    else:
+        wl = synth.WORKLOADS[args.workload]
+    mc, sd = wl.model, wl.seeds
+    m, p = wl.n_tree, wl.context
+    esz = 2 if mc.weight_dtype == "bf16" else 4
+
+    import torch
+    from paper_2412_18934_amd import device as D
+    from paper_2412_18934_amd import dv
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    dv.lib()  # fail loudly if the HIP library is missing
+
+    t0 = time.perf_counter()
+
+    def layer_fn(l):
+        if l % 8 == 0:
+            log("weights: layer %d/%d" % (l, mc.n_layers))
+        return synth.layer_weights(mc, sd["weights"], l)
+
+    W = D.DeviceWeights(mc.n_layers, layer_fn, synth.embed(mc, sd["weights"]),
+                        synth.lm_head(mc, sd["weights"]), synth.final_norm(mc))
+    cap = p + 64
+    kv = D.DeviceKV(mc.n_layers, mc.n_heads, mc.head_dim, cap, mc.weight_dtype)
+    for l in range(mc.n_layers):
+        k, v = synth.kv_layer(mc, sd["kv"], l, p)
+        kv.set_layer(l, k, v)
+    kv.c.len = p
+    toks, par = synth.random_tree(sd["tree"], m, wl.depth, mc.vocab, chain=wl.chain)
+    log("inputs resident in HBM (%.1f GB weights) after %.1f s" % (W.nbytes() / 1e9, time.perf_counter() - t0))
+
+    cfg = D.make_config(mc.n_layers, mc.d_model, mc.n_heads, mc.head_dim, mc.d_ffn, mc.vocab,
+                        mc.rms_eps, mc.rope_base, mc.weight_dtype, cap, 64)
+    stream = torch.cuda.current_stream().cuda_stream
+    h = dv.dv_verify_init(cfg, W.c, stream)
+    for _ in range(args.warmup):
+        acc = dv.dv_verify_step(h, toks, par, kv.c, 0)
+    log("warmup done (accept_len %d)" % acc.accept_len)
+
+    if args.roofline_events == "inline":
+        dv.dv_profile_enable(h, 1 << dv.DV_K_GEMM)
+    dv.dv_profile_read(h, dv.DV_K_GEMM, reset=True)
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for _ in range(args.steps):
+        acc = dv.dv_verify_step(h, toks, par, kv.c, 0)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    dv.dv_profile_enable(h, 0)
+    gemm_ms, gemm_n = dv.dv_profile_read(h, dv.DV_K_GEMM, reset=True)
+    ms = elapsed / args.steps * 1e3
+    log("timed %d steps: %.3f ms/step" % (args.steps, ms))
+
+    gbytes, glaunch = gemm_bytes(mc, m, esz)
+    roof = None
+    if gemm_n:
+        avg_ms = gemm_ms / gemm_n
+        per_launch = gbytes / glaunch
+        achieved = per_launch / (avg_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "kernel": "k_gemm_* (QKV, O, gate/up, down, lm_head)",
+                "bytes_per_launch": int(per_launch), "avg_launch_us": round(avg_ms * 1e3, 2),
+                "launches_per_step": glaunch}
+    sbytes = step_bytes(mc, m, p, esz)
+    step_gbs = sbytes / (ms * 1e-3) / 1e9
+
+    result = {
+        "metric": "draft tokens verified/s (13B-shape tree verify step, 1 GPU)",
+        "value": round(m / (ms * 1e-3), 2),
+        "unit": "draft tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": mc.weight_dtype, "data": "synthetic",
+        "config": {"workload": wl.name, "n_tree": m, "context": p, "depth": wl.depth,
+                   "layers": mc.n_layers, "d_model": mc.d_model, "d_ffn": mc.d_ffn,
+                   "vocab": mc.vocab},
+        "step_hbm": {"bytes": int(sbytes), "achieved_gbs": round(step_gbs, 1),
+                     "frac": round(step_gbs / HBM_PEAK_GBS, 4)},
+        "roofline": roof,
+        "accept_len": acc.accept_len,
+    }
+    dv.dv_verify_free(h)
+    if args.cpu_baseline == "on":
+        del W, kv
+        torch.cuda.empty_cache()
+        result["cpu_baseline"] = cpu_baseline(wl, toks, par)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

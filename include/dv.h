@@ -1,0 +1,187 @@
+/*
+ * dv.h - C ABI of the MI355X tree-verification library (libdv.so).
+ *
+ * One call runs the target model's parallel verification of a draft token
+ * tree: the candidates go through the decoder stack in a single forward pass
+ * over the committed KV cache, and the greedy acceptance rule picks the
+ * accepted tokens, which then start the next round (Dovetail, arXiv
+ * 2412.18934, Section 3.1 "CPU/GPU Heterogeneous Architecture"; greedy
+ * exact-match verification per Section 5 "Verifying Draft Tokens").  The
+ * verification latency T_V(gamma) this call realises is the quantity of
+ * Section 2.2, eq. (speedup-breakdown), modelled in Appendix B as
+ * max(T_c, T_p) + beta min(T_c, T_p).
+ *
+ * Conventions (the paper does not fix them; they are the standard Llama-2
+ * decoder block read from the models of Section 4):
+ *   - pre-norm RMSNorm, no biases, multi-head attention, SwiGLU FFN,
+ *     rotary embedding with rotate-half pairing, untied lm_head, final norm;
+ *   - every matrix is row-major [out][in]; activations are fp32;
+ *   - tree node 0 is the root (the pending token), parents[0] = -1 and
+ *     0 <= parents[i] < i for i >= 1; node i attends to every committed key
+ *     plus its ancestors and itself and sits at position len + depth(i) - 1
+ *     (root depth 1);
+ *   - new keys/values are rounded to the cache dtype before any use;
+ *   - argmax ties go to the lowest token id; the deepest accepted node wins,
+ *     lowest node index on ties; the bonus token is the argmax at that node.
+ *
+ * Memory: the caller owns weights, KV buffers, logits and accept structs.
+ * Device pointers are plain HIP device addresses (e.g. torch tensors'
+ * data_ptr()).  The handle owns its workspace and frees it in
+ * dv_verify_free; the library never frees caller memory.  A handle is bound
+ * to one HIP stream and is not thread-safe.
+ *
+ * Errors: every call returns DV_OK (0) or a negative code.  Arguments are
+ * validated before anything is launched, so a rejected call changes nothing
+ * and the handle stays usable.  A HIP runtime failure returns DV_EHIP and
+ * poisons the handle (every later call returns DV_EHIP).  dv_last_error
+ * gives a message for the most recent failure.
+ */
+#ifndef DV_H
+#define DV_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DV_OK 0
+#define DV_EINVAL (-1)    /* bad config, tree, token id, pointer or struct    */
+#define DV_ECAPACITY (-2) /* len + n_tree exceeds the KV capacity or max_ctx  */
+#define DV_ESTATE (-3)    /* commit without a matching pending step           */
+#define DV_EHIP (-4)      /* HIP runtime error; sticky                        */
+#define DV_ENOMEM (-5)    /* workspace allocation failed at init              */
+
+#define DV_F32 0
+#define DV_BF16 1
+
+#define DV_MAX_TREE 64
+
+/* Model shape.  weight_dtype is also the KV-cache dtype.  Shape limits:
+ * head_dim in {64, 128} with n_heads * head_dim == d_model; d_model and
+ * vocab multiples of 32; d_ffn a multiple of 16; 1 <= max_tree <= 64;
+ * for DV_BF16, d_model and d_ffn multiples of 32. */
+typedef struct dv_config {
+    int32_t n_layers;
+    int32_t d_model;
+    int32_t n_heads;
+    int32_t head_dim;
+    int32_t d_ffn;
+    int32_t vocab;
+    float rms_eps;
+    float rope_base;
+    int32_t weight_dtype; /* DV_F32 or DV_BF16                               */
+    int32_t max_ctx;      /* largest len + n_tree any step may reach          */
+    int32_t max_tree;     /* largest n_tree (and prefill chunk), <= 64        */
+} dv_config;
+
+/* Device pointers to weights, all of weight_dtype.  The per-layer fields are
+ * HOST arrays of n_layers device pointers; they are copied at init, the
+ * weights themselves are not copied and must outlive the handle. */
+typedef struct dv_weights {
+    const void *embed;       /* [vocab][d_model]                 */
+    const void *final_norm;  /* [d_model]                        */
+    const void *lm_head;     /* [vocab][d_model]                 */
+    const void *const *attn_norm; /* [d_model]                   */
+    const void *const *wq;        /* [d_model][d_model]          */
+    const void *const *wk;        /* [d_model][d_model]          */
+    const void *const *wv;        /* [d_model][d_model]          */
+    const void *const *wo;        /* [d_model][d_model]          */
+    const void *const *ffn_norm;  /* [d_model]                   */
+    const void *const *w_gate;    /* [d_ffn][d_model]            */
+    const void *const *w_up;      /* [d_ffn][d_model]            */
+    const void *const *w_down;    /* [d_model][d_ffn]            */
+} dv_weights;
+
+/* KV cache: device buffers [n_layers][n_heads][capacity][head_dim] of
+ * weight_dtype; entries [0, len) are committed.  len is host state that
+ * dv_kv_commit and dv_prefill advance. */
+typedef struct dv_kv {
+    void *k;
+    void *v;
+    int32_t capacity;
+    int32_t len;
+} dv_kv;
+
+/* Result of one verification step (host struct). */
+typedef struct dv_accept {
+    int32_t accept_len;             /* accepted nodes on the path, root included */
+    int32_t path[DV_MAX_TREE];      /* node indices root -> deepest accepted     */
+    int32_t bonus_token;            /* target's argmax at the last path node     */
+    int32_t n_tree;                 /* step size, checked by dv_kv_commit        */
+    int32_t base_len;               /* kv->len at the step, checked by commit    */
+    int32_t argmax[DV_MAX_TREE];    /* per-node argmax of the logits             */
+} dv_accept;
+
+typedef struct dv_handle dv_handle;
+
+/* Create a handle: validates cfg, copies the weight pointer tables, builds
+ * the rotary cos/sin table (angles in double precision, stored fp32) and
+ * allocates the workspace.  stream is a hipStream_t (NULL = default stream).
+ * Returns DV_EINVAL, DV_ENOMEM or DV_EHIP on failure (*out set to NULL). */
+int dv_verify_init(const dv_config *cfg, const dv_weights *w, void *stream, dv_handle **out);
+
+/* One verification step over a draft tree (Section 3.1).
+ *   tokens, tree_parents: HOST arrays of n_tree int32 (see tree contract);
+ *   kv: the cache; the tree's keys/values are written to slots
+ *       [len, len + n_tree); kv->len is not changed;
+ *   out_logits: device [n_tree][vocab] fp32, or NULL to skip writing logits;
+ *   out_accept: host struct, filled after the step completes (the call
+ *       synchronises the handle's stream).
+ * Repeating a step without committing recomputes the same result.
+ * Errors: DV_EINVAL (tree, ids, pointers), DV_ECAPACITY, DV_EHIP. */
+int dv_verify_step(dv_handle *h, const int32_t *tokens, const int32_t *tree_parents,
+                   int32_t n_tree, dv_kv *kv, float *out_logits, dv_accept *out_accept);
+
+/* Commit the accepted path of the pending step: for k < accept_len the
+ * entries of node path[k] move to slot len + k (all layers, heads, K and V;
+ * all sources are read before any destination is written), then
+ * kv->len += accept_len.  accept must come from the last dv_verify_step on
+ * this handle and kv (same n_tree and base_len), with path a root-to-node
+ * chain of that step's tree.  Errors: DV_EINVAL, DV_ESTATE, DV_EHIP. */
+int dv_kv_commit(dv_handle *h, dv_kv *kv, const dv_accept *accept);
+
+/* Build the cache from a prompt: runs tokens[0..n) as chains of at most
+ * max_tree tokens through the same kernels and commits all of them
+ * (kv->len += n).  out_next_token (host, nullable) receives the argmax after
+ * the last prompt token, the root of the first draft tree.
+ * Errors: DV_EINVAL, DV_ECAPACITY, DV_EHIP. */
+int dv_prefill(dv_handle *h, const int32_t *tokens, int32_t n, dv_kv *kv,
+               int32_t *out_next_token);
+
+/* Release the handle and its workspace (NULL is ignored). */
+void dv_verify_free(dv_handle *h);
+
+/* Message for the most recent failure on h (or of the last failed init when
+ * h is NULL).  Valid until the next call on the same handle. */
+const char *dv_last_error(const dv_handle *h);
+
+/* Host-only tree preprocessing used by dv_verify_step: validates parents
+ * (tree contract above, 1 <= n_tree <= 64) and writes, per node, its
+ * position base_len + depth - 1, its depth (root 1) and its ancestor-or-self
+ * bitmask (bit j set iff node j is on the root path of node i).  Output
+ * pointers are host arrays of n_tree entries.  Returns DV_OK or DV_EINVAL. */
+int dv_tree_prepare(const int32_t *tree_parents, int32_t n_tree, int32_t base_len,
+                    int32_t *out_pos, int32_t *out_depth, uint64_t *out_anc);
+
+/* Per-kernel timing with HIP events on the handle's stream.  class_mask
+ * selects kernel classes (bit c for class c; 0 turns timing off); each launch
+ * of a selected class is bracketed by events, read back when a step or
+ * prefill synchronises.  dv_profile_read returns the summed duration (ms) and
+ * launch count of one class since the last reset, and resets when
+ * reset != 0.  Classes: DV_K_GEMM (weight-streaming projections and
+ * lm_head), DV_K_ATTN (tree attention incl. split merge), DV_K_NORM,
+ * DV_K_OTHER (argmax reduce + acceptance).  Errors: DV_EINVAL. */
+#define DV_K_GEMM 0
+#define DV_K_ATTN 1
+#define DV_K_NORM 2
+#define DV_K_OTHER 3
+#define DV_K_COUNT 4
+int dv_profile_enable(dv_handle *h, int32_t class_mask);
+int dv_profile_read(dv_handle *h, int32_t kernel_class, double *total_ms, int64_t *launches,
+                    int32_t reset);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DV_H */

@@ -39,7 +39,7 @@ def bf16_to_f64(bits: np.ndarray) -> np.ndarray:
 def _to_float(raw: np.ndarray, dtype) -> np.ndarray:
     if raw.dtype == np.uint16:
         return bf16_to_f64(raw).astype(dtype, copy=False)
-    return np.asarray(raw).astype(dtype)
+    return np.asarray(raw).astype(dtype, copy=False)
 
 
 def round_to_bf16(x: np.ndarray) -> np.ndarray:

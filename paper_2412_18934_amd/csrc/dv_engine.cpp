@@ -1,0 +1,607 @@
+// Host side of libdv: argument validation, tree preprocessing, workspace,
+// the per-step launch sequence, KV commit and prefill.  Declarations and the
+// contract of every entry point are in include/dv.h.
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "dv.h"
+#include "dv_internal.h"
+
+namespace {
+
+thread_local std::string g_init_error;
+
+struct LayerW {
+    const void *attn_norm, *wq, *wk, *wv, *wo, *ffn_norm, *w_gate, *w_up, *w_down;
+};
+
+struct GemmPlan {
+    int n_tiles = 0, ks = 1, k_per_split = 0, mfma = 0;
+};
+
+struct ProfEv {
+    int cls;
+    hipEvent_t a, b;
+};
+
+}  // namespace
+
+struct dv_handle {
+    dv_config cfg{};
+    hipStream_t stream = nullptr;
+    int bf16 = 0;
+    size_t esz = 4;
+    const void *embed = nullptr, *final_norm = nullptr, *lm_head = nullptr;
+    std::vector<LayerW> layers;
+
+    // workspace (device)
+    float *x = nullptr, *u = nullptr, *q = nullptr, *attn = nullptr, *hbuf = nullptr;
+    float *part_o = nullptr, *part_m = nullptr, *part_l = nullptr;
+    int attn_split_max = 0;
+    float *part_gemm = nullptr;
+    int32_t *counters = nullptr;
+    float *arg_val = nullptr;
+    int32_t *arg_idx = nullptr;
+    float *rope_cos = nullptr, *rope_sin = nullptr;
+    StepDesc *d_sd = nullptr, *h_sd = nullptr;
+    DevAccept *d_acc = nullptr, *h_acc = nullptr;
+    GemmPlan p_qkv, p_o, p_gu, p_down, p_lm;
+
+    // pending (uncommitted) step
+    bool pending = false;
+    int32_t pend_n = 0, pend_base = 0;
+    int32_t pend_parents[DV_TREE_MAX];
+    void *pend_k = nullptr, *pend_v = nullptr;
+
+    bool poisoned = false;
+    std::string err;
+
+    // per-kernel-class event timing
+    int prof = 0;  // class mask
+    bool prof_open = false;
+    std::vector<hipEvent_t> ev_pool;
+    std::vector<ProfEv> ev_live;
+    double prof_ms[DV_K_COUNT] = {0, 0, 0, 0};
+    int64_t prof_n[DV_K_COUNT] = {0, 0, 0, 0};
+};
+
+namespace {
+
+int set_err(dv_handle *h, int code, const char *fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    if (h) h->err = buf;
+    else g_init_error = buf;
+    return code;
+}
+
+int hip_fail(dv_handle *h, hipError_t e, const char *what)
+{
+    if (h) h->poisoned = true;
+    return set_err(h, DV_EHIP, "HIP error in %s: %s", what, hipGetErrorString(e));
+}
+
+#define HIPCHK(h, call)                                        \
+    do {                                                       \
+        hipError_t e_ = (call);                                \
+        if (e_ != hipSuccess) return hip_fail((h), e_, #call); \
+    } while (0)
+
+int ceil_div(int a, int b) { return (a + b - 1) / b; }
+int round_up(int a, int b) { return ceil_div(a, b) * b; }
+
+// Split-K so that a projection launches enough workgroups to cover the
+// chip (256 CUs, ~2.5 workgroups each), with splits aligned to `align`.
+GemmPlan make_plan(int n_tiles, int K, int align, int mfma)
+{
+    GemmPlan p;
+    p.n_tiles = n_tiles;
+    p.mfma = mfma;
+    int ks = std::max(1, std::min(8, ceil_div(640, n_tiles)));
+    int kps = round_up(ceil_div(K, ks), align);
+    p.k_per_split = kps;
+    p.ks = ceil_div(K, kps);
+    return p;
+}
+
+void prof_begin(dv_handle *h, int cls)
+{
+    h->prof_open = false;
+    if (!(h->prof >> cls & 1)) return;
+    ProfEv e{cls, nullptr, nullptr};
+    if (h->ev_pool.size() >= 2) {
+        e.a = h->ev_pool.back(); h->ev_pool.pop_back();
+        e.b = h->ev_pool.back(); h->ev_pool.pop_back();
+    } else {
+        (void)hipEventCreate(&e.a);
+        (void)hipEventCreate(&e.b);
+    }
+    (void)hipEventRecord(e.a, h->stream);
+    h->ev_live.push_back(e);
+    h->prof_open = true;
+}
+
+void prof_end(dv_handle *h)
+{
+    if (!h->prof_open) return;
+    h->prof_open = false;
+    (void)hipEventRecord(h->ev_live.back().b, h->stream);
+}
+
+// after a stream sync: fold recorded event pairs into the totals
+void prof_collect(dv_handle *h)
+{
+    for (auto &e : h->ev_live) {
+        float ms = 0.f;
+        if (hipEventElapsedTime(&ms, e.a, e.b) == hipSuccess) {
+            h->prof_ms[e.cls] += ms;
+            h->prof_n[e.cls] += 1;
+        }
+        h->ev_pool.push_back(e.a);
+        h->ev_pool.push_back(e.b);
+    }
+    h->ev_live.clear();
+}
+
+int check_tree(dv_handle *h, const int32_t *parents, int n, int base, int32_t *pos,
+               int32_t *depth, uint64_t *anc)
+{
+    int rc = dv_tree_prepare(parents, n, base, pos, depth, anc);
+    if (rc != DV_OK) return set_err(h, rc, "invalid draft tree (parents[0] must be -1, 0 <= parents[i] < i, 1 <= n_tree <= 64)");
+    return DV_OK;
+}
+
+// Enqueue the forward pass over the tree described by h->h_sd (already
+// filled) and, when with_head, the lm_head, argmax and acceptance kernels.
+int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_head)
+{
+    const dv_config &c = h->cfg;
+    StepDesc *sd = h->h_sd;
+    const int M = sd->M, Mpad = sd->Mpad, P = sd->P;
+    const int d = c.d_model, hd = c.head_dim, H = c.n_heads, F = c.d_ffn;
+    hipStream_t s = h->stream;
+    HIPCHK(h, hipMemcpyAsync(h->d_sd, h->h_sd, sizeof(StepDesc), hipMemcpyHostToDevice, s));
+
+    const size_t layer_kv = (size_t)H * kv->capacity * hd * h->esz;
+    // attention split over the P + M keys
+    const int total = P + M;
+    const int target = std::max(1, ceil_div(1024, H));
+    const int kps = round_up(ceil_div(total, std::min(target, h->attn_split_max)), DV_ATTN_TILE);
+    const int n_split = ceil_div(total, kps);
+
+    GemmArgs g{};
+    g.M = M;
+    g.Mpad = Mpad;
+    g.cap = kv->capacity;
+    g.P = P;
+    g.hd = hd;
+    g.rope_cos = h->rope_cos;
+    g.rope_sin = h->rope_sin;
+    g.pos = h->d_sd->pos;
+    g.part = h->part_gemm;
+    g.counters = h->counters;
+
+    NormArgs na{};
+    na.d = d;
+    na.eps = c.rms_eps;
+    na.M = M;
+    na.tokens = h->d_sd->tokens;
+    na.u = h->u;
+    na.x = h->x;
+    na.x_out = h->x;
+
+    AttnArgs aa{};
+    aa.q = h->q;
+    aa.cap = kv->capacity;
+    aa.hd = hd;
+    aa.H = H;
+    aa.keys_per_split = kps;
+    aa.n_split = n_split;
+    aa.sd = h->d_sd;
+    aa.part_o = h->part_o;
+    aa.part_m = h->part_m;
+    aa.part_l = h->part_l;
+    aa.out = h->attn;
+
+    auto gemm = [&](const GemmPlan &p, int epi, const void *w0, const void *w1, const void *w2,
+                    int N, int K, const float *x, float *out) -> int {
+        GemmArgs a = g;
+        a.w0 = w0;
+        a.w1 = w1;
+        a.w2 = w2;
+        a.N = N;
+        a.K = K;
+        a.n_tiles = p.n_tiles;
+        a.ks = p.ks;
+        a.k_per_split = p.k_per_split;
+        a.x = x;
+        a.out = out;
+        prof_begin(h, DV_K_GEMM);
+        hipError_t e = launch_gemm(a, epi, h->bf16, p.mfma, s);
+        prof_end(h);
+        if (e != hipSuccess) return hip_fail(h, e, "gemm launch");
+        return DV_OK;
+    };
+    auto norm = [&](const void *gain, const void *embed) -> int {
+        NormArgs a = na;
+        a.gain = gain;
+        a.embed = embed;
+        prof_begin(h, DV_K_NORM);
+        hipError_t e = launch_rmsnorm(a, Mpad, h->bf16, s);
+        prof_end(h);
+        if (e != hipSuccess) return hip_fail(h, e, "rmsnorm launch");
+        return DV_OK;
+    };
+
+    int rc;
+    for (int l = 0; l < c.n_layers; ++l) {
+        const LayerW &w = h->layers[l];
+        if ((rc = norm(w.attn_norm, l == 0 ? h->embed : nullptr))) return rc;
+        g.kc = (char *)kv->k + l * layer_kv;
+        g.vc = (char *)kv->v + l * layer_kv;
+        if ((rc = gemm(h->p_qkv, EPI_QKV, w.wq, w.wk, w.wv, d, d, h->u, h->q))) return rc;
+        aa.kc = g.kc;
+        aa.vc = g.vc;
+        prof_begin(h, DV_K_ATTN);
+        hipError_t e = launch_attention(aa, h->bf16, s);
+        if (e == hipSuccess) e = launch_attn_merge(aa, Mpad, s);
+        prof_end(h);
+        if (e != hipSuccess) return hip_fail(h, e, "attention launch");
+        if ((rc = gemm(h->p_o, EPI_RESID, w.wo, nullptr, nullptr, d, d, h->attn, h->x))) return rc;
+        if ((rc = norm(w.ffn_norm, nullptr))) return rc;
+        if ((rc = gemm(h->p_gu, EPI_SWIGLU, w.w_gate, w.w_up, nullptr, F, d, h->u, h->hbuf))) return rc;
+        if ((rc = gemm(h->p_down, EPI_RESID, w.w_down, nullptr, nullptr, d, F, h->hbuf, h->x))) return rc;
+    }
+    if (!with_head) return DV_OK;
+    if ((rc = norm(h->final_norm, nullptr))) return rc;
+    {
+        GemmArgs a = g;
+        a.arg_val = h->arg_val;
+        a.arg_idx = h->arg_idx;
+        g = a;
+    }
+    if ((rc = gemm(h->p_lm, EPI_LOGITS, h->lm_head, nullptr, nullptr, c.vocab, d, h->u, out_logits)))
+        return rc;
+    AcceptArgs ac{};
+    ac.arg_val = h->arg_val;
+    ac.arg_idx = h->arg_idx;
+    ac.n_tiles = h->p_lm.n_tiles;
+    ac.sd = h->d_sd;
+    ac.acc = h->d_acc;
+    prof_begin(h, DV_K_OTHER);
+    hipError_t e = launch_accept(ac, s);
+    prof_end(h);
+    if (e != hipSuccess) return hip_fail(h, e, "accept launch");
+    return DV_OK;
+}
+
+void fill_desc(StepDesc *sd, const int32_t *tokens, const int32_t *parents, int n, int base,
+               const int32_t *pos, const int32_t *depth, const uint64_t *anc)
+{
+    std::memset(sd, 0, sizeof *sd);
+    sd->M = n;
+    sd->P = base;
+    sd->Mpad = round_up(n, 16);
+    for (int i = 0; i < n; ++i) {
+        sd->tokens[i] = tokens[i];
+        sd->parents[i] = parents[i];
+        sd->pos[i] = pos[i];
+        sd->depth[i] = depth[i];
+        sd->anc[i] = anc[i];
+    }
+}
+
+int check_kv(dv_handle *h, const dv_kv *kv)
+{
+    if (!kv || !kv->k || !kv->v) return set_err(h, DV_EINVAL, "null KV cache");
+    if (kv->capacity < 1 || kv->len < 0 || kv->len > kv->capacity)
+        return set_err(h, DV_EINVAL, "bad KV cache capacity/len (%d/%d)", kv->len, kv->capacity);
+    return DV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int dv_tree_prepare(const int32_t *parents, int32_t n, int32_t base_len, int32_t *out_pos,
+                    int32_t *out_depth, uint64_t *out_anc)
+{
+    if (!parents || !out_pos || !out_depth || !out_anc) return DV_EINVAL;
+    if (n < 1 || n > DV_MAX_TREE || base_len < 0) return DV_EINVAL;
+    if (parents[0] != -1) return DV_EINVAL;
+    for (int i = 1; i < n; ++i)
+        if (parents[i] < 0 || parents[i] >= i) return DV_EINVAL;
+    for (int i = 0; i < n; ++i) {
+        const int p = parents[i];
+        out_depth[i] = p < 0 ? 1 : out_depth[p] + 1;
+        out_anc[i] = (p < 0 ? 0ull : out_anc[p]) | (1ull << i);
+        out_pos[i] = base_len + out_depth[i] - 1;
+    }
+    return DV_OK;
+}
+
+int dv_verify_init(const dv_config *cfg, const dv_weights *w, void *stream, dv_handle **out)
+{
+    if (out) *out = nullptr;
+    if (!cfg || !w || !out) return set_err(nullptr, DV_EINVAL, "null argument");
+    const dv_config &c = *cfg;
+    if (c.n_layers < 1 || c.d_model < 32 || c.n_heads < 1 || c.d_ffn < 16 || c.vocab < 32)
+        return set_err(nullptr, DV_EINVAL, "bad model shape");
+    if (c.head_dim != 64 && c.head_dim != 128)
+        return set_err(nullptr, DV_EINVAL, "head_dim must be 64 or 128");
+    if ((long)c.n_heads * c.head_dim != c.d_model)
+        return set_err(nullptr, DV_EINVAL, "n_heads * head_dim must equal d_model");
+    if (c.d_model % 32 || c.vocab % 32 || c.d_ffn % 16)
+        return set_err(nullptr, DV_EINVAL, "d_model and vocab must be multiples of 32, d_ffn of 16");
+    if (c.weight_dtype != DV_F32 && c.weight_dtype != DV_BF16)
+        return set_err(nullptr, DV_EINVAL, "weight_dtype must be DV_F32 or DV_BF16");
+    if (c.max_tree < 1 || c.max_tree > DV_MAX_TREE)
+        return set_err(nullptr, DV_EINVAL, "max_tree must be in [1, 64]");
+    if (c.max_ctx < c.max_tree) return set_err(nullptr, DV_EINVAL, "max_ctx < max_tree");
+    if (!(c.rms_eps >= 0.f) || !std::isfinite(c.rms_eps) || !(c.rope_base > 0.f))
+        return set_err(nullptr, DV_EINVAL, "bad rms_eps or rope_base");
+    if (!w->embed || !w->final_norm || !w->lm_head || !w->attn_norm || !w->wq || !w->wk ||
+        !w->wv || !w->wo || !w->ffn_norm || !w->w_gate || !w->w_up || !w->w_down)
+        return set_err(nullptr, DV_EINVAL, "null weight pointer table");
+    for (int l = 0; l < c.n_layers; ++l)
+        if (!w->attn_norm[l] || !w->wq[l] || !w->wk[l] || !w->wv[l] || !w->wo[l] ||
+            !w->ffn_norm[l] || !w->w_gate[l] || !w->w_up[l] || !w->w_down[l])
+            return set_err(nullptr, DV_EINVAL, "null weight pointer in layer %d", l);
+
+    dv_handle *h = new dv_handle;
+    h->cfg = c;
+    h->stream = (hipStream_t)stream;
+    h->bf16 = c.weight_dtype == DV_BF16;
+    h->esz = h->bf16 ? 2 : 4;
+    h->embed = w->embed;
+    h->final_norm = w->final_norm;
+    h->lm_head = w->lm_head;
+    h->layers.resize(c.n_layers);
+    for (int l = 0; l < c.n_layers; ++l)
+        h->layers[l] = LayerW{w->attn_norm[l], w->wq[l], w->wk[l], w->wv[l], w->wo[l],
+                              w->ffn_norm[l], w->w_gate[l], w->w_up[l], w->w_down[l]};
+
+    const int d = c.d_model, F = c.d_ffn, H = c.n_heads, hd = c.head_dim, V = c.vocab;
+    const int mf = h->bf16;
+    h->p_qkv = make_plan(3 * d / DV_GEMM_TILE, d, mf ? 32 : 8, mf);
+    h->p_o = make_plan(d / DV_GEMM_TILE, d, mf ? 32 : 8, mf);
+    h->p_gu = make_plan(F / 16, d, mf ? 32 : 8, mf);
+    const int mf_down = mf && (F % 32 == 0);
+    h->p_down = make_plan(d / DV_GEMM_TILE, F, mf_down ? 32 : 8, mf_down);
+    h->p_lm = make_plan(V / DV_GEMM_TILE, d, mf ? 32 : 8, mf);
+
+    size_t part_elems = 0, max_tiles = 0;
+    for (const GemmPlan *p : {&h->p_qkv, &h->p_o, &h->p_gu, &h->p_down, &h->p_lm}) {
+        part_elems = std::max(part_elems, (size_t)p->ks * p->n_tiles * DV_TREE_MAX * DV_GEMM_TILE);
+        max_tiles = std::max(max_tiles, (size_t)p->n_tiles);
+    }
+    h->attn_split_max = std::max(1, ceil_div(1024, H));
+
+    auto dalloc = [&](void **p, size_t bytes) -> bool {
+        if (hipMalloc(p, bytes) != hipSuccess) return false;
+        return hipMemset(*p, 0, bytes) == hipSuccess;
+    };
+    const size_t rows = DV_TREE_MAX;
+    bool ok = dalloc((void **)&h->x, rows * d * 4) && dalloc((void **)&h->u, rows * d * 4) &&
+              dalloc((void **)&h->q, rows * d * 4) && dalloc((void **)&h->attn, rows * d * 4) &&
+              dalloc((void **)&h->hbuf, rows * F * 4) &&
+              dalloc((void **)&h->part_o, (size_t)H * h->attn_split_max * rows * hd * 4) &&
+              dalloc((void **)&h->part_m, (size_t)H * h->attn_split_max * rows * 4) &&
+              dalloc((void **)&h->part_l, (size_t)H * h->attn_split_max * rows * 4) &&
+              dalloc((void **)&h->part_gemm, part_elems * 4) &&
+              dalloc((void **)&h->counters, max_tiles * 4) &&
+              dalloc((void **)&h->arg_val, (size_t)h->p_lm.n_tiles * rows * 4) &&
+              dalloc((void **)&h->arg_idx, (size_t)h->p_lm.n_tiles * rows * 4) &&
+              dalloc((void **)&h->rope_cos, (size_t)c.max_ctx * (hd / 2) * 4) &&
+              dalloc((void **)&h->rope_sin, (size_t)c.max_ctx * (hd / 2) * 4) &&
+              dalloc((void **)&h->d_sd, sizeof(StepDesc)) &&
+              dalloc((void **)&h->d_acc, sizeof(DevAccept));
+    ok = ok && hipHostMalloc((void **)&h->h_sd, sizeof(StepDesc), hipHostMallocDefault) == hipSuccess &&
+         hipHostMalloc((void **)&h->h_acc, sizeof(DevAccept), hipHostMallocDefault) == hipSuccess;
+    if (!ok) {
+        std::string msg = std::string("workspace allocation failed: ") + hipGetErrorString(hipGetLastError());
+        dv_verify_free(h);
+        return set_err(nullptr, DV_ENOMEM, "%s", msg.c_str());
+    }
+
+    // rotary table: angle pos * base^(-2j/hd) in double, stored fp32
+    {
+        const int half = hd / 2;
+        std::vector<float> cs((size_t)c.max_ctx * half), sn((size_t)c.max_ctx * half);
+        for (int j = 0; j < half; ++j) {
+            const double theta = std::pow((double)c.rope_base, -2.0 * j / hd);
+            for (int p = 0; p < c.max_ctx; ++p) {
+                const double ang = (double)p * theta;
+                cs[(size_t)p * half + j] = (float)std::cos(ang);
+                sn[(size_t)p * half + j] = (float)std::sin(ang);
+            }
+        }
+        if (hipMemcpy(h->rope_cos, cs.data(), cs.size() * 4, hipMemcpyHostToDevice) != hipSuccess ||
+            hipMemcpy(h->rope_sin, sn.data(), sn.size() * 4, hipMemcpyHostToDevice) != hipSuccess) {
+            dv_verify_free(h);
+            return set_err(nullptr, DV_EHIP, "rope table upload failed");
+        }
+    }
+    if (hipDeviceSynchronize() != hipSuccess) {
+        dv_verify_free(h);
+        return set_err(nullptr, DV_EHIP, "device synchronisation after init failed");
+    }
+    *out = h;
+    return DV_OK;
+}
+
+int dv_verify_step(dv_handle *h, const int32_t *tokens, const int32_t *tree_parents, int32_t n_tree,
+                   dv_kv *kv, float *out_logits, dv_accept *out_accept)
+{
+    if (!h) return set_err(nullptr, DV_EINVAL, "null handle");
+    if (h->poisoned) return DV_EHIP;
+    if (!tokens || !tree_parents || !out_accept) return set_err(h, DV_EINVAL, "null argument");
+    int rc = check_kv(h, kv);
+    if (rc) return rc;
+    if (n_tree < 1 || n_tree > h->cfg.max_tree)
+        return set_err(h, DV_EINVAL, "n_tree %d outside [1, %d]", n_tree, h->cfg.max_tree);
+    for (int i = 0; i < n_tree; ++i)
+        if (tokens[i] < 0 || tokens[i] >= h->cfg.vocab)
+            return set_err(h, DV_EINVAL, "token id %d at node %d outside [0, %d)", tokens[i], i, h->cfg.vocab);
+    int32_t pos[DV_MAX_TREE], depth[DV_MAX_TREE];
+    uint64_t anc[DV_MAX_TREE];
+    if ((rc = check_tree(h, tree_parents, n_tree, kv->len, pos, depth, anc))) return rc;
+    if ((long)kv->len + n_tree > kv->capacity || (long)kv->len + n_tree > h->cfg.max_ctx)
+        return set_err(h, DV_ECAPACITY, "len %d + n_tree %d exceeds capacity %d / max_ctx %d",
+                       kv->len, n_tree, kv->capacity, h->cfg.max_ctx);
+
+    fill_desc(h->h_sd, tokens, tree_parents, n_tree, kv->len, pos, depth, anc);
+    if ((rc = enqueue_forward(h, kv, out_logits, true))) return rc;
+    HIPCHK(h, hipMemcpyAsync(h->h_acc, h->d_acc, sizeof(DevAccept), hipMemcpyDeviceToHost, h->stream));
+    HIPCHK(h, hipStreamSynchronize(h->stream));
+    prof_collect(h);
+
+    const DevAccept &a = *h->h_acc;
+    std::memset(out_accept, 0, sizeof *out_accept);
+    out_accept->accept_len = a.accept_len;
+    out_accept->bonus_token = a.bonus;
+    out_accept->n_tree = n_tree;
+    out_accept->base_len = kv->len;
+    for (int i = 0; i < a.accept_len && i < DV_MAX_TREE; ++i) out_accept->path[i] = a.path[i];
+    for (int i = 0; i < n_tree; ++i) out_accept->argmax[i] = a.argmax[i];
+
+    h->pending = true;
+    h->pend_n = n_tree;
+    h->pend_base = kv->len;
+    h->pend_k = kv->k;
+    h->pend_v = kv->v;
+    std::memcpy(h->pend_parents, tree_parents, n_tree * sizeof(int32_t));
+    return DV_OK;
+}
+
+int dv_kv_commit(dv_handle *h, dv_kv *kv, const dv_accept *acc)
+{
+    if (!h) return set_err(nullptr, DV_EINVAL, "null handle");
+    if (h->poisoned) return DV_EHIP;
+    if (!acc) return set_err(h, DV_EINVAL, "null accept struct");
+    int rc = check_kv(h, kv);
+    if (rc) return rc;
+    if (!h->pending) return set_err(h, DV_ESTATE, "no pending verification step to commit");
+    if (acc->n_tree != h->pend_n || acc->base_len != h->pend_base || kv->len != h->pend_base ||
+        kv->k != h->pend_k || kv->v != h->pend_v)
+        return set_err(h, DV_ESTATE, "accept struct or cache does not match the pending step");
+    const int n = acc->accept_len;
+    if (n < 1 || n > h->pend_n) return set_err(h, DV_EINVAL, "accept_len %d outside [1, %d]", n, h->pend_n);
+    if (acc->path[0] != 0) return set_err(h, DV_EINVAL, "path must start at the root");
+    bool identity = true;
+    for (int k = 1; k < n; ++k) {
+        const int node = acc->path[k];
+        if (node <= acc->path[k - 1] || node >= h->pend_n || h->pend_parents[node] != acc->path[k - 1])
+            return set_err(h, DV_EINVAL, "path is not a root-to-node chain of the pending tree");
+        if (node != k) identity = false;
+    }
+    if (!identity) {
+        CommitArgs ca{};
+        ca.kc = kv->k;
+        ca.vc = kv->v;
+        ca.LH = h->cfg.n_layers * h->cfg.n_heads;
+        ca.cap = kv->capacity;
+        ca.hd = h->cfg.head_dim;
+        ca.P = kv->len;
+        ca.n = n;
+        for (int k = 0; k < n; ++k) ca.path[k] = acc->path[k];
+        hipError_t e = launch_kv_commit(ca, h->bf16, h->stream);
+        if (e != hipSuccess) return hip_fail(h, e, "kv commit launch");
+    }
+    kv->len += n;
+    h->pending = false;
+    return DV_OK;
+}
+
+int dv_prefill(dv_handle *h, const int32_t *tokens, int32_t n, dv_kv *kv, int32_t *out_next_token)
+{
+    if (!h) return set_err(nullptr, DV_EINVAL, "null handle");
+    if (h->poisoned) return DV_EHIP;
+    if (!tokens || n < 1) return set_err(h, DV_EINVAL, "empty prompt");
+    int rc = check_kv(h, kv);
+    if (rc) return rc;
+    for (int i = 0; i < n; ++i)
+        if (tokens[i] < 0 || tokens[i] >= h->cfg.vocab)
+            return set_err(h, DV_EINVAL, "token id %d at %d outside [0, %d)", tokens[i], i, h->cfg.vocab);
+    if ((long)kv->len + n > kv->capacity || (long)kv->len + n > h->cfg.max_ctx)
+        return set_err(h, DV_ECAPACITY, "prompt of %d does not fit (len %d, capacity %d, max_ctx %d)",
+                       n, kv->len, kv->capacity, h->cfg.max_ctx);
+    const int chunk = h->cfg.max_tree;
+    int32_t parents[DV_MAX_TREE], pos[DV_MAX_TREE], depth[DV_MAX_TREE];
+    uint64_t anc[DV_MAX_TREE];
+    for (int i = 0; i < DV_MAX_TREE; ++i) parents[i] = i - 1;
+    int done = 0;
+    while (done < n) {
+        const int c = std::min(chunk, n - done);
+        const bool last = done + c == n;
+        if ((rc = check_tree(h, parents, c, kv->len, pos, depth, anc))) return rc;
+        fill_desc(h->h_sd, tokens + done, parents, c, kv->len, pos, depth, anc);
+        if ((rc = enqueue_forward(h, kv, nullptr, last))) return rc;
+        if (last) HIPCHK(h, hipMemcpyAsync(h->h_acc, h->d_acc, sizeof(DevAccept), hipMemcpyDeviceToHost, h->stream));
+        // the staging descriptor is reused by the next chunk
+        HIPCHK(h, hipStreamSynchronize(h->stream));
+        prof_collect(h);
+        kv->len += c;  // a chain's nodes already sit at slots len + k
+        done += c;
+        if (last && out_next_token) *out_next_token = h->h_acc->argmax[c - 1];
+    }
+    h->pending = false;
+    return DV_OK;
+}
+
+void dv_verify_free(dv_handle *h)
+{
+    if (!h) return;
+    if (h->stream) (void)hipStreamSynchronize(h->stream);
+    else (void)hipDeviceSynchronize();
+    for (void *p : {(void *)h->x, (void *)h->u, (void *)h->q, (void *)h->attn, (void *)h->hbuf,
+                    (void *)h->part_o, (void *)h->part_m, (void *)h->part_l, (void *)h->part_gemm,
+                    (void *)h->counters, (void *)h->arg_val, (void *)h->arg_idx, (void *)h->rope_cos,
+                    (void *)h->rope_sin, (void *)h->d_sd, (void *)h->d_acc})
+        if (p) (void)hipFree(p);
+    if (h->h_sd) (void)hipHostFree(h->h_sd);
+    if (h->h_acc) (void)hipHostFree(h->h_acc);
+    for (auto &e : h->ev_live) { (void)hipEventDestroy(e.a); (void)hipEventDestroy(e.b); }
+    for (auto e : h->ev_pool) (void)hipEventDestroy(e);
+    delete h;
+}
+
+const char *dv_last_error(const dv_handle *h)
+{
+    return h ? h->err.c_str() : g_init_error.c_str();
+}
+
+int dv_profile_enable(dv_handle *h, int32_t class_mask)
+{
+    if (!h) return set_err(nullptr, DV_EINVAL, "null handle");
+    if (class_mask < 0 || class_mask >= (1 << DV_K_COUNT))
+        return set_err(h, DV_EINVAL, "bad kernel class mask %d", class_mask);
+    h->prof = class_mask;
+    return DV_OK;
+}
+
+int dv_profile_read(dv_handle *h, int32_t cls, double *total_ms, int64_t *launches, int32_t reset)
+{
+    if (!h) return set_err(nullptr, DV_EINVAL, "null handle");
+    if (cls < 0 || cls >= DV_K_COUNT) return set_err(h, DV_EINVAL, "bad kernel class %d", cls);
+    if (total_ms) *total_ms = h->prof_ms[cls];
+    if (launches) *launches = h->prof_n[cls];
+    if (reset) {
+        h->prof_ms[cls] = 0;
+        h->prof_n[cls] = 0;
+    }
+    return DV_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,99 @@
+// Internal interface between the host engine (dv_engine.cpp) and the HIP
+// kernels (dv_kernels.hip).  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+#include <stdint.h>
+
+#define DV_TREE_MAX 64
+#define DV_GEMM_TILE 32     // logical output rows per workgroup tile
+#define DV_ATTN_TILE 32     // keys per attention LDS tile
+
+// Per-step description of the draft tree, uploaded once per step.
+struct StepDesc {
+    int32_t M;        // tree nodes
+    int32_t P;        // committed length before the step
+    int32_t Mpad;     // M rounded up to 16
+    int32_t pad0;
+    int32_t tokens[DV_TREE_MAX];
+    int32_t parents[DV_TREE_MAX];
+    int32_t pos[DV_TREE_MAX];
+    int32_t depth[DV_TREE_MAX];
+    uint64_t anc[DV_TREE_MAX];  // bit j set: node j is on node i's root path
+};
+
+// Result written by the acceptance kernel, copied back to the host.
+struct DevAccept {
+    int32_t accept_len;
+    int32_t bonus;
+    int32_t path[DV_TREE_MAX];
+    int32_t argmax[DV_TREE_MAX];
+};
+
+enum GemmEpi { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LOGITS = 3 };
+
+struct GemmArgs {
+    const void *w0, *w1, *w2;  // QKV: wq, wk, wv; SWIGLU: w_gate, w_up; else w0
+    int32_t N;                 // rows of one matrix (d_model, d_ffn or vocab)
+    int32_t K;                 // reduction length (row length of the matrices)
+    int32_t n_tiles;           // tiles of DV_GEMM_TILE logical rows
+    int32_t ks;                // split-K factor (workgroups per tile)
+    int32_t k_per_split;       // reduction elements per split (multiple of 32)
+    const float *x;            // activations [Mpad][K], rows >= M are zero
+    int32_t M, Mpad;
+    float *out;                // QKV: q [Mpad][d]; RESID: x [.][N]; SWIGLU: h [Mpad][N];
+                               // LOGITS: logits [M][N] or null
+    void *kc, *vc;             // QKV: this layer's K/V cache [H][cap][hd]
+    int32_t cap, P, hd;
+    const float *rope_cos, *rope_sin;  // [max_ctx][hd/2]
+    const int32_t *pos;        // QKV: device StepDesc.pos
+    float *part;               // split-K partial tiles [ks][n_tiles][Mpad][32]
+    int32_t *counters;         // [n_tiles], zero between launches
+    float *arg_val;            // LOGITS: per-tile max  [n_tiles][64]
+    int32_t *arg_idx;          // LOGITS: per-tile argmax [n_tiles][64]
+};
+
+struct NormArgs {
+    const float *x;            // [Mpad][d] residual stream (ignored when gathering)
+    float *x_out;              // gather mode: x written here
+    const void *embed;         // gather mode: embedding table, else null
+    const void *gain;          // [d] weight dtype
+    float *u;                  // [Mpad][d] output
+    int32_t d;
+    float eps;
+    int32_t M;
+    const int32_t *tokens;     // device: StepDesc.tokens
+};
+
+struct AttnArgs {
+    const float *q;            // [Mpad][H*hd] rotated queries
+    const void *kc, *vc;       // layer cache [H][cap][hd]
+    int32_t cap, hd, H;
+    int32_t keys_per_split, n_split;
+    const StepDesc *sd;
+    float *part_o;             // [H][n_split][64][hd]
+    float *part_m, *part_l;    // [H][n_split][64]
+    float *out;                // merge: [Mpad][H*hd]
+};
+
+struct AcceptArgs {
+    const float *arg_val;
+    const int32_t *arg_idx;
+    int32_t n_tiles;
+    const StepDesc *sd;
+    DevAccept *acc;
+};
+
+struct CommitArgs {
+    void *kc, *vc;             // whole cache [L][H][cap][hd]
+    int32_t LH, cap, hd, P, n;
+    int32_t path[DV_TREE_MAX];
+};
+
+// launchers (dv_kernels.hip); each returns the launch status
+hipError_t launch_gemm(const GemmArgs &a, int epi, int weight_bf16, int use_mfma, hipStream_t s);
+hipError_t launch_rmsnorm(const NormArgs &a, int Mpad, int weight_bf16, hipStream_t s);
+hipError_t launch_attention(const AttnArgs &a, int kv_bf16, hipStream_t s);
+hipError_t launch_attn_merge(const AttnArgs &a, int Mpad, hipStream_t s);
+hipError_t launch_accept(const AcceptArgs &a, hipStream_t s);
+hipError_t launch_kv_commit(const CommitArgs &a, int kv_bf16, hipStream_t s);

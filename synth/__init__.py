@@ -133,11 +133,12 @@ class Workload:
     chain: bool = False  # tree is a chain of n_tree tokens
     prefill: bool = False  # KV built by prefilling uniform-random prompt ids
     seed_base: int = 0
+    weight_seed: int = 0  # shared by every workload of one model
 
     @property
     def seeds(self):
         b = self.seed_base
-        return dict(weights=1 + b, prompt=2 + b, tree=3 + b, kv=4 + b)
+        return dict(weights=self.weight_seed or 1 + b, prompt=2 + b, tree=3 + b, kv=4 + b)
 
 
 TINY = ModelCfg(n_layers=2, d_model=256, n_heads=4, head_dim=64, d_ffn=688, vocab=1024,
@@ -151,18 +152,19 @@ WORKLOADS = {
     "tiny-f32-chain4": Workload("tiny-f32-chain4", TINY, context=64, n_tree=4, depth=4,
                                 chain=True, prefill=True, seed_base=100),
     "llama7b-bf16-m8-ctx512": Workload("llama7b-bf16-m8-ctx512", LLAMA7B, context=512,
-                                       n_tree=8, depth=5, seed_base=200),
+                                       n_tree=8, depth=5, seed_base=200, weight_seed=201),
     "llama13b-bf16-m16-ctx1024": Workload("llama13b-bf16-m16-ctx1024", LLAMA13B,
-                                          context=1024, n_tree=16, depth=6, seed_base=300),
+                                          context=1024, n_tree=16, depth=6, seed_base=300,
+                                          weight_seed=301),
     "llama13b-bf16-ctx8192": Workload("llama13b-bf16-ctx8192", LLAMA13B, context=8192,
-                                      n_tree=16, depth=6, seed_base=500),
+                                      n_tree=16, depth=6, seed_base=500, weight_seed=301),
 }
 SWEEP_M = (1, 2, 4, 8, 16, 32, 64)
 
 
 def sweep_workload(m: int) -> Workload:
     return Workload("llama13b-bf16-m%d-ctx1024" % m, LLAMA13B, context=1024, n_tree=m,
-                    depth=8, seed_base=400 + m)
+                    depth=8, seed_base=400 + m, weight_seed=301)
 
 
 def shrink(model: ModelCfg, **kw) -> ModelCfg:
