@@ -20,6 +20,7 @@ thread_local std::string g_init_error;
 
 struct LayerW {
     const void *attn_norm, *wq, *wk, *wv, *wo, *ffn_norm, *w_gate, *w_up, *w_down;
+    uint16_t *pk_qkv = nullptr, *pk_o = nullptr, *pk_gu = nullptr, *pk_down = nullptr;
 };
 
 struct GemmPlan {
@@ -46,13 +47,14 @@ struct dv_handle {
     float *part_o = nullptr, *part_m = nullptr, *part_l = nullptr;
     int attn_split_max = 0;
     float *part_gemm = nullptr;
-    int32_t *counters = nullptr;
     float *arg_val = nullptr;
     int32_t *arg_idx = nullptr;
     float *rope_cos = nullptr, *rope_sin = nullptr;
+    uint16_t *pk_lm = nullptr;
     StepDesc *d_sd = nullptr, *h_sd = nullptr;
     DevAccept *d_acc = nullptr, *h_acc = nullptr;
     GemmPlan p_qkv, p_o, p_gu, p_down, p_lm;
+    int n_cu = 256;
 
     // pending (uncommitted) step
     bool pending = false;
@@ -101,18 +103,33 @@ int hip_fail(dv_handle *h, hipError_t e, const char *what)
 int ceil_div(int a, int b) { return (a + b - 1) / b; }
 int round_up(int a, int b) { return ceil_div(a, b) * b; }
 
-// Split-K so that a projection launches enough workgroups to cover the
-// chip (256 CUs, ~2.5 workgroups each), with splits aligned to `align`.
-GemmPlan make_plan(int n_tiles, int K, int align, int mfma)
+// Split-K is used only for projections that add into the residual stream
+// (their partials are folded in by the next RMSNorm); it raises the number of
+// work units so that d_model-row projections still cover all CUs.
+GemmPlan make_plan(int n_tiles, int K, int align, int mfma, bool may_split, int n_cu)
 {
     GemmPlan p;
     p.n_tiles = n_tiles;
     p.mfma = mfma;
-    int ks = std::max(1, std::min(8, ceil_div(640, n_tiles)));
+    int ks = 1;
+    if (may_split) {
+        while (ks < 8 && n_tiles * ks < 2 * n_cu && K / (ks * 2) >= 4 * align) ks *= 2;
+    }
     int kps = round_up(ceil_div(K, ks), align);
     p.k_per_split = kps;
     p.ks = ceil_div(K, kps);
     return p;
+}
+
+// Resident grid for a launch: every workgroup loops over an equal share of
+// the work units.
+int gemm_grid(const GemmPlan &p, int epi, int bf16, int mt, int n_cu)
+{
+    const int units = p.n_tiles * p.ks;
+    const int cap = std::max(1, gemm_blocks_per_cu(epi, bf16, p.mfma, mt) * n_cu);
+    if (units <= cap) return units;
+    const int per = ceil_div(units, cap);
+    return ceil_div(units, per);
 }
 
 void prof_begin(dv_handle *h, int cls)
@@ -190,7 +207,6 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
     g.rope_sin = h->rope_sin;
     g.pos = h->d_sd->pos;
     g.part = h->part_gemm;
-    g.counters = h->counters;
 
     NormArgs na{};
     na.d = d;
@@ -199,7 +215,7 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
     na.tokens = h->d_sd->tokens;
     na.u = h->u;
     na.x = h->x;
-    na.x_out = h->x;
+    na.part = h->part_gemm;
 
     AttnArgs aa{};
     aa.q = h->q;
@@ -214,9 +230,11 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
     aa.part_l = h->part_l;
     aa.out = h->attn;
 
+    int pending_ks = 0;  // split-K partials of the last residual projection, not yet folded
     auto gemm = [&](const GemmPlan &p, int epi, const void *w0, const void *w1, const void *w2,
-                    int N, int K, const float *x, float *out) -> int {
+                    const uint16_t *packed, int N, int K, const float *x, float *out) -> int {
         GemmArgs a = g;
+        a.packed = packed;
         a.w0 = w0;
         a.w1 = w1;
         a.w2 = w2;
@@ -225,18 +243,23 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
         a.n_tiles = p.n_tiles;
         a.ks = p.ks;
         a.k_per_split = p.k_per_split;
+        a.n_units = p.n_tiles * p.ks;
         a.x = x;
         a.out = out;
+        const int grid = gemm_grid(p, epi, h->bf16, Mpad / 16, h->n_cu);
         prof_begin(h, DV_K_GEMM);
-        hipError_t e = launch_gemm(a, epi, h->bf16, p.mfma, s);
+        hipError_t e = launch_gemm(a, grid, epi, h->bf16, p.mfma, s);
         prof_end(h);
         if (e != hipSuccess) return hip_fail(h, e, "gemm launch");
+        if (epi == EPI_RESID) pending_ks = p.ks > 1 ? p.ks : 0;
         return DV_OK;
     };
     auto norm = [&](const void *gain, const void *embed) -> int {
         NormArgs a = na;
         a.gain = gain;
         a.embed = embed;
+        a.ks = embed ? 0 : pending_ks;
+        pending_ks = 0;
         prof_begin(h, DV_K_NORM);
         hipError_t e = launch_rmsnorm(a, Mpad, h->bf16, s);
         prof_end(h);
@@ -250,7 +273,7 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
         if ((rc = norm(w.attn_norm, l == 0 ? h->embed : nullptr))) return rc;
         g.kc = (char *)kv->k + l * layer_kv;
         g.vc = (char *)kv->v + l * layer_kv;
-        if ((rc = gemm(h->p_qkv, EPI_QKV, w.wq, w.wk, w.wv, d, d, h->u, h->q))) return rc;
+        if ((rc = gemm(h->p_qkv, EPI_QKV, w.wq, w.wk, w.wv, w.pk_qkv, d, d, h->u, h->q))) return rc;
         aa.kc = g.kc;
         aa.vc = g.vc;
         prof_begin(h, DV_K_ATTN);
@@ -258,10 +281,12 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
         if (e == hipSuccess) e = launch_attn_merge(aa, Mpad, s);
         prof_end(h);
         if (e != hipSuccess) return hip_fail(h, e, "attention launch");
-        if ((rc = gemm(h->p_o, EPI_RESID, w.wo, nullptr, nullptr, d, d, h->attn, h->x))) return rc;
+        if ((rc = gemm(h->p_o, EPI_RESID, w.wo, nullptr, nullptr, w.pk_o, d, d, h->attn, h->x))) return rc;
         if ((rc = norm(w.ffn_norm, nullptr))) return rc;
-        if ((rc = gemm(h->p_gu, EPI_SWIGLU, w.w_gate, w.w_up, nullptr, F, d, h->u, h->hbuf))) return rc;
-        if ((rc = gemm(h->p_down, EPI_RESID, w.w_down, nullptr, nullptr, d, F, h->hbuf, h->x))) return rc;
+        if ((rc = gemm(h->p_gu, EPI_SWIGLU, w.w_gate, w.w_up, nullptr, w.pk_gu, F, d, h->u, h->hbuf)))
+            return rc;
+        if ((rc = gemm(h->p_down, EPI_RESID, w.w_down, nullptr, nullptr, w.pk_down, d, F, h->hbuf, h->x)))
+            return rc;
     }
     if (!with_head) return DV_OK;
     if ((rc = norm(h->final_norm, nullptr))) return rc;
@@ -271,7 +296,8 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
         a.arg_idx = h->arg_idx;
         g = a;
     }
-    if ((rc = gemm(h->p_lm, EPI_LOGITS, h->lm_head, nullptr, nullptr, c.vocab, d, h->u, out_logits)))
+    if ((rc = gemm(h->p_lm, EPI_LOGITS, h->lm_head, nullptr, nullptr, h->pk_lm, c.vocab, d, h->u,
+                   out_logits)))
         return rc;
     AcceptArgs ac{};
     ac.arg_val = h->arg_val;
@@ -342,6 +368,7 @@ int dv_verify_init(const dv_config *cfg, const dv_weights *w, void *stream, dv_h
         return set_err(nullptr, DV_EINVAL, "head_dim must be 64 or 128");
     if ((long)c.n_heads * c.head_dim != c.d_model)
         return set_err(nullptr, DV_EINVAL, "n_heads * head_dim must equal d_model");
+    if (c.d_model > 8192) return set_err(nullptr, DV_EINVAL, "d_model above 8192");
     if (c.d_model % 32 || c.vocab % 32 || c.d_ffn % 16)
         return set_err(nullptr, DV_EINVAL, "d_model and vocab must be multiples of 32, d_ffn of 16");
     if (c.weight_dtype != DV_F32 && c.weight_dtype != DV_BF16)
@@ -359,6 +386,9 @@ int dv_verify_init(const dv_config *cfg, const dv_weights *w, void *stream, dv_h
             !w->ffn_norm[l] || !w->w_gate[l] || !w->w_up[l] || !w->w_down[l])
             return set_err(nullptr, DV_EINVAL, "null weight pointer in layer %d", l);
 
+    // weights may have been written by work still queued on another stream
+    if (hipDeviceSynchronize() != hipSuccess)
+        return set_err(nullptr, DV_EHIP, "device synchronisation before init failed");
     dv_handle *h = new dv_handle;
     h->cfg = c;
     h->stream = (hipStream_t)stream;
@@ -369,23 +399,37 @@ int dv_verify_init(const dv_config *cfg, const dv_weights *w, void *stream, dv_h
     h->lm_head = w->lm_head;
     h->layers.resize(c.n_layers);
     for (int l = 0; l < c.n_layers; ++l)
-        h->layers[l] = LayerW{w->attn_norm[l], w->wq[l], w->wk[l], w->wv[l], w->wo[l],
-                              w->ffn_norm[l], w->w_gate[l], w->w_up[l], w->w_down[l]};
+    {
+        LayerW &lw = h->layers[l];
+        lw.attn_norm = w->attn_norm[l];
+        lw.wq = w->wq[l];
+        lw.wk = w->wk[l];
+        lw.wv = w->wv[l];
+        lw.wo = w->wo[l];
+        lw.ffn_norm = w->ffn_norm[l];
+        lw.w_gate = w->w_gate[l];
+        lw.w_up = w->w_up[l];
+        lw.w_down = w->w_down[l];
+    }
 
     const int d = c.d_model, F = c.d_ffn, H = c.n_heads, hd = c.head_dim, V = c.vocab;
     const int mf = h->bf16;
-    h->p_qkv = make_plan(3 * d / DV_GEMM_TILE, d, mf ? 32 : 8, mf);
-    h->p_o = make_plan(d / DV_GEMM_TILE, d, mf ? 32 : 8, mf);
-    h->p_gu = make_plan(F / 16, d, mf ? 32 : 8, mf);
-    const int mf_down = mf && (F % 32 == 0);
-    h->p_down = make_plan(d / DV_GEMM_TILE, F, mf_down ? 32 : 8, mf_down);
-    h->p_lm = make_plan(V / DV_GEMM_TILE, d, mf ? 32 : 8, mf);
-
-    size_t part_elems = 0, max_tiles = 0;
-    for (const GemmPlan *p : {&h->p_qkv, &h->p_o, &h->p_gu, &h->p_down, &h->p_lm}) {
-        part_elems = std::max(part_elems, (size_t)p->ks * p->n_tiles * DV_TREE_MAX * DV_GEMM_TILE);
-        max_tiles = std::max(max_tiles, (size_t)p->n_tiles);
+    {
+        int dev = 0, ncu = 0;
+        if (hipGetDevice(&dev) == hipSuccess &&
+            hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+            ncu > 0)
+            h->n_cu = ncu;
     }
+    const int al = mf ? 32 : 8;
+    h->p_qkv = make_plan(3 * d / DV_GEMM_TILE, d, al, mf, false, h->n_cu);
+    h->p_o = make_plan(d / DV_GEMM_TILE, d, al, mf, true, h->n_cu);
+    h->p_gu = make_plan(F / 16, d, al, mf, false, h->n_cu);
+    const int mf_down = mf && (F % 32 == 0);
+    h->p_down = make_plan(d / DV_GEMM_TILE, F, mf_down ? 32 : 8, mf_down, true, h->n_cu);
+    h->p_lm = make_plan(V / DV_GEMM_TILE, d, al, mf, false, h->n_cu);
+
+    const size_t part_elems = (size_t)std::max(h->p_o.ks, h->p_down.ks) * DV_TREE_MAX * d;
     h->attn_split_max = std::max(1, ceil_div(1024, H));
 
     auto dalloc = [&](void **p, size_t bytes) -> bool {
@@ -400,7 +444,6 @@ int dv_verify_init(const dv_config *cfg, const dv_weights *w, void *stream, dv_h
               dalloc((void **)&h->part_m, (size_t)H * h->attn_split_max * rows * 4) &&
               dalloc((void **)&h->part_l, (size_t)H * h->attn_split_max * rows * 4) &&
               dalloc((void **)&h->part_gemm, part_elems * 4) &&
-              dalloc((void **)&h->counters, max_tiles * 4) &&
               dalloc((void **)&h->arg_val, (size_t)h->p_lm.n_tiles * rows * 4) &&
               dalloc((void **)&h->arg_idx, (size_t)h->p_lm.n_tiles * rows * 4) &&
               dalloc((void **)&h->rope_cos, (size_t)c.max_ctx * (hd / 2) * 4) &&
@@ -431,6 +474,40 @@ int dv_verify_init(const dv_config *cfg, const dv_weights *w, void *stream, dv_h
             hipMemcpy(h->rope_sin, sn.data(), sn.size() * 4, hipMemcpyHostToDevice) != hipSuccess) {
             dv_verify_free(h);
             return set_err(nullptr, DV_EHIP, "rope table upload failed");
+        }
+    }
+    // MFMA path: keep the projection matrices in tile order (one extra copy of
+    // the projection weights in HBM, written once here)
+    if (mf) {
+        auto pack = [&](const GemmPlan &p, int epi, const void *w0, const void *w1, const void *w2,
+                        int N, int K, uint16_t **dst) -> bool {
+            if (!p.mfma) return true;
+            const size_t elems = (size_t)p.n_tiles * DV_GEMM_TILE * K;
+            if (hipMalloc((void **)dst, elems * 2) != hipSuccess) return false;
+            GemmArgs a{};
+            a.w0 = w0;
+            a.w1 = w1;
+            a.w2 = w2;
+            a.N = N;
+            a.K = K;
+            a.n_tiles = p.n_tiles;
+            a.hd = hd;
+            return launch_pack(a, epi, *dst, nullptr) == hipSuccess;
+        };
+        bool okp = true;
+        for (int l = 0; l < c.n_layers && okp; ++l) {
+            LayerW &w = h->layers[l];
+            okp = pack(h->p_qkv, EPI_QKV, w.wq, w.wk, w.wv, d, d, &w.pk_qkv) &&
+                  pack(h->p_o, EPI_RESID, w.wo, nullptr, nullptr, d, d, &w.pk_o) &&
+                  pack(h->p_gu, EPI_SWIGLU, w.w_gate, w.w_up, nullptr, F, d, &w.pk_gu) &&
+                  pack(h->p_down, EPI_RESID, w.w_down, nullptr, nullptr, d, F, &w.pk_down);
+        }
+        okp = okp && pack(h->p_lm, EPI_LOGITS, h->lm_head, nullptr, nullptr, V, d, &h->pk_lm);
+        if (!okp) {
+            std::string msg = std::string("packed weight allocation failed: ") +
+                              hipGetErrorString(hipGetLastError());
+            dv_verify_free(h);
+            return set_err(nullptr, DV_ENOMEM, "%s", msg.c_str());
         }
     }
     if (hipDeviceSynchronize() != hipSuccess) {
@@ -566,10 +643,14 @@ void dv_verify_free(dv_handle *h)
     if (h->stream) (void)hipStreamSynchronize(h->stream);
     else (void)hipDeviceSynchronize();
     for (void *p : {(void *)h->x, (void *)h->u, (void *)h->q, (void *)h->attn, (void *)h->hbuf,
-                    (void *)h->part_o, (void *)h->part_m, (void *)h->part_l, (void *)h->part_gemm,
-                    (void *)h->counters, (void *)h->arg_val, (void *)h->arg_idx, (void *)h->rope_cos,
+                    (void *)h->part_o, (void *)h->part_m, (void *)h->part_l,  (void *)h->part_gemm,
+                    (void *)h->arg_val, (void *)h->arg_idx, (void *)h->rope_cos,
                     (void *)h->rope_sin, (void *)h->d_sd, (void *)h->d_acc})
         if (p) (void)hipFree(p);
+    for (auto &w : h->layers)
+        for (void *p : {(void *)w.pk_qkv, (void *)w.pk_o, (void *)w.pk_gu, (void *)w.pk_down})
+            if (p) (void)hipFree(p);
+    if (h->pk_lm) (void)hipFree(h->pk_lm);
     if (h->h_sd) (void)hipHostFree(h->h_sd);
     if (h->h_acc) (void)hipHostFree(h->h_acc);
     for (auto &e : h->ev_live) { (void)hipEventDestroy(e.a); (void)hipEventDestroy(e.b); }

@@ -34,29 +34,33 @@ enum GemmEpi { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LOGITS = 3 };
 
 struct GemmArgs {
     const void *w0, *w1, *w2;  // QKV: wq, wk, wv; SWIGLU: w_gate, w_up; else w0
+    const uint16_t *packed;    // bf16 MFMA path: the matrices in tile order (see
+                               // k_pack_tiles), read instead of w0..w2
     int32_t N;                 // rows of one matrix (d_model, d_ffn or vocab)
     int32_t K;                 // reduction length (row length of the matrices)
     int32_t n_tiles;           // tiles of DV_GEMM_TILE logical rows
-    int32_t ks;                // split-K factor (workgroups per tile)
+    int32_t ks;                // split-K factor (RESID only; partials go to `part`)
     int32_t k_per_split;       // reduction elements per split (multiple of 32)
+    int32_t n_units;           // n_tiles * ks work units, looped over by the grid
     const float *x;            // activations [Mpad][K], rows >= M are zero
     int32_t M, Mpad;
-    float *out;                // QKV: q [Mpad][d]; RESID: x [.][N]; SWIGLU: h [Mpad][N];
-                               // LOGITS: logits [M][N] or null
+    float *out;                // QKV: q [Mpad][d]; RESID (ks == 1): x [.][N];
+                               // SWIGLU: h [Mpad][N]; LOGITS: logits [M][N] or null
     void *kc, *vc;             // QKV: this layer's K/V cache [H][cap][hd]
     int32_t cap, P, hd;
     const float *rope_cos, *rope_sin;  // [max_ctx][hd/2]
     const int32_t *pos;        // QKV: device StepDesc.pos
-    float *part;               // split-K partial tiles [ks][n_tiles][Mpad][32]
-    int32_t *counters;         // [n_tiles], zero between launches
-    float *arg_val;            // LOGITS: per-tile max  [n_tiles][64]
-    int32_t *arg_idx;          // LOGITS: per-tile argmax [n_tiles][64]
+    float *part;               // RESID, ks > 1: partial sums [ks][64][N], folded
+                               // into the residual stream by the next k_rmsnorm
+    float *arg_val;            // LOGITS: per-tile max    [64][n_tiles]
+    int32_t *arg_idx;          // LOGITS: per-tile argmax [64][n_tiles]
 };
 
 struct NormArgs {
-    const float *x;            // [Mpad][d] residual stream (ignored when gathering)
-    float *x_out;              // gather mode: x written here
-    const void *embed;         // gather mode: embedding table, else null
+    float *x;                  // [Mpad][d] residual stream
+    const void *embed;         // when set: x = embedding rows of the tokens first
+    const float *part;         // when ks > 0: x += sum_s part[s][m][:] first
+    int32_t ks;
     const void *gain;          // [d] weight dtype
     float *u;                  // [Mpad][d] output
     int32_t d;
@@ -77,7 +81,7 @@ struct AttnArgs {
 };
 
 struct AcceptArgs {
-    const float *arg_val;
+    const float *arg_val;      // [64][n_tiles]
     const int32_t *arg_idx;
     int32_t n_tiles;
     const StepDesc *sd;
@@ -91,7 +95,12 @@ struct CommitArgs {
 };
 
 // launchers (dv_kernels.hip); each returns the launch status
-hipError_t launch_gemm(const GemmArgs &a, int epi, int weight_bf16, int use_mfma, hipStream_t s);
+// copy a projection's bf16 rows into MFMA tile order (init time)
+hipError_t launch_pack(const GemmArgs &a, int epi, uint16_t *dst, hipStream_t s);
+// workgroups of 256 threads one CU can hold for a GEMM variant (cached)
+int gemm_blocks_per_cu(int epi, int weight_bf16, int use_mfma, int mt);
+hipError_t launch_gemm(const GemmArgs &a, int grid, int epi, int weight_bf16, int use_mfma,
+                       hipStream_t s);
 hipError_t launch_rmsnorm(const NormArgs &a, int Mpad, int weight_bf16, hipStream_t s);
 hipError_t launch_attention(const AttnArgs &a, int kv_bf16, hipStream_t s);
 hipError_t launch_attn_merge(const AttnArgs &a, int Mpad, hipStream_t s);

@@ -18,6 +18,8 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <algorithm>
+
 #include "dv_internal.h"
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -89,51 +91,34 @@ __device__ __forceinline__ RowMap row_map(const GemmArgs &a, int epi, int t)
 }
 
 // ---------------------------------------------------------------------------
-// GEMM tail: split-K combine and epilogues on the tile in LDS
+// GEMM epilogues on the tile in LDS
 //
-// tileY[m][r] (m < Mpad, r < 32) holds this workgroup's sums.  With ks > 1
-// every workgroup stores its partial tile, and the last one to arrive (an
-// integer counter per tile) adds the ks partials in split order, so the
-// result does not depend on arrival order.
+// tileY[m][r] (m < Mpad, r < 32) holds one work unit's sums.  A tile is
+// owned by exactly one workgroup unless the projection is split over K
+// (RESID only): then each split stores its partial tile and the next
+// k_rmsnorm adds the splits into the residual stream in split order, so no
+// workgroup ever waits for another and the sum order is fixed.
 
 #define TILE_LD (DV_GEMM_TILE + 1)
 
 __device__ __forceinline__ float silu(float z) { return z / (1.0f + expf(-z)); }
 
 template <int EPI, typename KV>
-__device__ void gemm_finish(const GemmArgs &a, float (*tileY)[TILE_LD], int t, int ksl)
+__device__ void gemm_epilogue(const GemmArgs &a, float (*tileY)[TILE_LD], int t, int ksl)
 {
     const int tid = threadIdx.x;
-    const int nel = a.Mpad * DV_GEMM_TILE;
-    if (a.ks > 1) {
-        __shared__ int last;
-        float *mine = a.part + ((size_t)ksl * a.n_tiles + t) * nel;
-        for (int e = tid; e < nel; e += blockDim.x)
-            mine[e] = tileY[e / DV_GEMM_TILE][e % DV_GEMM_TILE];
-        __threadfence();
-        __syncthreads();
-        if (tid == 0) {
-            int old = __hip_atomic_fetch_add(&a.counters[t], 1, __ATOMIC_ACQ_REL,
-                                             __HIP_MEMORY_SCOPE_AGENT);
-            last = (old == a.ks - 1);
-        }
-        __syncthreads();
-        if (!last) return;
-        __threadfence();
-        for (int e = tid; e < nel; e += blockDim.x) {
-            float s = 0.f;
-            for (int k = 0; k < a.ks; ++k)
-                s += __builtin_nontemporal_load(a.part + ((size_t)k * a.n_tiles + t) * nel + e);
-            tileY[e / DV_GEMM_TILE][e % DV_GEMM_TILE] = s;
-        }
-        if (tid == 0) a.counters[t] = 0;
-        __syncthreads();
-    }
-
     if (EPI == EPI_RESID) {
-        for (int e = tid; e < a.M * DV_GEMM_TILE; e += blockDim.x) {
-            const int m = e / DV_GEMM_TILE, r = e % DV_GEMM_TILE;
-            a.out[(size_t)m * a.N + t * DV_GEMM_TILE + r] += tileY[m][r];
+        if (a.ks > 1) {
+            float *dst = a.part + (size_t)ksl * DV_TREE_MAX * a.N + t * DV_GEMM_TILE;
+            for (int e = tid; e < a.M * DV_GEMM_TILE; e += blockDim.x) {
+                const int m = e / DV_GEMM_TILE, r = e % DV_GEMM_TILE;
+                dst[(size_t)m * a.N + r] = tileY[m][r];
+            }
+        } else {
+            for (int e = tid; e < a.M * DV_GEMM_TILE; e += blockDim.x) {
+                const int m = e / DV_GEMM_TILE, r = e % DV_GEMM_TILE;
+                a.out[(size_t)m * a.N + t * DV_GEMM_TILE + r] += tileY[m][r];
+            }
         }
     } else if (EPI == EPI_SWIGLU) {
         for (int e = tid; e < a.Mpad * 16; e += blockDim.x) {
@@ -182,8 +167,8 @@ __device__ void gemm_finish(const GemmArgs &a, float (*tileY)[TILE_LD], int t, i
                 const float v = tileY[tid][r];
                 if (v > best) { best = v; bi = r; }
             }
-            a.arg_val[(size_t)t * DV_TREE_MAX + tid] = best;
-            a.arg_idx[(size_t)t * DV_TREE_MAX + tid] = t * DV_GEMM_TILE + bi;
+            a.arg_val[(size_t)tid * a.n_tiles + t] = best;
+            a.arg_idx[(size_t)tid * a.n_tiles + t] = t * DV_GEMM_TILE + bi;
         }
     }
 }
@@ -196,8 +181,11 @@ __device__ void gemm_finish(const GemmArgs &a, float (*tileY)[TILE_LD], int t, i
 // row) and B[8(l/16)..+8][l%16] (8 fp32 activations of token l%16, split
 // into bf16 hi + lo so the product keeps ~16 mantissa bits; two MFMAs per
 // operand pair).  D: lane l holds rows 4(l/16)..+4 of token l%16.
-// Four waves share a tile and take interleaved chunks of U k-steps; their
-// accumulators are summed in LDS in wave order.
+//
+// Work unit = (tile, K split).  The grid is sized to stay resident and
+// loops over units; within a unit the four waves take contiguous quarters
+// of the K range, U k-steps per batch of loads, and their accumulators are
+// summed in LDS in wave order.
 
 template <int MT> struct MfmaCfg { static constexpr int U = MT == 1 ? 8 : (MT == 2 ? 4 : 2); };
 
@@ -212,91 +200,104 @@ __device__ __forceinline__ void split_hi_lo(const float4 &a, const float4 &b, bf
     }
 }
 
+// Weight tiles in MFMA order.  For tile t, k-step s (32 columns) and half h,
+// the 16 x 32 block is stored as 1 KB in lane order: lane l's 16 bytes are
+// row row0[h] + l%16, columns 32 s + 8 (l/16) .. +8.  Blocks are ordered
+// (t, s, h), so one wave's load instruction reads 1 KB contiguous and a
+// wave walking its k range streams one contiguous region.
+
+__global__ __launch_bounds__(128) void k_pack_tiles(GemmArgs a, int epi, uint16_t *dst)
+{
+    const int t = blockIdx.x, h = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int S = a.K / 32;
+    const RowMap rm = row_map(a, epi, t);
+    const uint16_t *src = reinterpret_cast<const uint16_t *>(rm.ptr[h]) +
+                          (size_t)(rm.row0[h] + (lane & 15)) * a.K + (lane >> 4) * 8;
+    for (int s = blockIdx.y; s < S; s += gridDim.y) {
+        const uint4 v = *reinterpret_cast<const uint4 *>(src + 32 * s);
+        *reinterpret_cast<uint4 *>(dst + (((size_t)t * S + s) * 2 + h) * 512 + lane * 8) = v;
+    }
+}
+
+template <int MT, int N_STEPS>
+__device__ __forceinline__ void mfma_steps(const uint16_t *wtile, const float *const *xrow,
+                                           int k, f32x4 (&acc)[2][MT])
+{
+    u32x4 wa[N_STEPS][2];
+    float4 xa[N_STEPS][MT][2];
+#pragma unroll
+    for (int u = 0; u < N_STEPS; ++u) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+            wa[u][h] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(wtile + (2 * u + h) * 512));
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+            xa[u][mt][0] = *reinterpret_cast<const float4 *>(xrow[mt] + k + 32 * u);
+            xa[u][mt][1] = *reinterpret_cast<const float4 *>(xrow[mt] + k + 32 * u + 4);
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < N_STEPS; ++u) {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+            bf16x8 hi, lo;
+            split_hi_lo(xa[u][mt][0], xa[u][mt][1], hi, lo);
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const bf16x8 w = __builtin_bit_cast(bf16x8, wa[u][h]);
+                acc[h][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, hi, acc[h][mt], 0, 0, 0);
+                acc[h][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, lo, acc[h][mt], 0, 0, 0);
+            }
+        }
+    }
+}
+
 template <int MT, int EPI, typename KV>
 __global__ __launch_bounds__(256) void k_gemm_mfma(GemmArgs a)
 {
     constexpr int U = MfmaCfg<MT>::U;
-    const int t = blockIdx.x, ksl = blockIdx.y;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int rl = lane & 15, g = lane >> 4;
-    const int K = a.K;
-
-    const RowMap rm = row_map(a, EPI, t);
-    const uint16_t *wrow[2];
-#pragma unroll
-    for (int h = 0; h < 2; ++h)
-        wrow[h] = reinterpret_cast<const uint16_t *>(rm.ptr[h]) + (size_t)(rm.row0[h] + rl) * K + g * 8;
-    const int kb = ksl * a.k_per_split;
-    const int ke = min(K, kb + a.k_per_split);
-    const int nsteps = (ke - kb) / 32;
-    const float *xrow[MT];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) xrow[mt] = a.x + (size_t)(mt * 16 + rl) * K + g * 8;
-
-    f32x4 acc[2][MT];
-#pragma unroll
-    for (int h = 0; h < 2; ++h)
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) acc[h][mt] = (f32x4){0.f, 0.f, 0.f, 0.f};
-
-    for (int base = wave * U; base < nsteps; base += 4 * U) {
-        u32x4 wa[U][2];
-        float4 xa[U][MT][2];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int s = base + u;
-            if (s < nsteps) {
-                const int k = kb + s * 32;
-#pragma unroll
-                for (int h = 0; h < 2; ++h)
-                    wa[u][h] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(wrow[h] + k));
-#pragma unroll
-                for (int mt = 0; mt < MT; ++mt) {
-                    xa[u][mt][0] = *reinterpret_cast<const float4 *>(xrow[mt] + k);
-                    xa[u][mt][1] = *reinterpret_cast<const float4 *>(xrow[mt] + k + 4);
-                }
-            } else {
-#pragma unroll
-                for (int h = 0; h < 2; ++h) wa[u][h] = (u32x4){0u, 0u, 0u, 0u};
-#pragma unroll
-                for (int mt = 0; mt < MT; ++mt)
-                    xa[u][mt][0] = xa[u][mt][1] = make_float4(0.f, 0.f, 0.f, 0.f);
-            }
-        }
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt) {
-                bf16x8 hi, lo;
-                split_hi_lo(xa[u][mt][0], xa[u][mt][1], hi, lo);
-#pragma unroll
-                for (int h = 0; h < 2; ++h) {
-                    const bf16x8 w = __builtin_bit_cast(bf16x8, wa[u][h]);
-                    acc[h][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, hi, acc[h][mt], 0, 0, 0);
-                    acc[h][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, lo, acc[h][mt], 0, 0, 0);
-                }
-            }
-        }
-    }
-
-    // combine the four waves in wave order
+    const int K = a.K, S = K / 32;
     __shared__ float red[4][2][MT][4][64];
     __shared__ float tileY[DV_TREE_MAX][TILE_LD];
+
+    for (int unit = blockIdx.x; unit < a.n_units; unit += gridDim.x) {
+        const int t = unit / a.ks, ksl = unit - t * a.ks;
+        const float *xrow[MT];
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+        for (int mt = 0; mt < MT; ++mt) xrow[mt] = a.x + (size_t)(mt * 16 + rl) * K + g * 8;
+        const int kb = ksl * a.k_per_split;
+        const int nsteps = (min(K, kb + a.k_per_split) - kb) / 32;
+        const int s0 = (wave * nsteps) >> 2, s1 = ((wave + 1) * nsteps) >> 2;
+        const uint16_t *wt = a.packed + ((size_t)t * S + kb / 32) * 1024 + lane * 8;
+
+        f32x4 acc[2][MT];
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
+        for (int h = 0; h < 2; ++h)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) red[wave][h][mt][j][lane] = acc[h][mt][j];
-    __syncthreads();
-    for (int e = threadIdx.x; e < 2 * MT * 4 * 64; e += 256) {
-        const int l = e & 63, j = (e >> 6) & 3, mt = (e >> 8) % MT, h = (e >> 8) / MT;
-        const float s = ((red[0][h][mt][j][l] + red[1][h][mt][j][l]) + red[2][h][mt][j][l]) +
-                        red[3][h][mt][j][l];
-        tileY[mt * 16 + (l & 15)][h * 16 + 4 * (l >> 4) + j] = s;
+            for (int mt = 0; mt < MT; ++mt) acc[h][mt] = (f32x4){0.f, 0.f, 0.f, 0.f};
+        int s = s0;
+        for (; s + U <= s1; s += U) mfma_steps<MT, U>(wt + (size_t)s * 1024, xrow, kb + 32 * s, acc);
+        for (; s < s1; ++s) mfma_steps<MT, 1>(wt + (size_t)s * 1024, xrow, kb + 32 * s, acc);
+
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) red[wave][h][mt][j][lane] = acc[h][mt][j];
+        __syncthreads();
+        for (int e = threadIdx.x; e < 2 * MT * 4 * 64; e += 256) {
+            const int l = e & 63, j = (e >> 6) & 3, mt = (e >> 8) % MT, h = (e >> 8) / MT;
+            const float v = ((red[0][h][mt][j][l] + red[1][h][mt][j][l]) + red[2][h][mt][j][l]) +
+                            red[3][h][mt][j][l];
+            tileY[mt * 16 + (l & 15)][h * 16 + 4 * (l >> 4) + j] = v;
+        }
+        __syncthreads();
+        gemm_epilogue<EPI, KV>(a, tileY, t, ksl);
+        __syncthreads();
     }
-    __syncthreads();
-    gemm_finish<EPI, KV>(a, tileY, t, ksl);
 }
 
 // ---------------------------------------------------------------------------
@@ -331,74 +332,105 @@ template <> struct Load8<uint16_t> {
 template <typename W, int EPI, typename KV>
 __global__ __launch_bounds__(256) void k_gemm_valu(GemmArgs a)
 {
-    const int t = blockIdx.x, ksl = blockIdx.y;
     const int r = threadIdx.x >> 3, kl = threadIdx.x & 7;
     const int K = a.K;
-    const RowMap rm = row_map(a, EPI, t);
-    const int hsel = r >> 4;
-    const W *wrow = reinterpret_cast<const W *>(rm.ptr[hsel]) + (size_t)(rm.row0[hsel] + (r & 15)) * K;
-    const int kb = ksl * a.k_per_split;
-    const int ke = min(K, kb + a.k_per_split);
-
     __shared__ float tileY[DV_TREE_MAX][TILE_LD];
-    for (int m0 = 0; m0 < a.Mpad; m0 += 16) {
-        float acc[16];
+    for (int unit = blockIdx.x; unit < a.n_units; unit += gridDim.x) {
+        const int t = unit / a.ks, ksl = unit - t * a.ks;
+        const RowMap rm = row_map(a, EPI, t);
+        const int hsel = r >> 4;
+        const W *wrow = reinterpret_cast<const W *>(rm.ptr[hsel]) + (size_t)(rm.row0[hsel] + (r & 15)) * K;
+        const int kb = ksl * a.k_per_split;
+        const int ke = min(K, kb + a.k_per_split);
+        for (int m0 = 0; m0 < a.Mpad; m0 += 16) {
+            float acc[16];
 #pragma unroll
-        for (int m = 0; m < 16; ++m) acc[m] = 0.f;
-        for (int k = kb + kl * 8; k < ke; k += 64) {
-            float w[8];
-            Load8<W>::get(wrow + k, w);
+            for (int m = 0; m < 16; ++m) acc[m] = 0.f;
+            for (int k = kb + kl * 8; k < ke; k += 64) {
+                float w[8];
+                Load8<W>::get(wrow + k, w);
+#pragma unroll
+                for (int m = 0; m < 16; ++m) {
+                    float xv[8];
+                    Load8<float>::get(a.x + (size_t)(m0 + m) * K + k, xv);
+                    float s = acc[m];
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) s = fmaf(w[i], xv[i], s);
+                    acc[m] = s;
+                }
+            }
 #pragma unroll
             for (int m = 0; m < 16; ++m) {
-                float xv[8];
-                Load8<float>::get(a.x + (size_t)(m0 + m) * K + k, xv);
-                float s = acc[m];
-#pragma unroll
-                for (int i = 0; i < 8; ++i) s = fmaf(w[i], xv[i], s);
-                acc[m] = s;
+                float v = acc[m];
+                v += __shfl_xor(v, 1);
+                v += __shfl_xor(v, 2);
+                v += __shfl_xor(v, 4);
+                if (kl == 0) tileY[m0 + m][r] = v;
             }
         }
-#pragma unroll
-        for (int m = 0; m < 16; ++m) {
-            float v = acc[m];
-            v += __shfl_xor(v, 1);
-            v += __shfl_xor(v, 2);
-            v += __shfl_xor(v, 4);
-            if (kl == 0) tileY[m0 + m][r] = v;
-        }
+        __syncthreads();
+        gemm_epilogue<EPI, KV>(a, tileY, t, ksl);
+        __syncthreads();
     }
-    __syncthreads();
-    gemm_finish<EPI, KV>(a, tileY, t, ksl);
 }
 
 // ---------------------------------------------------------------------------
-// RMSNorm (optionally gathering the embedding rows first).
-// One workgroup per token row; rows in [M, Mpad) are written as zeros.
+// RMSNorm, one workgroup per token row (rows in [M, Mpad) are written as 0).
+// Before normalising, the row of the residual stream is completed: either
+// gathered from the embedding table (first layer) or incremented by the
+// split-K partial sums of the projection that produced it, in split order.
+// 256 threads x 4 consecutive floats per pass.
 
 template <typename W>
 __global__ __launch_bounds__(256) void k_rmsnorm(NormArgs a)
 {
     const int m = blockIdx.x, tid = threadIdx.x, d = a.d;
     float *urow = a.u + (size_t)m * d;
+    float *xrow = a.x + (size_t)m * d;
     if (m >= a.M) {
-        for (int i = tid; i < d; i += 256) urow[i] = 0.f;
-        if (a.embed)
-            for (int i = tid; i < d; i += 256) a.x_out[(size_t)m * d + i] = 0.f;
+        for (int i = 4 * tid; i < d; i += 1024) {
+            *reinterpret_cast<float4 *>(urow + i) = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (a.embed) *reinterpret_cast<float4 *>(xrow + i) = make_float4(0.f, 0.f, 0.f, 0.f);
+        }
         return;
     }
-    const float *xrow;
-    if (a.embed) {
-        const W *e = reinterpret_cast<const W *>(a.embed) + (size_t)a.tokens[m] * d;
-        float *xo = a.x_out + (size_t)m * d;
-        for (int i = tid; i < d; i += 256) xo[i] = Elem<W>::load(e, i);
-        xrow = xo;
-    } else {
-        xrow = a.x + (size_t)m * d;
+    constexpr int MAXV = 8;  // d <= 8 * 1024
+    float4 v[MAXV];
+    const W *e = a.embed ? reinterpret_cast<const W *>(a.embed) + (size_t)a.tokens[m] * d : nullptr;
+#pragma unroll
+    for (int c = 0; c < MAXV; ++c) {
+        const int i = 4 * tid + 1024 * c;
+        if (i < d) {
+            if (e) {
+                v[c] = make_float4(Elem<W>::load(e, i), Elem<W>::load(e, i + 1),
+                                   Elem<W>::load(e, i + 2), Elem<W>::load(e, i + 3));
+            } else {
+                v[c] = *reinterpret_cast<const float4 *>(xrow + i);
+            }
+        }
+    }
+    for (int s = 0; s < a.ks; ++s) {
+        const float *p = a.part + ((size_t)s * DV_TREE_MAX + m) * d;
+#pragma unroll
+        for (int c = 0; c < MAXV; ++c) {
+            const int i = 4 * tid + 1024 * c;
+            if (i < d) {
+                const float4 q = *reinterpret_cast<const float4 *>(p + i);
+                v[c].x += q.x; v[c].y += q.y; v[c].z += q.z; v[c].w += q.w;
+            }
+        }
     }
     float ss = 0.f;
-    for (int i = tid; i < d; i += 256) {
-        const float v = xrow[i];
-        ss = fmaf(v, v, ss);
+#pragma unroll
+    for (int c = 0; c < MAXV; ++c) {
+        const int i = 4 * tid + 1024 * c;
+        if (i < d) {
+            if (e || a.ks) *reinterpret_cast<float4 *>(xrow + i) = v[c];
+            ss = fmaf(v[c].x, v[c].x, ss);
+            ss = fmaf(v[c].y, v[c].y, ss);
+            ss = fmaf(v[c].z, v[c].z, ss);
+            ss = fmaf(v[c].w, v[c].w, ss);
+        }
     }
     for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
     __shared__ float wsum[4];
@@ -406,8 +438,19 @@ __global__ __launch_bounds__(256) void k_rmsnorm(NormArgs a)
     __syncthreads();
     const float tot = ((wsum[0] + wsum[1]) + wsum[2]) + wsum[3];
     const float rinv = 1.0f / sqrtf(tot / (float)d + a.eps);
-    const W *g = reinterpret_cast<const W *>(a.gain);
-    for (int i = tid; i < d; i += 256) urow[i] = xrow[i] * rinv * Elem<W>::load(g, i);
+    const W *gp = reinterpret_cast<const W *>(a.gain);
+#pragma unroll
+    for (int c = 0; c < MAXV; ++c) {
+        const int i = 4 * tid + 1024 * c;
+        if (i < d) {
+            float4 o;
+            o.x = v[c].x * rinv * Elem<W>::load(gp, i);
+            o.y = v[c].y * rinv * Elem<W>::load(gp, i + 1);
+            o.z = v[c].z * rinv * Elem<W>::load(gp, i + 2);
+            o.w = v[c].w * rinv * Elem<W>::load(gp, i + 3);
+            *reinterpret_cast<float4 *>(urow + i) = o;
+        }
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -550,25 +593,40 @@ __global__ void k_attn_merge(AttnArgs a)
 }
 
 // ---------------------------------------------------------------------------
-// Vocab-wide argmax (per-tile partials in tile order, strict > keeps the
-// lowest id) and the greedy acceptance walk over the tree.
+// Vocab-wide argmax and the greedy acceptance walk over the tree.
+// 16 threads per node scan the per-tile (max, argmax) partials; the (value,
+// index) pairs are combined by "larger value, then smaller index", which is
+// order-independent, so ties resolve to the lowest token id.
 
-__global__ void k_accept(AcceptArgs a)
+__device__ __forceinline__ void arg_better(float &v, int &i, float v2, int i2)
+{
+    if (v2 > v || (v2 == v && i2 < i)) { v = v2; i = i2; }
+}
+
+__global__ __launch_bounds__(1024) void k_accept(AcceptArgs a)
 {
     __shared__ int32_t amax[DV_TREE_MAX];
+    __shared__ int32_t ok[DV_TREE_MAX];
     const StepDesc *sd = a.sd;
     const int M = sd->M, tid = threadIdx.x;
-    if (tid < M) {
-        float best = a.arg_val[tid];
-        int bi = a.arg_idx[tid];
-        for (int t = 1; t < a.n_tiles; ++t) {
-            const float v = a.arg_val[(size_t)t * DV_TREE_MAX + tid];
-            if (v > best) { best = v; bi = a.arg_idx[(size_t)t * DV_TREE_MAX + tid]; }
+    const int m = tid >> 4, sub = tid & 15;
+    if (m < M) {
+        const float *val = a.arg_val + (size_t)m * a.n_tiles;
+        const int32_t *idx = a.arg_idx + (size_t)m * a.n_tiles;
+        float best = -INFINITY;
+        int bi = 0x7fffffff;
+        for (int t = sub; t < a.n_tiles; t += 16) arg_better(best, bi, val[t], idx[t]);
+#pragma unroll
+        for (int off = 8; off > 0; off >>= 1) {
+            const float v2 = __shfl_xor(best, off, 16);
+            const int i2 = __shfl_xor(bi, off, 16);
+            arg_better(best, bi, v2, i2);
         }
-        amax[tid] = bi;
-        a.acc->argmax[tid] = bi;
+        if (sub == 0) {
+            amax[m] = bi;
+            a.acc->argmax[m] = bi;
+        }
     }
-    __shared__ int32_t ok[DV_TREE_MAX];
     __syncthreads();
     if (tid == 0) {
         ok[0] = 1;
@@ -615,43 +673,69 @@ __global__ __launch_bounds__(256) void k_kv_commit(CommitArgs a)
 // launchers
 
 template <int EPI, typename KV>
-static hipError_t gemm_dispatch(const GemmArgs &a, int weight_bf16, int use_mfma, hipStream_t s)
+static const void *gemm_kernel(int weight_bf16, int use_mfma, int mt)
 {
-    const dim3 grid(a.n_tiles, a.ks), block(256);
     if (weight_bf16 && use_mfma) {
-        switch (a.Mpad / 16) {
-        case 1: hipLaunchKernelGGL((k_gemm_mfma<1, EPI, KV>), grid, block, 0, s, a); break;
-        case 2: hipLaunchKernelGGL((k_gemm_mfma<2, EPI, KV>), grid, block, 0, s, a); break;
-        case 3: hipLaunchKernelGGL((k_gemm_mfma<3, EPI, KV>), grid, block, 0, s, a); break;
-        case 4: hipLaunchKernelGGL((k_gemm_mfma<4, EPI, KV>), grid, block, 0, s, a); break;
-        default: return hipErrorInvalidValue;
+        switch (mt) {
+        case 1: return (const void *)k_gemm_mfma<1, EPI, KV>;
+        case 2: return (const void *)k_gemm_mfma<2, EPI, KV>;
+        case 3: return (const void *)k_gemm_mfma<3, EPI, KV>;
+        case 4: return (const void *)k_gemm_mfma<4, EPI, KV>;
+        default: return nullptr;
         }
-    } else if (weight_bf16) {
-        hipLaunchKernelGGL((k_gemm_valu<uint16_t, EPI, KV>), grid, block, 0, s, a);
-    } else {
-        hipLaunchKernelGGL((k_gemm_valu<float, EPI, KV>), grid, block, 0, s, a);
     }
-    return hipGetLastError();
+    if (weight_bf16) return (const void *)k_gemm_valu<uint16_t, EPI, KV>;
+    return (const void *)k_gemm_valu<float, EPI, KV>;
 }
 
-hipError_t launch_gemm(const GemmArgs &a, int epi, int weight_bf16, int use_mfma, hipStream_t s)
+static const void *gemm_kernel_any(int epi, int weight_bf16, int use_mfma, int mt)
 {
     if (weight_bf16) {
         switch (epi) {
-        case EPI_QKV: return gemm_dispatch<EPI_QKV, uint16_t>(a, 1, use_mfma, s);
-        case EPI_RESID: return gemm_dispatch<EPI_RESID, uint16_t>(a, 1, use_mfma, s);
-        case EPI_SWIGLU: return gemm_dispatch<EPI_SWIGLU, uint16_t>(a, 1, use_mfma, s);
-        case EPI_LOGITS: return gemm_dispatch<EPI_LOGITS, uint16_t>(a, 1, use_mfma, s);
+        case EPI_QKV: return gemm_kernel<EPI_QKV, uint16_t>(1, use_mfma, mt);
+        case EPI_RESID: return gemm_kernel<EPI_RESID, uint16_t>(1, use_mfma, mt);
+        case EPI_SWIGLU: return gemm_kernel<EPI_SWIGLU, uint16_t>(1, use_mfma, mt);
+        case EPI_LOGITS: return gemm_kernel<EPI_LOGITS, uint16_t>(1, use_mfma, mt);
         }
     } else {
         switch (epi) {
-        case EPI_QKV: return gemm_dispatch<EPI_QKV, float>(a, 0, 0, s);
-        case EPI_RESID: return gemm_dispatch<EPI_RESID, float>(a, 0, 0, s);
-        case EPI_SWIGLU: return gemm_dispatch<EPI_SWIGLU, float>(a, 0, 0, s);
-        case EPI_LOGITS: return gemm_dispatch<EPI_LOGITS, float>(a, 0, 0, s);
+        case EPI_QKV: return gemm_kernel<EPI_QKV, float>(0, 0, mt);
+        case EPI_RESID: return gemm_kernel<EPI_RESID, float>(0, 0, mt);
+        case EPI_SWIGLU: return gemm_kernel<EPI_SWIGLU, float>(0, 0, mt);
+        case EPI_LOGITS: return gemm_kernel<EPI_LOGITS, float>(0, 0, mt);
         }
     }
-    return hipErrorInvalidValue;
+    return nullptr;
+}
+
+hipError_t launch_pack(const GemmArgs &a, int epi, uint16_t *dst, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_pack_tiles, dim3(a.n_tiles, std::min(a.K / 32, 64)), dim3(128), 0, s, a, epi, dst);
+    return hipGetLastError();
+}
+
+int gemm_blocks_per_cu(int epi, int weight_bf16, int use_mfma, int mt)
+{
+    static int cache[4][2][2][5];
+    int &c = cache[epi & 3][weight_bf16 ? 1 : 0][use_mfma ? 1 : 0][(mt >= 1 && mt <= 4) ? mt : 0];
+    if (c == 0) {
+        const void *k = gemm_kernel_any(epi, weight_bf16, use_mfma, mt);
+        int n = 0;
+        if (!k || hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k, 256, 0) != hipSuccess || n < 1)
+            n = 1;
+        c = n;
+    }
+    return c;
+}
+
+hipError_t launch_gemm(const GemmArgs &a, int grid, int epi, int weight_bf16, int use_mfma,
+                       hipStream_t s)
+{
+    const void *k = gemm_kernel_any(epi, weight_bf16, use_mfma, a.Mpad / 16);
+    if (!k || grid < 1) return hipErrorInvalidValue;
+    GemmArgs arg = a;
+    void *params[] = {&arg};
+    return hipLaunchKernel(k, dim3(grid), dim3(256), params, 0, s);
 }
 
 hipError_t launch_rmsnorm(const NormArgs &a, int Mpad, int weight_bf16, hipStream_t s)
@@ -686,7 +770,7 @@ hipError_t launch_attn_merge(const AttnArgs &a, int Mpad, hipStream_t s)
 
 hipError_t launch_accept(const AcceptArgs &a, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_accept, dim3(1), dim3(64), 0, s, a);
+    hipLaunchKernelGGL(k_accept, dim3(1), dim3(1024), 0, s, a);
     return hipGetLastError();
 }
 

@@ -75,7 +75,7 @@ def _fake_weights(n_layers=2):
 
 @pytest.mark.parametrize("bad", [
     dict(head_dim=96), dict(n_heads=3), dict(d_model=250, n_heads=5, head_dim=50),
-    dict(vocab=1000), dict(d_ffn=680), dict(max_tree=65), dict(max_tree=0),
+    dict(vocab=1000), dict(d_ffn=680), dict(d_model=8448, n_heads=66, head_dim=128), dict(max_tree=65), dict(max_tree=0),
     dict(max_ctx=10), dict(weight_dtype=7), dict(rope_base=0.0), dict(rms_eps=-1.0),
     dict(n_layers=0),
 ])

@@ -63,8 +63,9 @@ def test_tiny_f32_prefill_and_chain():
 # ---------------------------------------------------------------------------
 # bf16 models that span several tiles with ragged tails
 
+# init_std 0.09 gives logits of the spread a 13B-shaped model has (std ~1.4)
 BF16 = dict(n_layers=2, d_model=256, n_heads=2, head_dim=128, d_ffn=512, vocab=2048,
-            weight_dtype="bf16", init_std=0.02)
+            weight_dtype="bf16", init_std=0.09)
 
 
 @pytest.fixture(scope="module")
@@ -85,15 +86,17 @@ def test_bf16_random_tree_parity(bf16_case, m):
     ref = _ref(om, kv_o, toks, par)
     acc, lg = case.step(kv, toks, par)
     err, near = compare_step(acc, lg, ref, 2e-2)
-    assert near <= max(2, m // 4)
+    assert near <= max(3, m // 3)
     # the tree's keys/values in slots [p, p+m): one bf16 rounding step (2^-7
-    # relative) plus the fp32 accumulation error of a length-d dot product
+    # relative) plus, in layer 0, the fp32 accumulation error of one length-d
+    # dot product; later layers also inherit the earlier layers' differences
     for l in range(case.cfg.n_layers):
         k, v = kv.layer_host(l, p + m)
         for got, want in ((k, ref["new_k"][l]), (v, ref["new_v"][l])):
             want = np.transpose(want, (1, 0, 2))
+            rms = np.sqrt(np.mean(want ** 2))
             np.testing.assert_allclose(ov.bf16_to_f64(got[:, p:]), want, rtol=2 ** -7,
-                                       atol=1e-4 * np.sqrt(np.mean(want ** 2)))
+                                       atol=(1e-4 if l == 0 else 5e-3) * rms)
 
 
 def test_bf16_empty_context_and_planted_acceptance(bf16_case):
@@ -119,7 +122,7 @@ def test_bf16_empty_context_and_planted_acceptance(bf16_case):
 
 def test_bf16_head_dim_64_parity():
     cfg = small_cfg(n_layers=2, d_model=256, n_heads=4, head_dim=64, d_ffn=528, vocab=1056,
-                    weight_dtype="bf16", init_std=0.02)
+                    weight_dtype="bf16", init_std=0.09)
     case = GpuCase(cfg, seed=81, capacity=200)
     try:
         om = case.w.oracle()
