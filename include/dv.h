@@ -93,9 +93,13 @@ typedef struct dv_weights {
     const void *const *w_down;    /* [d_model][d_ffn]            */
 } dv_weights;
 
-/* KV cache: device buffers [n_layers][n_heads][capacity][head_dim] of
- * weight_dtype; entries [0, len) are committed.  len is host state that
- * dv_kv_commit and dv_prefill advance. */
+/* KV cache: device buffers of weight_dtype, per layer and head
+ *   k: [n_layers][n_heads][capacity][head_dim]   (key-major rows)
+ *   v: [n_layers][n_heads][head_dim][capacity]   (dim-major: entry j of a
+ *      head is column j, so consecutive cache slots of one dim are adjacent)
+ * Slots [0, len) are committed.  capacity must be a positive multiple of 32
+ * (DV_EINVAL otherwise).  len is host state that dv_kv_commit and
+ * dv_prefill advance. */
 typedef struct dv_kv {
     void *k;
     void *v;

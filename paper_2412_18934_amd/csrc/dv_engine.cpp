@@ -25,6 +25,7 @@ struct LayerW {
 
 struct GemmPlan {
     int n_tiles = 0, ks = 1, k_per_split = 0, mfma = 0;
+    GemmShape shape{4, 8, 1};
 };
 
 struct ProfEv {
@@ -44,6 +45,8 @@ struct dv_handle {
 
     // workspace (device)
     float *x = nullptr, *u = nullptr, *q = nullptr, *attn = nullptr, *hbuf = nullptr;
+    float *ssq = nullptr;  // per-token sums of squares, [64][DV_NORM_SLICES]
+    uint16_t *u_s = nullptr, *attn_s = nullptr, *h_s = nullptr;  // split-layout activations
     float *part_o = nullptr, *part_m = nullptr, *part_l = nullptr;
     int attn_split_max = 0;
     float *part_gemm = nullptr;
@@ -104,17 +107,16 @@ int ceil_div(int a, int b) { return (a + b - 1) / b; }
 int round_up(int a, int b) { return ceil_div(a, b) * b; }
 
 // Split-K is used only for projections that add into the residual stream
-// (their partials are folded in by the next RMSNorm); it raises the number of
-// work units so that d_model-row projections still cover all CUs.
-GemmPlan make_plan(int n_tiles, int K, int align, int mfma, bool may_split, int n_cu)
+// (their partials are folded in by the next RMSNorm).  ks is the requested
+// split count, reduced until each split keeps at least 4 load batches of k.
+GemmPlan make_plan(int n_tiles, int K, int align, int mfma, int ks, GemmShape shape)
 {
     GemmPlan p;
     p.n_tiles = n_tiles;
     p.mfma = mfma;
-    int ks = 1;
-    if (may_split) {
-        while (ks < 8 && n_tiles * ks < 2 * n_cu && K / (ks * 2) >= 4 * align) ks *= 2;
-    }
+    p.shape = shape;
+    if (mfma && n_tiles % shape.tp) p.shape.tp = 1;
+    while (ks > 1 && K / ks < 4 * align) ks /= 2;
     int kps = round_up(ceil_div(K, ks), align);
     p.k_per_split = kps;
     p.ks = ceil_div(K, kps);
@@ -125,8 +127,8 @@ GemmPlan make_plan(int n_tiles, int K, int align, int mfma, bool may_split, int 
 // the work units.
 int gemm_grid(const GemmPlan &p, int epi, int bf16, int mt, int n_cu)
 {
-    const int units = p.n_tiles * p.ks;
-    const int cap = std::max(1, gemm_blocks_per_cu(epi, bf16, p.mfma, mt) * n_cu);
+    const int units = (p.mfma ? p.n_tiles / p.shape.tp : p.n_tiles) * p.ks;
+    const int cap = std::max(1, gemm_blocks_per_cu(epi, bf16, p.mfma, mt, p.shape) * n_cu);
     if (units <= cap) return units;
     const int per = ceil_div(units, cap);
     return ceil_div(units, per);
@@ -191,11 +193,18 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
     HIPCHK(h, hipMemcpyAsync(h->d_sd, h->h_sd, sizeof(StepDesc), hipMemcpyHostToDevice, s));
 
     const size_t layer_kv = (size_t)H * kv->capacity * hd * h->esz;
-    // attention split over the P + M keys
+    // attention: the P + M keys of each head are split evenly into
+    // tile-aligned ranges of about DV_ATTN_SPLIT_KEYS (one merge pass combines
+    // them); a context that fits one range needs no merge
     const int total = P + M;
-    const int target = std::max(1, ceil_div(1024, H));
-    const int kps = round_up(ceil_div(total, std::min(target, h->attn_split_max)), DV_ATTN_TILE);
-    const int n_split = ceil_div(total, kps);
+    int kps, n_split;
+    if (h->bf16) {
+        n_split = std::min(ceil_div(total, DV_ATTN_SPLIT_KEYS), h->attn_split_max);
+        kps = round_up(ceil_div(total, n_split), DV_ATTN_TILE);
+    } else {
+        kps = round_up(ceil_div(total, h->attn_split_max), DV_ATTN_TILE);
+    }
+    n_split = ceil_div(total, kps);
 
     GemmArgs g{};
     g.M = M;
@@ -207,15 +216,20 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
     g.rope_sin = h->rope_sin;
     g.pos = h->d_sd->pos;
     g.part = h->part_gemm;
+    g.ssq = h->ssq;
+    g.eps = c.rms_eps;
+    g.dn = d;
+    g.out_split = h->p_down.mfma ? h->h_s : nullptr;  // SWIGLU output feeds the down projection
 
     NormArgs na{};
     na.d = d;
-    na.eps = c.rms_eps;
+    na.ssq = h->ssq;
     na.M = M;
     na.tokens = h->d_sd->tokens;
     na.u = h->u;
     na.x = h->x;
     na.part = h->part_gemm;
+    na.us = h->bf16 ? h->u_s : nullptr;  // norm output feeds QKV, gate/up and lm_head
 
     AttnArgs aa{};
     aa.q = h->q;
@@ -229,12 +243,15 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
     aa.part_m = h->part_m;
     aa.part_l = h->part_l;
     aa.out = h->attn;
+    aa.out_split = h->p_o.mfma ? h->attn_s : nullptr;
 
     int pending_ks = 0;  // split-K partials of the last residual projection, not yet folded
     auto gemm = [&](const GemmPlan &p, int epi, const void *w0, const void *w1, const void *w2,
-                    const uint16_t *packed, int N, int K, const float *x, float *out) -> int {
+                    const uint16_t *packed, int N, int K, const float *x, const uint16_t *xs,
+                    float *out) -> int {
         GemmArgs a = g;
         a.packed = packed;
+        a.xs = xs;
         a.w0 = w0;
         a.w1 = w1;
         a.w2 = w2;
@@ -243,12 +260,12 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
         a.n_tiles = p.n_tiles;
         a.ks = p.ks;
         a.k_per_split = p.k_per_split;
-        a.n_units = p.n_tiles * p.ks;
+        a.n_units = (p.mfma ? p.n_tiles / p.shape.tp : p.n_tiles) * p.ks;
         a.x = x;
         a.out = out;
         const int grid = gemm_grid(p, epi, h->bf16, Mpad / 16, h->n_cu);
         prof_begin(h, DV_K_GEMM);
-        hipError_t e = launch_gemm(a, grid, epi, h->bf16, p.mfma, s);
+        hipError_t e = launch_gemm(a, grid, epi, h->bf16, p.mfma, p.shape, s);
         prof_end(h);
         if (e != hipSuccess) return hip_fail(h, e, "gemm launch");
         if (epi == EPI_RESID) pending_ks = p.ks > 1 ? p.ks : 0;
@@ -273,19 +290,24 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
         if ((rc = norm(w.attn_norm, l == 0 ? h->embed : nullptr))) return rc;
         g.kc = (char *)kv->k + l * layer_kv;
         g.vc = (char *)kv->v + l * layer_kv;
-        if ((rc = gemm(h->p_qkv, EPI_QKV, w.wq, w.wk, w.wv, w.pk_qkv, d, d, h->u, h->q))) return rc;
+        if ((rc = gemm(h->p_qkv, EPI_QKV, w.wq, w.wk, w.wv, w.pk_qkv, d, d, h->u, h->u_s, h->q)))
+            return rc;
         aa.kc = g.kc;
         aa.vc = g.vc;
         prof_begin(h, DV_K_ATTN);
         hipError_t e = launch_attention(aa, h->bf16, s);
-        if (e == hipSuccess) e = launch_attn_merge(aa, Mpad, s);
+        if (e == hipSuccess && n_split > 1) e = launch_attn_merge(aa, Mpad, s);
         prof_end(h);
         if (e != hipSuccess) return hip_fail(h, e, "attention launch");
-        if ((rc = gemm(h->p_o, EPI_RESID, w.wo, nullptr, nullptr, w.pk_o, d, d, h->attn, h->x))) return rc;
-        if ((rc = norm(w.ffn_norm, nullptr))) return rc;
-        if ((rc = gemm(h->p_gu, EPI_SWIGLU, w.w_gate, w.w_up, nullptr, w.pk_gu, F, d, h->u, h->hbuf)))
+        if ((rc = gemm(h->p_o, EPI_RESID, w.wo, nullptr, nullptr, w.pk_o, d, d, h->attn, h->attn_s,
+                       h->x)))
             return rc;
-        if ((rc = gemm(h->p_down, EPI_RESID, w.w_down, nullptr, nullptr, w.pk_down, d, F, h->hbuf, h->x)))
+        if ((rc = norm(w.ffn_norm, nullptr))) return rc;
+        if ((rc = gemm(h->p_gu, EPI_SWIGLU, w.w_gate, w.w_up, nullptr, w.pk_gu, F, d, h->u, h->u_s,
+                       h->hbuf)))
+            return rc;
+        if ((rc = gemm(h->p_down, EPI_RESID, w.w_down, nullptr, nullptr, w.pk_down, d, F, h->hbuf,
+                       h->h_s, h->x)))
             return rc;
     }
     if (!with_head) return DV_OK;
@@ -297,7 +319,7 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
         g = a;
     }
     if ((rc = gemm(h->p_lm, EPI_LOGITS, h->lm_head, nullptr, nullptr, h->pk_lm, c.vocab, d, h->u,
-                   out_logits)))
+                   h->u_s, out_logits)))
         return rc;
     AcceptArgs ac{};
     ac.arg_val = h->arg_val;
@@ -331,8 +353,9 @@ void fill_desc(StepDesc *sd, const int32_t *tokens, const int32_t *parents, int 
 int check_kv(dv_handle *h, const dv_kv *kv)
 {
     if (!kv || !kv->k || !kv->v) return set_err(h, DV_EINVAL, "null KV cache");
-    if (kv->capacity < 1 || kv->len < 0 || kv->len > kv->capacity)
-        return set_err(h, DV_EINVAL, "bad KV cache capacity/len (%d/%d)", kv->len, kv->capacity);
+    if (kv->capacity < 32 || kv->capacity % 32 || kv->len < 0 || kv->len > kv->capacity)
+        return set_err(h, DV_EINVAL, "bad KV cache capacity/len (%d/%d); capacity must be a positive multiple of 32",
+                       kv->len, kv->capacity);
     return DV_OK;
 }
 
@@ -422,15 +445,18 @@ int dv_verify_init(const dv_config *cfg, const dv_weights *w, void *stream, dv_h
             h->n_cu = ncu;
     }
     const int al = mf ? 32 : 8;
-    h->p_qkv = make_plan(3 * d / DV_GEMM_TILE, d, al, mf, false, h->n_cu);
-    h->p_o = make_plan(d / DV_GEMM_TILE, d, al, mf, true, h->n_cu);
-    h->p_gu = make_plan(F / 16, d, al, mf, false, h->n_cu);
+    // shapes and K splits measured on MI355X for the weight-streaming regime
+    // (13B-sized projections, weights read once from HBM per step)
+    const GemmShape wide8{8, 4, 2}, wide4{4, 8, 2}, narrow{4, 8, 1};
+    h->p_qkv = make_plan(3 * d / DV_GEMM_TILE, d, al, mf, 1, wide8);
+    h->p_o = make_plan(d / DV_GEMM_TILE, d, al, mf, 8, narrow);
+    h->p_gu = make_plan(F / 16, d, al, mf, 1, wide4);
     const int mf_down = mf && (F % 32 == 0);
-    h->p_down = make_plan(d / DV_GEMM_TILE, F, mf_down ? 32 : 8, mf_down, true, h->n_cu);
-    h->p_lm = make_plan(V / DV_GEMM_TILE, d, al, mf, false, h->n_cu);
+    h->p_down = make_plan(d / DV_GEMM_TILE, F, mf_down ? 32 : 8, mf_down, 8, wide4);
+    h->p_lm = make_plan(V / DV_GEMM_TILE, d, al, mf, 1, wide4);
 
     const size_t part_elems = (size_t)std::max(h->p_o.ks, h->p_down.ks) * DV_TREE_MAX * d;
-    h->attn_split_max = std::max(1, ceil_div(1024, H));
+    h->attn_split_max = std::max(ceil_div(c.max_ctx, DV_ATTN_SPLIT_KEYS), ceil_div(512, H));
 
     auto dalloc = [&](void **p, size_t bytes) -> bool {
         if (hipMalloc(p, bytes) != hipSuccess) return false;
@@ -440,6 +466,10 @@ int dv_verify_init(const dv_config *cfg, const dv_weights *w, void *stream, dv_h
     bool ok = dalloc((void **)&h->x, rows * d * 4) && dalloc((void **)&h->u, rows * d * 4) &&
               dalloc((void **)&h->q, rows * d * 4) && dalloc((void **)&h->attn, rows * d * 4) &&
               dalloc((void **)&h->hbuf, rows * F * 4) &&
+              dalloc((void **)&h->ssq, rows * DV_NORM_SLICES * 4) &&
+              dalloc((void **)&h->u_s, (size_t)d * 2 * rows * 2) &&
+              dalloc((void **)&h->attn_s, (size_t)d * 2 * rows * 2) &&
+              dalloc((void **)&h->h_s, (size_t)F * 2 * rows * 2) &&
               dalloc((void **)&h->part_o, (size_t)H * h->attn_split_max * rows * hd * 4) &&
               dalloc((void **)&h->part_m, (size_t)H * h->attn_split_max * rows * 4) &&
               dalloc((void **)&h->part_l, (size_t)H * h->attn_split_max * rows * 4) &&
@@ -643,6 +673,7 @@ void dv_verify_free(dv_handle *h)
     if (h->stream) (void)hipStreamSynchronize(h->stream);
     else (void)hipDeviceSynchronize();
     for (void *p : {(void *)h->x, (void *)h->u, (void *)h->q, (void *)h->attn, (void *)h->hbuf,
+                    (void *)h->u_s, (void *)h->attn_s, (void *)h->h_s, (void *)h->ssq,
                     (void *)h->part_o, (void *)h->part_m, (void *)h->part_l,  (void *)h->part_gemm,
                     (void *)h->arg_val, (void *)h->arg_idx, (void *)h->rope_cos,
                     (void *)h->rope_sin, (void *)h->d_sd, (void *)h->d_acc})

@@ -51,6 +51,58 @@ template <> struct Elem<uint16_t> {
 };
 
 // ---------------------------------------------------------------------------
+// split layout of activations (see dv_internal.h)
+
+__device__ __forceinline__ size_t split_index(int m, int k, int MT)
+{
+    const int s = k >> 5, g = (k >> 3) & 3, j = k & 7, mt = m >> 4, n = m & 15;
+    return (((size_t)s * MT + mt) * 2 * 64 + g * 16 + n) * 8 + j;  // hi; lo is +512
+}
+
+__device__ __forceinline__ void store_split(uint16_t *xs, int m, int k, int MT, float v)
+{
+    const size_t i = split_index(m, k, MT);
+    const float hi = __uint_as_float(__float_as_uint(v) & 0xffff0000u);
+    xs[i] = (uint16_t)(__float_as_uint(v) >> 16);
+    xs[i + 512] = f2bf(v - hi);
+}
+
+// fp32 -> bf16 hi (truncation) + lo (RNE of the remainder), 8 values
+__device__ __forceinline__ void split_hi_lo(const float4 &a, const float4 &b, bf16x8 &hi, bf16x8 &lo)
+{
+    const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const float h = __uint_as_float(__float_as_uint(v[i]) & 0xffff0000u);
+        hi[i] = (__bf16)h;
+        lo[i] = (__bf16)(v[i] - h);
+    }
+}
+
+// four consecutive columns k..k+3 (k % 4 == 0) of one token
+__device__ __forceinline__ void store_split4(uint16_t *xs, int m, int k, int MT, float4 v)
+{
+    const size_t i = split_index(m, k, MT);
+    const float f[4] = {v.x, v.y, v.z, v.w};
+    uint32_t hi[2], lo[2];
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+        uint32_t h2 = 0, l2 = 0;
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+            const float x = f[2 * p + q];
+            const float h = __uint_as_float(__float_as_uint(x) & 0xffff0000u);
+            h2 |= (__float_as_uint(x) >> 16) << (16 * q);
+            l2 |= (uint32_t)f2bf(x - h) << (16 * q);
+        }
+        hi[p] = h2;
+        lo[p] = l2;
+    }
+    *reinterpret_cast<uint2 *>(xs + i) = make_uint2(hi[0], hi[1]);
+    *reinterpret_cast<uint2 *>(xs + i + 512) = make_uint2(lo[0], lo[1]);
+}
+
+// ---------------------------------------------------------------------------
 // GEMM tile -> weight rows
 //
 // A workgroup tile has DV_GEMM_TILE = 32 logical rows made of two halves of
@@ -107,6 +159,24 @@ template <int EPI, typename KV>
 __device__ void gemm_epilogue(const GemmArgs &a, float (*tileY)[TILE_LD], int t, int ksl)
 {
     const int tid = threadIdx.x;
+    if (EPI != EPI_RESID) {
+        // 1/rms of each token (the normalisation the input skipped)
+        __shared__ float rinv[DV_TREE_MAX];
+        if (tid < a.Mpad) {
+            float r = 0.f;
+            if (tid < a.M) {
+                float sq = 0.f;
+#pragma unroll
+                for (int sl = 0; sl < DV_NORM_SLICES; ++sl) sq += a.ssq[tid * DV_NORM_SLICES + sl];
+                r = 1.0f / sqrtf(sq / (float)a.dn + a.eps);
+            }
+            rinv[tid] = r;
+        }
+        __syncthreads();
+        for (int e = tid; e < a.Mpad * DV_GEMM_TILE; e += blockDim.x)
+            tileY[e / DV_GEMM_TILE][e % DV_GEMM_TILE] *= rinv[e / DV_GEMM_TILE];
+        __syncthreads();
+    }
     if (EPI == EPI_RESID) {
         if (a.ks > 1) {
             float *dst = a.part + (size_t)ksl * DV_TREE_MAX * a.N + t * DV_GEMM_TILE;
@@ -123,7 +193,9 @@ __device__ void gemm_epilogue(const GemmArgs &a, float (*tileY)[TILE_LD], int t,
     } else if (EPI == EPI_SWIGLU) {
         for (int e = tid; e < a.Mpad * 16; e += blockDim.x) {
             const int m = e / 16, r = e % 16;
-            a.out[(size_t)m * a.N + t * 16 + r] = silu(tileY[m][r]) * tileY[m][16 + r];
+            const float hv = silu(tileY[m][r]) * tileY[m][16 + r];
+            if (a.out_split) store_split(a.out_split, m, t * 16 + r, a.Mpad >> 4, hv);
+            else a.out[(size_t)m * a.N + t * 16 + r] = hv;
         }
     } else if (EPI == EPI_QKV) {
         const int per_seg = a.N / DV_GEMM_TILE;
@@ -146,11 +218,16 @@ __device__ void gemm_epilogue(const GemmArgs &a, float (*tileY)[TILE_LD], int t,
             if (seg == 0) {
                 a.out[(size_t)m * a.N + h * a.hd + j] = y1;
                 a.out[(size_t)m * a.N + h * a.hd + j + half] = y2;
-            } else {
-                KV *c = reinterpret_cast<KV *>(seg == 1 ? a.kc : a.vc);
+            } else if (seg == 1) {  // K: [H][cap][hd]
+                KV *c = reinterpret_cast<KV *>(a.kc);
                 const size_t row = ((size_t)h * a.cap + a.P + m) * a.hd;
                 Elem<KV>::store(c, row + j, y1);
                 Elem<KV>::store(c, row + j + half, y2);
+            } else {                // V: [H][hd][cap]
+                KV *c = reinterpret_cast<KV *>(a.vc);
+                const size_t col = (size_t)h * a.hd * a.cap + a.P + m;
+                Elem<KV>::store(c, col + (size_t)j * a.cap, y1);
+                Elem<KV>::store(c, col + (size_t)(j + half) * a.cap, y2);
             }
         }
     } else {  // EPI_LOGITS
@@ -187,19 +264,6 @@ __device__ void gemm_epilogue(const GemmArgs &a, float (*tileY)[TILE_LD], int t,
 // of the K range, U k-steps per batch of loads, and their accumulators are
 // summed in LDS in wave order.
 
-template <int MT> struct MfmaCfg { static constexpr int U = MT == 1 ? 8 : (MT == 2 ? 4 : 2); };
-
-__device__ __forceinline__ void split_hi_lo(const float4 &a, const float4 &b, bf16x8 &hi, bf16x8 &lo)
-{
-    const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        const float h = __uint_as_float(__float_as_uint(v[i]) & 0xffff0000u);
-        hi[i] = (__bf16)h;
-        lo[i] = (__bf16)(v[i] - h);
-    }
-}
-
 // Weight tiles in MFMA order.  For tile t, k-step s (32 columns) and half h,
 // the 16 x 32 block is stored as 1 KB in lane order: lane l's 16 bytes are
 // row row0[h] + l%16, columns 32 s + 8 (l/16) .. +8.  Blocks are ordered
@@ -219,84 +283,106 @@ __global__ __launch_bounds__(128) void k_pack_tiles(GemmArgs a, int epi, uint16_
     }
 }
 
-template <int MT, int N_STEPS>
-__device__ __forceinline__ void mfma_steps(const uint16_t *wtile, const float *const *xrow,
-                                           int k, f32x4 (&acc)[2][MT])
+// N_STEPS k-steps for TP tiles: all weight and activation loads first, then
+// the MFMAs (TP tiles x 2 halves x MT token tiles x hi/lo).
+template <int MT, int TP, int N_STEPS>
+__device__ __forceinline__ void mfma_steps(const uint16_t *wtile, size_t tile_stride,
+                                           const uint16_t *xtile, f32x4 (&acc)[TP][2][MT])
 {
-    u32x4 wa[N_STEPS][2];
-    float4 xa[N_STEPS][MT][2];
+    u32x4 wa[N_STEPS][TP][2];
+    u32x4 xa[N_STEPS][MT][2];
 #pragma unroll
     for (int u = 0; u < N_STEPS; ++u) {
 #pragma unroll
-        for (int h = 0; h < 2; ++h)
-            wa[u][h] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(wtile + (2 * u + h) * 512));
+        for (int p = 0; p < TP; ++p)
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-            xa[u][mt][0] = *reinterpret_cast<const float4 *>(xrow[mt] + k + 32 * u);
-            xa[u][mt][1] = *reinterpret_cast<const float4 *>(xrow[mt] + k + 32 * u + 4);
-        }
+            for (int h = 0; h < 2; ++h)
+                wa[u][p][h] = *reinterpret_cast<const u32x4 *>(wtile + p * tile_stride + (2 * u + h) * 512);
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int q = 0; q < 2; ++q)
+                xa[u][mt][q] = *reinterpret_cast<const u32x4 *>(xtile + ((u * MT + mt) * 2 + q) * 512);
     }
 #pragma unroll
     for (int u = 0; u < N_STEPS; ++u) {
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
-            bf16x8 hi, lo;
-            split_hi_lo(xa[u][mt][0], xa[u][mt][1], hi, lo);
+            const bf16x8 hi = __builtin_bit_cast(bf16x8, xa[u][mt][0]);
+            const bf16x8 lo = __builtin_bit_cast(bf16x8, xa[u][mt][1]);
 #pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const bf16x8 w = __builtin_bit_cast(bf16x8, wa[u][h]);
-                acc[h][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, hi, acc[h][mt], 0, 0, 0);
-                acc[h][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, lo, acc[h][mt], 0, 0, 0);
-            }
+            for (int p = 0; p < TP; ++p)
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const bf16x8 w = __builtin_bit_cast(bf16x8, wa[u][p][h]);
+                    acc[p][h][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, hi, acc[p][h][mt], 0, 0, 0);
+                    acc[p][h][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, lo, acc[p][h][mt], 0, 0, 0);
+                }
         }
     }
 }
 
-template <int MT, int EPI, typename KV>
-__global__ __launch_bounds__(256) void k_gemm_mfma(GemmArgs a)
+// MFMA GEMM for bf16 weights (packed tiles) and split-layout activations.
+// v_mfma_f32_16x16x32_bf16: A = 16 weight rows x 32 k, B = 32 k x 16 tokens;
+// each activation is the sum of its bf16 hi and lo parts, so every product
+// keeps ~16 mantissa bits of the fp32 activation (two MFMAs per pair).
+// D: lane l holds rows 4(l/16)..+4 of token l%16.
+// Work unit = (TP consecutive tiles sharing the activation operand, K split).
+// The grid is sized to stay resident and loops over units; within a unit the
+// NW waves take contiguous shares of the k-steps, U k-steps per batch of
+// loads, and their accumulators are summed in LDS in wave order.
+
+template <int MT, int EPI, typename KV, int NW, int U, int TP>
+__global__ __launch_bounds__(64 * NW) void k_gemm_mfma(GemmArgs a)
 {
-    constexpr int U = MfmaCfg<MT>::U;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int rl = lane & 15, g = lane >> 4;
     const int K = a.K, S = K / 32;
-    __shared__ float red[4][2][MT][4][64];
+    __shared__ float red[NW][2][MT][4][64];
     __shared__ float tileY[DV_TREE_MAX][TILE_LD];
+    const int n_groups = a.n_tiles / TP;
+    const size_t tile_stride = (size_t)S * 1024;
 
-    for (int unit = blockIdx.x; unit < a.n_units; unit += gridDim.x) {
-        const int t = unit / a.ks, ksl = unit - t * a.ks;
-        const float *xrow[MT];
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) xrow[mt] = a.x + (size_t)(mt * 16 + rl) * K + g * 8;
-        const int kb = ksl * a.k_per_split;
-        const int nsteps = (min(K, kb + a.k_per_split) - kb) / 32;
-        const int s0 = (wave * nsteps) >> 2, s1 = ((wave + 1) * nsteps) >> 2;
-        const uint16_t *wt = a.packed + ((size_t)t * S + kb / 32) * 1024 + lane * 8;
+    for (int unit = blockIdx.x; unit < n_groups * a.ks; unit += gridDim.x) {
+        const int tg = unit / a.ks, ksl = unit - tg * a.ks;
+        const int sb = ksl * (a.k_per_split / 32);
+        const int nsteps = min(S - sb, a.k_per_split / 32);
+        const int s0 = sb + (wave * nsteps) / NW, s1 = sb + ((wave + 1) * nsteps) / NW;
+        const uint16_t *wt = a.packed + (size_t)(tg * TP) * tile_stride + lane * 8;
+        const uint16_t *xt = a.xs + lane * 8;
 
-        f32x4 acc[2][MT];
+        f32x4 acc[TP][2][MT];
 #pragma unroll
-        for (int h = 0; h < 2; ++h)
+        for (int p = 0; p < TP; ++p)
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt) acc[h][mt] = (f32x4){0.f, 0.f, 0.f, 0.f};
+            for (int h = 0; h < 2; ++h)
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) acc[p][h][mt] = (f32x4){0.f, 0.f, 0.f, 0.f};
         int s = s0;
-        for (; s + U <= s1; s += U) mfma_steps<MT, U>(wt + (size_t)s * 1024, xrow, kb + 32 * s, acc);
-        for (; s < s1; ++s) mfma_steps<MT, 1>(wt + (size_t)s * 1024, xrow, kb + 32 * s, acc);
+        for (; s + U <= s1; s += U)
+            mfma_steps<MT, TP, U>(wt + (size_t)s * 1024, tile_stride, xt + (size_t)s * MT * 1024, acc);
+        for (; s < s1; ++s)
+            mfma_steps<MT, TP, 1>(wt + (size_t)s * 1024, tile_stride, xt + (size_t)s * MT * 1024, acc);
 
 #pragma unroll
-        for (int h = 0; h < 2; ++h)
+        for (int p = 0; p < TP; ++p) {
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
+            for (int h = 0; h < 2; ++h)
 #pragma unroll
-                for (int j = 0; j < 4; ++j) red[wave][h][mt][j][lane] = acc[h][mt][j];
-        __syncthreads();
-        for (int e = threadIdx.x; e < 2 * MT * 4 * 64; e += 256) {
-            const int l = e & 63, j = (e >> 6) & 3, mt = (e >> 8) % MT, h = (e >> 8) / MT;
-            const float v = ((red[0][h][mt][j][l] + red[1][h][mt][j][l]) + red[2][h][mt][j][l]) +
-                            red[3][h][mt][j][l];
-            tileY[mt * 16 + (l & 15)][h * 16 + 4 * (l >> 4) + j] = v;
+                for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) red[wave][h][mt][j][lane] = acc[p][h][mt][j];
+            __syncthreads();
+            for (int e = threadIdx.x; e < 2 * MT * 4 * 64; e += 64 * NW) {
+                const int l = e & 63, j = (e >> 6) & 3, mt = (e >> 8) % MT, h = (e >> 8) / MT;
+                float v = red[0][h][mt][j][l];
+#pragma unroll
+                for (int w = 1; w < NW; ++w) v += red[w][h][mt][j][l];
+                tileY[mt * 16 + (l & 15)][h * 16 + 4 * (l >> 4) + j] = v;
+            }
+            __syncthreads();
+            gemm_epilogue<EPI, KV>(a, tileY, tg * TP + p, ksl);
+            __syncthreads();
         }
-        __syncthreads();
-        gemm_epilogue<EPI, KV>(a, tileY, t, ksl);
-        __syncthreads();
     }
 }
 
@@ -381,89 +467,311 @@ __global__ __launch_bounds__(256) void k_gemm_valu(GemmArgs a)
 // split-K partial sums of the projection that produced it, in split order.
 // 256 threads x 4 consecutive floats per pass.
 
-template <typename W>
+template <typename W, int NV, int KS>
 __global__ __launch_bounds__(256) void k_rmsnorm(NormArgs a)
 {
-    const int m = blockIdx.x, tid = threadIdx.x, d = a.d;
+    constexpr int NT = 256, SPAN = 4 * NT;
+    const int m = blockIdx.x, sl = blockIdx.y, tid = threadIdx.x, d = a.d;
+    const int c0 = sl * (d / DV_NORM_SLICES), c1 = c0 + d / DV_NORM_SLICES;
     float *urow = a.u + (size_t)m * d;
     float *xrow = a.x + (size_t)m * d;
+    const int MT = gridDim.x >> 4;  // grid.x = Mpad rows
     if (m >= a.M) {
-        for (int i = 4 * tid; i < d; i += 1024) {
-            *reinterpret_cast<float4 *>(urow + i) = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (a.embed) *reinterpret_cast<float4 *>(xrow + i) = make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int i = c0 + 4 * tid; i < c1; i += SPAN) {
+            const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (a.us) store_split4(a.us, m, i, MT, z);
+            else *reinterpret_cast<float4 *>(urow + i) = z;
+            if (a.embed) *reinterpret_cast<float4 *>(xrow + i) = z;
         }
+        if (tid == 0) a.ssq[m * DV_NORM_SLICES + sl] = 0.f;
         return;
     }
-    constexpr int MAXV = 8;  // d <= 8 * 1024
-    float4 v[MAXV];
-    const W *e = a.embed ? reinterpret_cast<const W *>(a.embed) + (size_t)a.tokens[m] * d : nullptr;
+    // NV = ceil(slice / SPAN) float4 per thread; KS = number of split-K
+    // partials to add (compile-time, so that all loads of the slice are
+    // issued together; KS < 0: a runtime count).  Addresses are clamped, not
+    // branched on: lanes past the slice end re-read its last float4 and drop it.
+    int idx[NV];
 #pragma unroll
-    for (int c = 0; c < MAXV; ++c) {
-        const int i = 4 * tid + 1024 * c;
-        if (i < d) {
-            if (e) {
-                v[c] = make_float4(Elem<W>::load(e, i), Elem<W>::load(e, i + 1),
-                                   Elem<W>::load(e, i + 2), Elem<W>::load(e, i + 3));
-            } else {
-                v[c] = *reinterpret_cast<const float4 *>(xrow + i);
-            }
-        }
+    for (int c = 0; c < NV; ++c) idx[c] = min(c0 + 4 * tid + SPAN * c, c1 - 4);
+    float4 v[NV];
+    if (a.embed) {
+        const W *e = reinterpret_cast<const W *>(a.embed) + (size_t)a.tokens[m] * d;
+#pragma unroll
+        for (int c = 0; c < NV; ++c)
+            v[c] = make_float4(Elem<W>::load(e, idx[c]), Elem<W>::load(e, idx[c] + 1),
+                               Elem<W>::load(e, idx[c] + 2), Elem<W>::load(e, idx[c] + 3));
+    } else {
+#pragma unroll
+        for (int c = 0; c < NV; ++c) v[c] = *reinterpret_cast<const float4 *>(xrow + idx[c]);
     }
-    for (int s = 0; s < a.ks; ++s) {
-        const float *p = a.part + ((size_t)s * DV_TREE_MAX + m) * d;
+    const int ks = KS >= 0 ? KS : a.ks;
+    if (KS > 0) {
+        float4 q[KS > 0 ? KS : 1][NV];
 #pragma unroll
-        for (int c = 0; c < MAXV; ++c) {
-            const int i = 4 * tid + 1024 * c;
-            if (i < d) {
-                const float4 q = *reinterpret_cast<const float4 *>(p + i);
+        for (int s = 0; s < (KS > 0 ? KS : 1); ++s)
+#pragma unroll
+            for (int c = 0; c < NV; ++c)
+                q[s][c] = *reinterpret_cast<const float4 *>(a.part + ((size_t)s * DV_TREE_MAX + m) * d + idx[c]);
+#pragma unroll
+        for (int s = 0; s < (KS > 0 ? KS : 1); ++s)
+#pragma unroll
+            for (int c = 0; c < NV; ++c) {
+                v[c].x += q[s][c].x; v[c].y += q[s][c].y; v[c].z += q[s][c].z; v[c].w += q[s][c].w;
+            }
+    } else {
+        for (int s = 0; s < ks; ++s) {
+#pragma unroll
+            for (int c = 0; c < NV; ++c) {
+                const float4 q = *reinterpret_cast<const float4 *>(a.part + ((size_t)s * DV_TREE_MAX + m) * d + idx[c]);
                 v[c].x += q.x; v[c].y += q.y; v[c].z += q.z; v[c].w += q.w;
             }
         }
     }
+    const W *gp = reinterpret_cast<const W *>(a.gain);
     float ss = 0.f;
 #pragma unroll
-    for (int c = 0; c < MAXV; ++c) {
-        const int i = 4 * tid + 1024 * c;
-        if (i < d) {
-            if (e || a.ks) *reinterpret_cast<float4 *>(xrow + i) = v[c];
+    for (int c = 0; c < NV; ++c) {
+        const int i = idx[c];
+        if (c0 + 4 * tid + SPAN * c < c1) {
+            if (a.embed || ks) *reinterpret_cast<float4 *>(xrow + i) = v[c];
             ss = fmaf(v[c].x, v[c].x, ss);
             ss = fmaf(v[c].y, v[c].y, ss);
             ss = fmaf(v[c].z, v[c].z, ss);
             ss = fmaf(v[c].w, v[c].w, ss);
+            float4 o;
+            o.x = v[c].x * Elem<W>::load(gp, i);
+            o.y = v[c].y * Elem<W>::load(gp, i + 1);
+            o.z = v[c].z * Elem<W>::load(gp, i + 2);
+            o.w = v[c].w * Elem<W>::load(gp, i + 3);
+            if (a.us) store_split4(a.us, m, i, MT, o);
+            else *reinterpret_cast<float4 *>(urow + i) = o;
         }
     }
     for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
-    __shared__ float wsum[4];
+    __shared__ float wsum[NT / 64];
     if ((tid & 63) == 0) wsum[tid >> 6] = ss;
     __syncthreads();
-    const float tot = ((wsum[0] + wsum[1]) + wsum[2]) + wsum[3];
-    const float rinv = 1.0f / sqrtf(tot / (float)d + a.eps);
-    const W *gp = reinterpret_cast<const W *>(a.gain);
+    if (tid == 0) {
+        float tot = 0.f;
 #pragma unroll
-    for (int c = 0; c < MAXV; ++c) {
-        const int i = 4 * tid + 1024 * c;
-        if (i < d) {
-            float4 o;
-            o.x = v[c].x * rinv * Elem<W>::load(gp, i);
-            o.y = v[c].y * rinv * Elem<W>::load(gp, i + 1);
-            o.z = v[c].z * rinv * Elem<W>::load(gp, i + 2);
-            o.w = v[c].w * rinv * Elem<W>::load(gp, i + 3);
-            *reinterpret_cast<float4 *>(urow + i) = o;
-        }
+        for (int w = 0; w < NT / 64; ++w) tot += wsum[w];
+        a.ssq[m * DV_NORM_SLICES + sl] = tot;
     }
 }
 
 // ---------------------------------------------------------------------------
 // Tree-masked attention, split over keys (flash-decoding style).
+//
+// Cache layouts: K [H][cap][hd] (key-major), V [H][hd][cap] (dim-major).
 // Workgroup (split s, head h) covers keys [s*kps, (s+1)*kps) of the P + M
-// cache slots; the tree's own keys were written to slots P.. by the QKV
-// epilogue.  Key j is visible to node i iff j < P or bit (j-P) of anc(i).
-// Queries are handled 16 at a time; K/V tiles of 32 keys sit in LDS as fp32;
-// an online softmax keeps (max, sum, o) per query.  Outputs per split:
-// o (unnormalised), running max and sum.
+// cache slots; the tree's own keys/values were written to slots P.. by the
+// QKV epilogue.  Key j is visible to node i iff j < P or bit (j-P) of
+// anc(i).  Each split writes its unnormalised output with the running max
+// and sum; k_attn_merge combines the splits (or, with one split, the
+// workgroup writes the normalised output itself).
 
-template <int HD, typename KV>
-__global__ __launch_bounds__(256) void k_attn(AttnArgs a)
+// bf16 cache, MFMA.  Queries are taken 16 at a time; the four waves take
+// interleaved 32-key tiles and are combined in LDS at the end.
+//   S^T = K Q^T: A = 16 keys x 32 dims (16 bytes of one key row per lane),
+//   B = Q^T (fp32 queries split into bf16 hi + lo).  Tile "a" holds keys
+//   k0 + 8(r/4) + r%4 in row r, tile "b" the same + 4, so lane l ends up with
+//   the scores of token l%16 for the 8 consecutive keys k0 + 8(l/16) .. +8.
+//   O = P V: A = P (those 8 scores per lane, exponentiated, split hi + lo),
+//   B = V^T rows: 16 bytes = the same 8 consecutive keys of one dim.
+
+template <int HD, int NW>
+__global__ __launch_bounds__(64 * NW) void k_attn_mfma(AttnArgs a)
+{
+    constexpr int NC = HD / 32;  // QK k-steps over dims
+    constexpr int ND = HD / 16;  // PV output dim tiles
+    const int split = blockIdx.x, h = blockIdx.y;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int n = lane & 15, g = lane >> 4;
+    const StepDesc *sd = a.sd;
+    const int M = sd->M, P = sd->P, total = P + M;
+    const int kbeg = split * a.keys_per_split;
+    const int kend = min(total, kbeg + a.keys_per_split);
+    const int ntile = (kend - kbeg + 31) / 32;
+    const int D = a.H * HD;
+    const float scale = 1.0f / sqrtf((float)HD);
+    const uint16_t *kc = reinterpret_cast<const uint16_t *>(a.kc) + (size_t)h * a.cap * HD;
+    const uint16_t *vc = reinterpret_cast<const uint16_t *>(a.vc) + (size_t)h * HD * a.cap;
+
+    __shared__ float sm_m[NW][16], sm_l[NW][16];
+    __shared__ float sm_o[NW][16][HD + 4];
+
+    // K rows (A operands of the two score tiles) and V^T columns of one
+    // 32-key tile for this lane
+    struct KTile {
+        u32x4 ka[NC], kb[NC];
+    };
+    auto load_k = [&](int t, KTile &T) {
+        const int k0 = kbeg + 32 * t;
+        const int ka = min(k0 + 8 * (n >> 2) + (n & 3), kend - 1);
+        const int kb = min(k0 + 8 * (n >> 2) + 4 + (n & 3), kend - 1);
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            T.ka[c] = *reinterpret_cast<const u32x4 *>(kc + (size_t)ka * HD + 32 * c + 8 * g);
+            T.kb[c] = *reinterpret_cast<const u32x4 *>(kc + (size_t)kb * HD + 32 * c + 8 * g);
+        }
+    };
+    auto load_v = [&](int t, u32x4 (&vv)[ND]) {
+        const int k0 = kbeg + 32 * t;
+#pragma unroll
+        for (int dt = 0; dt < ND; ++dt)
+            vv[dt] = *reinterpret_cast<const u32x4 *>(vc + (size_t)(dt * 16 + n) * a.cap + k0 + 8 * g);
+    };
+
+    for (int q0 = 0; q0 < M; q0 += 16) {
+        const int tok = q0 + n;
+        const bool tok_ok = tok < M;
+        KTile cur, nxt;
+        u32x4 vv[ND];
+        if (wave < ntile) load_k(wave, cur);  // in flight while q is prepared
+        const float *qrow = a.q + (size_t)min(tok, M - 1) * D + h * HD + g * 8;
+        bf16x8 qh[NC], ql[NC];
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            float4 x0 = *reinterpret_cast<const float4 *>(qrow + 32 * c);
+            float4 x1 = *reinterpret_cast<const float4 *>(qrow + 32 * c + 4);
+            if (!tok_ok) x0 = x1 = make_float4(0.f, 0.f, 0.f, 0.f);
+            split_hi_lo(x0, x1, qh[c], ql[c]);
+        }
+        const uint64_t anc = tok_ok ? sd->anc[tok] : 0ull;
+        float m_run = -INFINITY, l_run = 0.f;
+        f32x4 o[ND];
+#pragma unroll
+        for (int dt = 0; dt < ND; ++dt) o[dt] = (f32x4){0.f, 0.f, 0.f, 0.f};
+
+        for (int t = wave; t < ntile; t += NW) {
+            load_v(t, vv);                              // needed after the softmax
+            if (t + NW < ntile) load_k(t + NW, nxt);    // the wave's next tile
+            const int k0 = kbeg + 32 * t;
+            f32x4 sa = (f32x4){0.f, 0.f, 0.f, 0.f}, sb = sa;
+#pragma unroll
+            for (int c = 0; c < NC; ++c) {
+                const bf16x8 ka8 = __builtin_bit_cast(bf16x8, cur.ka[c]);
+                const bf16x8 kb8 = __builtin_bit_cast(bf16x8, cur.kb[c]);
+                sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka8, qh[c], sa, 0, 0, 0);
+                sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka8, ql[c], sa, 0, 0, 0);
+                sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb8, qh[c], sb, 0, 0, 0);
+                sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb8, ql[c], sb, 0, 0, 0);
+            }
+            float sv[8];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                sv[j] = sa[j] * scale;
+                sv[4 + j] = sb[j] * scale;
+            }
+            float mt = -INFINITY;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int key = k0 + 8 * g + i;
+                bool vis = tok_ok && key < kend;
+                if (key >= P) vis = vis && ((anc >> (key - P)) & 1ull);
+                if (!vis) sv[i] = -INFINITY;
+                mt = fmaxf(mt, sv[i]);
+            }
+            mt = fmaxf(mt, __shfl_xor(mt, 16));
+            mt = fmaxf(mt, __shfl_xor(mt, 32));
+            const float mnew = fmaxf(m_run, mt);
+            float alpha = 1.f, ps = 0.f;
+            float pv[8];
+            if (mnew == -INFINITY) {
+#pragma unroll
+                for (int i = 0; i < 8; ++i) pv[i] = 0.f;
+            } else {
+                alpha = (m_run == -INFINITY) ? 0.f : expf(m_run - mnew);
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    pv[i] = (sv[i] == -INFINITY) ? 0.f : expf(sv[i] - mnew);
+                    ps += pv[i];
+                }
+            }
+            ps += __shfl_xor(ps, 16);
+            ps += __shfl_xor(ps, 32);
+            l_run = l_run * alpha + ps;
+            m_run = mnew;
+            // O rows held by this lane are tokens 4g + j
+            float al[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) al[j] = __shfl(alpha, 4 * g + j);
+            if (k0 + 32 > kend) {
+                // ragged last tile: values of slots past the split end are dropped
+#pragma unroll
+                for (int dt = 0; dt < ND; ++dt)
+#pragma unroll
+                    for (int w = 0; w < 4; ++w) {
+                        const int key = k0 + 8 * g + 2 * w;
+                        uint32_t x = vv[dt][w];
+                        if (key >= kend) x &= 0xffff0000u;
+                        if (key + 1 >= kend) x &= 0x0000ffffu;
+                        vv[dt][w] = x;
+                    }
+            }
+            bf16x8 ph, pl;
+            split_hi_lo(make_float4(pv[0], pv[1], pv[2], pv[3]), make_float4(pv[4], pv[5], pv[6], pv[7]),
+                        ph, pl);
+#pragma unroll
+            for (int dt = 0; dt < ND; ++dt) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) o[dt][j] *= al[j];
+                const bf16x8 v8 = __builtin_bit_cast(bf16x8, vv[dt]);
+                o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph, v8, o[dt], 0, 0, 0);
+                o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pl, v8, o[dt], 0, 0, 0);
+            }
+            cur = nxt;
+        }
+
+        // combine the waves (fixed wave order)
+        if (g == 0) {
+            sm_m[wave][n] = m_run;
+            sm_l[wave][n] = l_run;
+        }
+#pragma unroll
+        for (int dt = 0; dt < ND; ++dt)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) sm_o[wave][4 * g + j][dt * 16 + n] = o[dt][j];
+        __syncthreads();
+        for (int e = threadIdx.x; e < 16 * HD; e += 64 * NW) {
+            const int i = e / HD, dd = e % HD;
+            const int ti = q0 + i;
+            float mx = -INFINITY;
+#pragma unroll
+            for (int w = 0; w < NW; ++w) mx = fmaxf(mx, sm_m[w][i]);
+            float l = 0.f, ov = 0.f;
+#pragma unroll
+            for (int w = 0; w < NW; ++w) {
+                const float mw = sm_m[w][i];
+                if (mw == -INFINITY) continue;
+                const float wgt = expf(mw - mx);
+                l = fmaf(wgt, sm_l[w][i], l);
+                ov = fmaf(wgt, sm_o[w][i][dd], ov);
+            }
+            if (a.n_split == 1) {
+                if (ti < sd->Mpad) {
+                    const float r = ti < M ? ov / l : 0.f;
+                    if (a.out_split) store_split(a.out_split, ti, h * HD + dd, sd->Mpad >> 4, r);
+                    else a.out[(size_t)ti * D + h * HD + dd] = r;
+                }
+            } else if (ti < M) {
+                const size_t pb = ((size_t)h * a.n_split + split) * DV_TREE_MAX + ti;
+                a.part_o[pb * HD + dd] = ov;
+                if (dd == 0) {
+                    a.part_m[pb] = mx;
+                    a.part_l[pb] = l;
+                }
+            }
+        }
+        __syncthreads();
+    }
+}
+
+// fp32 cache (VALU).  K/V tiles of 32 keys sit in LDS as fp32; 16 queries
+// at a time; an online softmax keeps (max, sum, o) per query.
+
+template <int HD>
+__global__ __launch_bounds__(256) void k_attn_f32(AttnArgs a)
 {
     constexpr int DPT = HD / 16;  // output dims per thread
     const int split = blockIdx.x, h = blockIdx.y, tid = threadIdx.x;
@@ -472,13 +780,13 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a)
     const int kb = split * a.keys_per_split;
     const int ke = min(total, kb + a.keys_per_split);
     const float scale = 1.0f / sqrtf((float)HD);
-    const KV *kc = reinterpret_cast<const KV *>(a.kc) + (size_t)h * a.cap * HD;
-    const KV *vc = reinterpret_cast<const KV *>(a.vc) + (size_t)h * a.cap * HD;
+    const float *kc = reinterpret_cast<const float *>(a.kc) + (size_t)h * a.cap * HD;
+    const float *vc = reinterpret_cast<const float *>(a.vc) + (size_t)h * HD * a.cap;
     const int D = a.H * HD;
 
     __shared__ float qs[16][HD];
     __shared__ float kt[DV_ATTN_TILE][HD + 1];
-    __shared__ float vt[DV_ATTN_TILE][HD];
+    __shared__ float vt[DV_ATTN_TILE][HD + 1];
     __shared__ float sc[16][DV_ATTN_TILE + 1];
     __shared__ float mrun[16], lrun[16], alph[16];
 
@@ -499,13 +807,9 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a)
             const int nk = min(DV_ATTN_TILE, ke - t0);
             for (int e = tid; e < DV_ATTN_TILE * HD; e += 256) {
                 const int j = e / HD, d = e % HD;
-                float kv = 0.f, vv = 0.f;
-                if (j < nk) {
-                    kv = Elem<KV>::load(kc, (size_t)(t0 + j) * HD + d);
-                    vv = Elem<KV>::load(vc, (size_t)(t0 + j) * HD + d);
-                }
-                kt[j][d] = kv;
-                vt[j][d] = vv;
+                kt[j][d] = j < nk ? kc[(size_t)(t0 + j) * HD + d] : 0.f;
+                const int jv = e % DV_ATTN_TILE, dv = e / DV_ATTN_TILE;
+                vt[jv][dv] = jv < nk ? vc[(size_t)dv * a.cap + t0 + jv] : 0.f;
             }
             __syncthreads();
             for (int e = tid; e < 16 * DV_ATTN_TILE; e += 256) {
@@ -532,8 +836,8 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a)
                 if (mnew != -INFINITY) {
                     al = (mold == -INFINITY) ? 0.f : expf(mold - mnew);
                     for (int j = 0; j < DV_ATTN_TILE; ++j) {
-                        const float s = sc[tid][j];
-                        const float p = (s == -INFINITY) ? 0.f : expf(s - mnew);
+                        const float sj = sc[tid][j];
+                        const float p = (sj == -INFINITY) ? 0.f : expf(sj - mnew);
                         sc[tid][j] = p;
                         sum += p;
                     }
@@ -556,40 +860,75 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a)
             }
             __syncthreads();
         }
-        const size_t pbase = ((size_t)h * a.n_split + split) * DV_TREE_MAX;
-        if (qi < nq) {
+        if (a.n_split == 1) {
+            if (q0 + qi < sd->Mpad) {
 #pragma unroll
-            for (int c = 0; c < DPT; ++c) a.part_o[(pbase + q0 + qi) * HD + dd + c] = o[c];
-        }
-        if (tid < nq) {
-            a.part_m[pbase + q0 + tid] = mrun[tid];
-            a.part_l[pbase + q0 + tid] = lrun[tid];
+                for (int c = 0; c < DPT; ++c) {
+                    const float r = qi < nq ? o[c] / lrun[qi] : 0.f;
+                    if (a.out_split) store_split(a.out_split, q0 + qi, h * HD + dd + c, sd->Mpad >> 4, r);
+                    else a.out[(size_t)(q0 + qi) * D + h * HD + dd + c] = r;
+                }
+            }
+        } else {
+            const size_t pbase = ((size_t)h * a.n_split + split) * DV_TREE_MAX;
+            if (qi < nq) {
+#pragma unroll
+                for (int c = 0; c < DPT; ++c) a.part_o[(pbase + q0 + qi) * HD + dd + c] = o[c];
+            }
+            if (tid < nq) {
+                a.part_m[pbase + q0 + tid] = mrun[tid];
+                a.part_l[pbase + q0 + tid] = lrun[tid];
+            }
         }
         __syncthreads();
     }
 }
 
 // Combine the splits of each (node, head): softmax-weighted sum of the split
-// outputs in split order.  Grid (Mpad, H), block hd threads; rows >= M are 0.
-__global__ void k_attn_merge(AttnArgs a)
+// outputs.  Splits are read 16 at a time (all loads of a chunk in flight
+// together) and folded in split order with a running maximum.  Grid (Mpad, H),
+// block hd threads; rows >= M are 0.
+__global__ __launch_bounds__(128) void k_attn_merge(AttnArgs a)
 {
+    constexpr int CH = 16;
     const int i = blockIdx.x, h = blockIdx.y, d = threadIdx.x, HD = a.hd;
-    const int M = a.sd->M;
-    float *out = a.out + (size_t)i * a.H * HD + h * HD + d;
-    if (i >= M) { *out = 0.f; return; }
-    const size_t base = (size_t)h * a.n_split * DV_TREE_MAX + i;
-    float mx = -INFINITY;
-    for (int s = 0; s < a.n_split; ++s) mx = fmaxf(mx, a.part_m[base + (size_t)s * DV_TREE_MAX]);
-    float l = 0.f, o = 0.f;
-    for (int s = 0; s < a.n_split; ++s) {
-        const size_t ps = base + (size_t)s * DV_TREE_MAX;
-        const float ms = a.part_m[ps];
-        if (ms == -INFINITY) continue;
-        const float w = expf(ms - mx);
-        l = fmaf(w, a.part_l[ps], l);
-        o = fmaf(w, a.part_o[ps * HD + d], o);
+    const int M = a.sd->M, MT = gridDim.x >> 4;
+    if (i >= M) {
+        if (a.out_split) store_split(a.out_split, i, h * HD + d, MT, 0.f);
+        else a.out[(size_t)i * a.H * HD + h * HD + d] = 0.f;
+        return;
     }
-    *out = o / l;
+    const size_t base = (size_t)h * a.n_split * DV_TREE_MAX + i;
+    float run_m = -INFINITY, l = 0.f, o = 0.f;
+    for (int s0 = 0; s0 < a.n_split; s0 += CH) {
+        float ms[CH], ls[CH], os[CH];
+#pragma unroll
+        for (int c = 0; c < CH; ++c) {
+            const size_t ps = base + (size_t)min(s0 + c, a.n_split - 1) * DV_TREE_MAX;
+            ms[c] = a.part_m[ps];
+            ls[c] = a.part_l[ps];
+            os[c] = a.part_o[ps * HD + d];
+        }
+        float mx = run_m;
+#pragma unroll
+        for (int c = 0; c < CH; ++c)
+            if (s0 + c < a.n_split) mx = fmaxf(mx, ms[c]);
+        if (mx == -INFINITY) continue;
+        const float sc = run_m == -INFINITY ? 0.f : expf(run_m - mx);
+        l *= sc;
+        o *= sc;
+#pragma unroll
+        for (int c = 0; c < CH; ++c) {
+            if (s0 + c < a.n_split && ms[c] != -INFINITY) {
+                const float w = expf(ms[c] - mx);
+                l = fmaf(w, ls[c], l);
+                o = fmaf(w, os[c], o);
+            }
+        }
+        run_m = mx;
+    }
+    if (a.out_split) store_split(a.out_split, i, h * HD + d, MT, o / l);
+    else a.out[(size_t)i * a.H * HD + h * HD + d] = o / l;
 }
 
 // ---------------------------------------------------------------------------
@@ -649,63 +988,102 @@ __global__ __launch_bounds__(1024) void k_accept(AcceptArgs a)
 
 // ---------------------------------------------------------------------------
 // KV commit: slot P+k <- slot P+path[k] for k < n, for every (layer, head)
-// of K (blockIdx.y = 0) and V (1).  A destination can be the source of
-// another k, so every row is read into LDS before any row is written.
+// of K (blockIdx.y = 0, rows [cap][hd]) and V (1, columns of [hd][cap]).  A
+// destination can be the source of another k, so every entry is read into
+// LDS before any entry is written.
 
 template <typename KV>
 __global__ __launch_bounds__(256) void k_kv_commit(CommitArgs a)
 {
     __shared__ KV buf[DV_TREE_MAX * 128];
-    KV *base = reinterpret_cast<KV *>(blockIdx.y ? a.vc : a.kc) + (size_t)blockIdx.x * a.cap * a.hd;
+    const bool is_v = blockIdx.y != 0;
+    KV *base = reinterpret_cast<KV *>(is_v ? a.vc : a.kc) + (size_t)blockIdx.x * a.cap * a.hd;
     const int nel = a.n * a.hd;
     for (int e = threadIdx.x; e < nel; e += blockDim.x) {
         const int k = e / a.hd, d = e % a.hd;
-        buf[e] = base[(size_t)(a.P + a.path[k]) * a.hd + d];
+        const size_t src = is_v ? (size_t)d * a.cap + a.P + a.path[k] : (size_t)(a.P + a.path[k]) * a.hd + d;
+        buf[e] = base[src];
     }
     __syncthreads();
     for (int e = threadIdx.x; e < nel; e += blockDim.x) {
         const int k = e / a.hd, d = e % a.hd;
-        if (a.path[k] != k) base[(size_t)(a.P + k) * a.hd + d] = buf[e];
+        if (a.path[k] == k) continue;
+        const size_t dst = is_v ? (size_t)d * a.cap + a.P + k : (size_t)(a.P + k) * a.hd + d;
+        base[dst] = buf[e];
     }
 }
 
 // ---------------------------------------------------------------------------
 // launchers
 
-template <int EPI, typename KV>
-static const void *gemm_kernel(int weight_bf16, int use_mfma, int mt)
+// Load batch per variant: U k-steps for one token tile, fewer as MT grows
+// (register budget); waves per workgroup capped at 4 for MT >= 3.
+template <int EPI, typename KV, int NW, int U, int TP>
+static const void *gemm_kernel_mfma(int mt)
 {
-    if (weight_bf16 && use_mfma) {
-        switch (mt) {
-        case 1: return (const void *)k_gemm_mfma<1, EPI, KV>;
-        case 2: return (const void *)k_gemm_mfma<2, EPI, KV>;
-        case 3: return (const void *)k_gemm_mfma<3, EPI, KV>;
-        case 4: return (const void *)k_gemm_mfma<4, EPI, KV>;
-        default: return nullptr;
-        }
+    switch (mt) {
+    case 1: return (const void *)k_gemm_mfma<1, EPI, KV, NW, U, TP>;
+    case 2: return (const void *)k_gemm_mfma<2, EPI, KV, NW, (U > 4 ? U / 2 : 2), TP>;
+    case 3: return (const void *)k_gemm_mfma<3, EPI, KV, 4, 2, TP>;
+    case 4: return (const void *)k_gemm_mfma<4, EPI, KV, 4, 2, TP>;
+    default: return nullptr;
     }
-    if (weight_bf16) return (const void *)k_gemm_valu<uint16_t, EPI, KV>;
-    return (const void *)k_gemm_valu<float, EPI, KV>;
 }
 
-static const void *gemm_kernel_any(int epi, int weight_bf16, int use_mfma, int mt)
+template <int EPI>
+static const void *gemm_kernel(int weight_bf16, int use_mfma, int mt, GemmShape sh)
 {
-    if (weight_bf16) {
-        switch (epi) {
-        case EPI_QKV: return gemm_kernel<EPI_QKV, uint16_t>(1, use_mfma, mt);
-        case EPI_RESID: return gemm_kernel<EPI_RESID, uint16_t>(1, use_mfma, mt);
-        case EPI_SWIGLU: return gemm_kernel<EPI_SWIGLU, uint16_t>(1, use_mfma, mt);
-        case EPI_LOGITS: return gemm_kernel<EPI_LOGITS, uint16_t>(1, use_mfma, mt);
-        }
-    } else {
-        switch (epi) {
-        case EPI_QKV: return gemm_kernel<EPI_QKV, float>(0, 0, mt);
-        case EPI_RESID: return gemm_kernel<EPI_RESID, float>(0, 0, mt);
-        case EPI_SWIGLU: return gemm_kernel<EPI_SWIGLU, float>(0, 0, mt);
-        case EPI_LOGITS: return gemm_kernel<EPI_LOGITS, float>(0, 0, mt);
-        }
+    if (weight_bf16 && use_mfma) {
+        if (sh.nw == 8 && sh.tp == 2) return gemm_kernel_mfma<EPI, uint16_t, 8, 4, 2>(mt);
+        if (sh.tp == 2) return gemm_kernel_mfma<EPI, uint16_t, 4, 8, 2>(mt);
+        return gemm_kernel_mfma<EPI, uint16_t, 4, 8, 1>(mt);
+    }
+    if (weight_bf16) return (const void *)k_gemm_valu<uint16_t, EPI, uint16_t>;
+    return (const void *)k_gemm_valu<float, EPI, float>;
+}
+
+static const void *gemm_kernel_any(int epi, int weight_bf16, int use_mfma, int mt, GemmShape sh)
+{
+    switch (epi) {
+    case EPI_QKV: return gemm_kernel<EPI_QKV>(weight_bf16, use_mfma, mt, sh);
+    case EPI_RESID: return gemm_kernel<EPI_RESID>(weight_bf16, use_mfma, mt, sh);
+    case EPI_SWIGLU: return gemm_kernel<EPI_SWIGLU>(weight_bf16, use_mfma, mt, sh);
+    case EPI_LOGITS: return gemm_kernel<EPI_LOGITS>(weight_bf16, use_mfma, mt, sh);
     }
     return nullptr;
+}
+
+static int gemm_threads(int weight_bf16, int use_mfma, int mt, GemmShape sh)
+{
+    if (!(weight_bf16 && use_mfma)) return 256;
+    return mt >= 3 ? 256 : 64 * sh.nw;
+}
+
+int gemm_blocks_per_cu(int epi, int weight_bf16, int use_mfma, int mt, GemmShape sh)
+{
+    static int cache[4][2][2][5][2][2];
+    int &c = cache[epi & 3][weight_bf16 ? 1 : 0][use_mfma ? 1 : 0][(mt >= 1 && mt <= 4) ? mt : 0]
+                  [sh.nw == 8 ? 1 : 0][sh.tp == 2 ? 1 : 0];
+    if (c == 0) {
+        const void *k = gemm_kernel_any(epi, weight_bf16, use_mfma, mt, sh);
+        int n = 0;
+        if (!k || hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k, gemm_threads(weight_bf16, use_mfma, mt, sh),
+                                                               0) != hipSuccess || n < 1)
+            n = 1;
+        c = n;
+    }
+    return c;
+}
+
+hipError_t launch_gemm(const GemmArgs &a, int grid, int epi, int weight_bf16, int use_mfma,
+                       GemmShape sh, hipStream_t s)
+{
+    const void *k = gemm_kernel_any(epi, weight_bf16, use_mfma, a.Mpad / 16, sh);
+    if (!k || grid < 1) return hipErrorInvalidValue;
+    GemmArgs arg = a;
+    void *params[] = {&arg};
+    return hipLaunchKernel(k, dim3(grid), dim3(gemm_threads(weight_bf16, use_mfma, a.Mpad / 16, sh)), params, 0,
+                           s);
 }
 
 hipError_t launch_pack(const GemmArgs &a, int epi, uint16_t *dst, hipStream_t s)
@@ -714,48 +1092,47 @@ hipError_t launch_pack(const GemmArgs &a, int epi, uint16_t *dst, hipStream_t s)
     return hipGetLastError();
 }
 
-int gemm_blocks_per_cu(int epi, int weight_bf16, int use_mfma, int mt)
+template <typename W, int NV>
+static hipError_t rmsnorm_dispatch_ks(const NormArgs &a, int Mpad, hipStream_t s)
 {
-    static int cache[4][2][2][5];
-    int &c = cache[epi & 3][weight_bf16 ? 1 : 0][use_mfma ? 1 : 0][(mt >= 1 && mt <= 4) ? mt : 0];
-    if (c == 0) {
-        const void *k = gemm_kernel_any(epi, weight_bf16, use_mfma, mt);
-        int n = 0;
-        if (!k || hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k, 256, 0) != hipSuccess || n < 1)
-            n = 1;
-        c = n;
+    const dim3 grid(Mpad, DV_NORM_SLICES), block(256);
+    switch (a.ks) {
+    case 0: hipLaunchKernelGGL((k_rmsnorm<W, NV, 0>), grid, block, 0, s, a); break;
+    case 2: hipLaunchKernelGGL((k_rmsnorm<W, NV, 2>), grid, block, 0, s, a); break;
+    case 4: hipLaunchKernelGGL((k_rmsnorm<W, NV, 4>), grid, block, 0, s, a); break;
+    case 8: hipLaunchKernelGGL((k_rmsnorm<W, NV, 8>), grid, block, 0, s, a); break;
+    default: hipLaunchKernelGGL((k_rmsnorm<W, NV, -1>), grid, block, 0, s, a); break;
     }
-    return c;
+    return hipGetLastError();
 }
 
-hipError_t launch_gemm(const GemmArgs &a, int grid, int epi, int weight_bf16, int use_mfma,
-                       hipStream_t s)
+template <typename W>
+static hipError_t rmsnorm_dispatch(const NormArgs &a, int Mpad, hipStream_t s)
 {
-    const void *k = gemm_kernel_any(epi, weight_bf16, use_mfma, a.Mpad / 16);
-    if (!k || grid < 1) return hipErrorInvalidValue;
-    GemmArgs arg = a;
-    void *params[] = {&arg};
-    return hipLaunchKernel(k, dim3(grid), dim3(256), params, 0, s);
+    const int slice = a.d / DV_NORM_SLICES;
+    if (a.d % (4 * DV_NORM_SLICES)) return hipErrorInvalidValue;
+    switch ((slice + 1023) / 1024) {
+    case 1: return rmsnorm_dispatch_ks<W, 1>(a, Mpad, s);
+    case 2: return rmsnorm_dispatch_ks<W, 2>(a, Mpad, s);
+    default: return hipErrorInvalidValue;
+    }
 }
 
 hipError_t launch_rmsnorm(const NormArgs &a, int Mpad, int weight_bf16, hipStream_t s)
 {
-    if (weight_bf16)
-        hipLaunchKernelGGL(k_rmsnorm<uint16_t>, dim3(Mpad), dim3(256), 0, s, a);
-    else
-        hipLaunchKernelGGL(k_rmsnorm<float>, dim3(Mpad), dim3(256), 0, s, a);
-    return hipGetLastError();
+    return weight_bf16 ? rmsnorm_dispatch<uint16_t>(a, Mpad, s) : rmsnorm_dispatch<float>(a, Mpad, s);
 }
 
 hipError_t launch_attention(const AttnArgs &a, int kv_bf16, hipStream_t s)
 {
     const dim3 grid(a.n_split, a.H), block(256);
+    const dim3 block8(64 * DV_ATTN_WAVES);
     if (a.hd == 128) {
-        if (kv_bf16) hipLaunchKernelGGL((k_attn<128, uint16_t>), grid, block, 0, s, a);
-        else hipLaunchKernelGGL((k_attn<128, float>), grid, block, 0, s, a);
+        if (kv_bf16) hipLaunchKernelGGL((k_attn_mfma<128, DV_ATTN_WAVES>), grid, block8, 0, s, a);
+        else hipLaunchKernelGGL(k_attn_f32<128>, grid, block, 0, s, a);
     } else if (a.hd == 64) {
-        if (kv_bf16) hipLaunchKernelGGL((k_attn<64, uint16_t>), grid, block, 0, s, a);
-        else hipLaunchKernelGGL((k_attn<64, float>), grid, block, 0, s, a);
+        if (kv_bf16) hipLaunchKernelGGL((k_attn_mfma<64, DV_ATTN_WAVES>), grid, block8, 0, s, a);
+        else hipLaunchKernelGGL(k_attn_f32<64>, grid, block, 0, s, a);
     } else {
         return hipErrorInvalidValue;
     }

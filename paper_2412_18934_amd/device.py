@@ -62,18 +62,20 @@ class DeviceWeights:
 
 
 class DeviceKV:
-    """KV cache [L][H][capacity][hd] for K and V, weight dtype."""
+    """KV cache: K [L][H][capacity][hd], V [L][H][hd][capacity] (dim-major),
+    weight dtype.  capacity must be a multiple of 32."""
 
     def __init__(self, n_layers, n_heads, head_dim, capacity, weight_dtype, device="cuda:0",
                  fill=None):
         dt = torch.bfloat16 if weight_dtype == "bf16" else torch.float32
-        shape = (n_layers, n_heads, capacity, head_dim)
+        kshape = (n_layers, n_heads, capacity, head_dim)
+        vshape = (n_layers, n_heads, head_dim, capacity)
         if fill is None:
-            self.k = torch.zeros(shape, dtype=dt, device=device)
-            self.v = torch.zeros(shape, dtype=dt, device=device)
+            self.k = torch.zeros(kshape, dtype=dt, device=device)
+            self.v = torch.zeros(vshape, dtype=dt, device=device)
         else:
-            self.k = torch.full(shape, fill, dtype=dt, device=device)
-            self.v = torch.full(shape, fill, dtype=dt, device=device)
+            self.k = torch.full(kshape, fill, dtype=dt, device=device)
+            self.v = torch.full(vshape, fill, dtype=dt, device=device)
         self.c = dv.dv_kv(self.k.data_ptr(), self.v.data_ptr(), capacity, 0)
 
     @property
@@ -84,13 +86,13 @@ class DeviceKV:
         """Write committed entries [0, n) of layer l from host arrays [H][n][hd]."""
         n = k.shape[1]
         self.k[l, :, :n].copy_(to_device(k, self.k.device))
-        self.v[l, :, :n].copy_(to_device(v, self.v.device))
+        self.v[l, :, :, :n].copy_(to_device(v, self.v.device).transpose(1, 2))
 
     def layer_host(self, l: int, n: int):
-        """Entries [0, n) of layer l as host arrays in the stored format."""
+        """Entries [0, n) of layer l as host arrays [H][n][hd] in the stored format."""
         def host(t):
-            t = t[l, :, :n].contiguous().cpu()
+            t = t.contiguous().cpu()
             if t.dtype == torch.bfloat16:
                 return t.view(torch.int16).numpy().view(np.uint16)
             return t.numpy()
-        return host(self.k), host(self.v)
+        return host(self.k[l, :, :n]), host(self.v[l, :, :, :n].transpose(1, 2))

@@ -123,7 +123,7 @@ def test_bf16_empty_context_and_planted_acceptance(bf16_case):
 def test_bf16_head_dim_64_parity():
     cfg = small_cfg(n_layers=2, d_model=256, n_heads=4, head_dim=64, d_ffn=528, vocab=1056,
                     weight_dtype="bf16", init_std=0.09)
-    case = GpuCase(cfg, seed=81, capacity=200)
+    case = GpuCase(cfg, seed=81, capacity=224)
     try:
         om = case.w.oracle()
         kv = case.new_kv()
