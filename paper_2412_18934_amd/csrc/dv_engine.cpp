@@ -134,10 +134,13 @@ int gemm_grid(const GemmPlan &p, int epi, int bf16, int mt, int n_cu)
     return ceil_div(units, per);
 }
 
-void prof_begin(dv_handle *h, int cls)
+// Event pair for the next launch of class cls, or nullptr when that class is
+// not being timed.  GEMM launches pass the pair to hipExtLaunchKernel (the
+// dispatch packet records the timestamps); other classes are bracketed by
+// hipEventRecord.
+ProfEv *prof_pair(dv_handle *h, int cls)
 {
-    h->prof_open = false;
-    if (!(h->prof >> cls & 1)) return;
+    if (!(h->prof >> cls & 1)) return nullptr;
     ProfEv e{cls, nullptr, nullptr};
     if (h->ev_pool.size() >= 2) {
         e.a = h->ev_pool.back(); h->ev_pool.pop_back();
@@ -146,8 +149,16 @@ void prof_begin(dv_handle *h, int cls)
         (void)hipEventCreate(&e.a);
         (void)hipEventCreate(&e.b);
     }
-    (void)hipEventRecord(e.a, h->stream);
     h->ev_live.push_back(e);
+    return &h->ev_live.back();
+}
+
+void prof_begin(dv_handle *h, int cls)
+{
+    h->prof_open = false;
+    ProfEv *e = prof_pair(h, cls);
+    if (!e) return;
+    (void)hipEventRecord(e->a, h->stream);
     h->prof_open = true;
 }
 
@@ -264,9 +275,9 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
         a.x = x;
         a.out = out;
         const int grid = gemm_grid(p, epi, h->bf16, Mpad / 16, h->n_cu);
-        prof_begin(h, DV_K_GEMM);
-        hipError_t e = launch_gemm(a, grid, epi, h->bf16, p.mfma, p.shape, s);
-        prof_end(h);
+        ProfEv *ev = prof_pair(h, DV_K_GEMM);
+        hipError_t e = launch_gemm(a, grid, epi, h->bf16, p.mfma, p.shape, s, ev ? ev->a : nullptr,
+                                   ev ? ev->b : nullptr);
         if (e != hipSuccess) return hip_fail(h, e, "gemm launch");
         if (epi == EPI_RESID) pending_ks = p.ks > 1 ? p.ks : 0;
         return DV_OK;

@@ -131,8 +131,9 @@ struct CommitArgs {
 hipError_t launch_pack(const GemmArgs &a, int epi, uint16_t *dst, hipStream_t s);
 // workgroups of 256 threads one CU can hold for a GEMM variant (cached)
 int gemm_blocks_per_cu(int epi, int weight_bf16, int use_mfma, int mt, GemmShape sh);
+// ev_start/ev_stop (optional, both or neither): timestamps of this launch
 hipError_t launch_gemm(const GemmArgs &a, int grid, int epi, int weight_bf16, int use_mfma,
-                       GemmShape sh, hipStream_t s);
+                       GemmShape sh, hipStream_t s, hipEvent_t ev_start, hipEvent_t ev_stop);
 hipError_t launch_rmsnorm(const NormArgs &a, int Mpad, int weight_bf16, hipStream_t s);
 hipError_t launch_attention(const AttnArgs &a, int kv_bf16, hipStream_t s);
 hipError_t launch_attn_merge(const AttnArgs &a, int Mpad, hipStream_t s);

@@ -14,6 +14,7 @@
 //
 // Weights are bf16 or fp32, activations and accumulation fp32.  Every
 // reduction runs in a fixed order, so results are bitwise reproducible.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -948,17 +949,32 @@ __global__ __launch_bounds__(1024) void k_accept(AcceptArgs a)
     __shared__ int32_t ok[DV_TREE_MAX];
     const StepDesc *sd = a.sd;
     const int M = sd->M, tid = threadIdx.x;
-    const int m = tid >> 4, sub = tid & 15;
+    // tpt threads per node (64, 32 or 16), each scanning a contiguous chunk of
+    // the tiles 16 loads at a time (clamped indices only repeat a real entry)
+    const int tpt = sd->Mpad <= 16 ? 64 : (sd->Mpad <= 32 ? 32 : 16);
+    const int m = tid / tpt, sub = tid % tpt;
     if (m < M) {
         const float *val = a.arg_val + (size_t)m * a.n_tiles;
         const int32_t *idx = a.arg_idx + (size_t)m * a.n_tiles;
+        const int chunk = (a.n_tiles + tpt - 1) / tpt;
+        const int t0 = sub * chunk, t1 = min(a.n_tiles, t0 + chunk);
         float best = -INFINITY;
         int bi = 0x7fffffff;
-        for (int t = sub; t < a.n_tiles; t += 16) arg_better(best, bi, val[t], idx[t]);
+        for (int t = t0; t < t1; t += 16) {
+            float v[16];
+            int ix[16];
 #pragma unroll
-        for (int off = 8; off > 0; off >>= 1) {
-            const float v2 = __shfl_xor(best, off, 16);
-            const int i2 = __shfl_xor(bi, off, 16);
+            for (int c = 0; c < 16; ++c) {
+                const int tt = min(t + c, t1 - 1);
+                v[c] = val[tt];
+                ix[c] = idx[tt];
+            }
+#pragma unroll
+            for (int c = 0; c < 16; ++c) arg_better(best, bi, v[c], ix[c]);
+        }
+        for (int off = tpt >> 1; off > 0; off >>= 1) {
+            const float v2 = __shfl_xor(best, off, tpt);
+            const int i2 = __shfl_xor(bi, off, tpt);
             arg_better(best, bi, v2, i2);
         }
         if (sub == 0) {
@@ -1076,14 +1092,16 @@ int gemm_blocks_per_cu(int epi, int weight_bf16, int use_mfma, int mt, GemmShape
 }
 
 hipError_t launch_gemm(const GemmArgs &a, int grid, int epi, int weight_bf16, int use_mfma,
-                       GemmShape sh, hipStream_t s)
+                       GemmShape sh, hipStream_t s, hipEvent_t ev_start, hipEvent_t ev_stop)
 {
     const void *k = gemm_kernel_any(epi, weight_bf16, use_mfma, a.Mpad / 16, sh);
     if (!k || grid < 1) return hipErrorInvalidValue;
     GemmArgs arg = a;
     void *params[] = {&arg};
-    return hipLaunchKernel(k, dim3(grid), dim3(gemm_threads(weight_bf16, use_mfma, a.Mpad / 16, sh)), params, 0,
-                           s);
+    const dim3 block(gemm_threads(weight_bf16, use_mfma, a.Mpad / 16, sh));
+    // with events: timestamps taken by the dispatch itself (no extra packets)
+    if (ev_start && ev_stop) return hipExtLaunchKernel(k, dim3(grid), block, params, 0, s, ev_start, ev_stop, 0);
+    return hipLaunchKernel(k, dim3(grid), block, params, 0, s);
 }
 
 hipError_t launch_pack(const GemmArgs &a, int epi, uint16_t *dst, hipStream_t s)
