@@ -982,20 +982,27 @@ __global__ __launch_bounds__(1024) void k_accept(AcceptArgs a)
             a.acc->argmax[m] = bi;
         }
     }
+    // the tree in LDS, so the serial walk below makes no global round trips
+    __shared__ int32_t par_s[DV_TREE_MAX], tok_s[DV_TREE_MAX], dep_s[DV_TREE_MAX];
+    if (tid < M) {
+        par_s[tid] = sd->parents[tid];
+        tok_s[tid] = sd->tokens[tid];
+        dep_s[tid] = sd->depth[tid];
+    }
     __syncthreads();
     if (tid == 0) {
         ok[0] = 1;
         int best = 0;
         for (int i = 1; i < M; ++i) {
-            const int p = sd->parents[i];
-            ok[i] = ok[p] && sd->tokens[i] == amax[p];
-            if (ok[i] && sd->depth[i] > sd->depth[best]) best = i;
+            const int p = par_s[i];
+            ok[i] = ok[p] && tok_s[i] == amax[p];
+            if (ok[i] && dep_s[i] > dep_s[best]) best = i;
         }
-        const int n = sd->depth[best];
+        const int n = dep_s[best];
         int node = best;
         for (int k = n - 1; k >= 0; --k) {
             a.acc->path[k] = node;
-            node = sd->parents[node];
+            node = par_s[node];
         }
         a.acc->accept_len = n;
         a.acc->bonus = amax[best];

@@ -1,0 +1,140 @@
+"""Summaries of rocprofv3 output for libdv kernels (text, for profiles/).
+
+    python -m paper_2412_18934_amd.profiling stats <kernel_stats.csv> <kernel_trace.csv> <out.md> <command>
+    python -m paper_2412_18934_amd.profiling hbm <fetch counter_collection.csv> <write counter_collection.csv> <out.txt> <command>
+
+``stats`` writes a per-kernel table (calls, average, share) plus the average
+duration of the projection kernels (k_gemm_*), the figure bench.py's roofline
+uses.  ``hbm`` turns FETCH_SIZE / WRITE_SIZE (KiB per dispatch) into bytes per
+dispatch, scaled by what the same counters read for a reference copy of known
+size (the 256 MiB device copy bench.py --calibrate-copy issues: 256 MiB read
+and 256 MiB written), and records a hash of the kernel source so that a reader
+can tell whether the numbers still describe the current kernels.
+"""
+from __future__ import annotations
+
+import collections
+import csv
+import hashlib
+import os
+import statistics
+import sys
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+KERNEL_SOURCES = ("csrc/dv_kernels.hip", "csrc/dv_engine.cpp", "csrc/dv_internal.h")
+CALIB_BYTES = 256 << 20
+
+
+def source_hash() -> str:
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(PKG, rel), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def _short(name: str) -> str:
+    return name.replace("void ", "").split("(")[0]
+
+
+def summarize_stats(stats_csv, trace_csv, out_path, command):
+    rows = list(csv.DictReader(open(stats_csv)))
+    lines = ["# rocprofv3 kernel statistics", "", "Command:", "", "    " + command, "",
+             "Source hash of the kernels: `%s`" % source_hash(), "",
+             "| kernel | calls | average (us) | share |", "|---|---|---|---|"]
+    gemm_ns, gemm_n = 0.0, 0
+    for r in rows:
+        name = _short(r["Name"])
+        n = int(r["Calls"])
+        avg = float(r["AverageNs"]) / 1e3
+        lines.append("| `%s` | %d | %.2f | %.1f%% |" % (name, n, avg, float(r["Percentage"])))
+        if name.startswith("k_gemm"):
+            gemm_ns += float(r["TotalDurationNs"])
+            gemm_n += n
+    lines += ["", "Projection kernels (k_gemm_*): %d launches, average %.2f us."
+              % (gemm_n, gemm_ns / max(gemm_n, 1) / 1e3)]
+    # one full step from the trace: the span between two k_accept dispatches
+    trace = list(csv.DictReader(open(trace_csv)))
+    trace.sort(key=lambda r: int(r["Start_Timestamp"]))
+    acc = [i for i, r in enumerate(trace) if _short(r["Kernel_Name"]).startswith("k_accept")]
+    if len(acc) >= 2:
+        step = trace[acc[-2] + 1: acc[-1] + 1]
+        span = (int(step[-1]["End_Timestamp"]) - int(step[0]["Start_Timestamp"])) / 1e3
+        busy = sum(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in step) / 1e3
+        per = collections.defaultdict(list)
+        for r in step:
+            per[_short(r["Kernel_Name"])].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+        lines += ["", "Last full step in the trace: %d dispatches, GPU span %.1f us, kernels busy %.1f us."
+                  % (len(step), span, busy), "", "| kernel (last step) | calls | average (us) | total (us) |",
+                  "|---|---|---|---|"]
+        for k, v in sorted(per.items(), key=lambda kv: -sum(kv[1])):
+            lines.append("| `%s` | %d | %.2f | %.1f |" % (k, len(v), statistics.mean(v), sum(v)))
+    with open(out_path, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+
+
+def summarize_hbm(fetch_csv, write_csv, out_path, command):
+    def per_kernel(path):
+        agg = collections.defaultdict(list)
+        for r in csv.DictReader(open(path)):
+            agg[_short(r["Kernel_Name"])].append(float(r["Counter_Value"]))
+        return agg
+    f, w = per_kernel(fetch_csv), per_kernel(write_csv)
+    # reference: the copy that reads CALIB_BYTES (largest copyBuffer dispatch)
+    f_ref = max(f.get("__amd_rocclr_copyBuffer", [0.0]))
+    w_ref = max(w.get("__amd_rocclr_copyBuffer", [0.0]))
+    fs = CALIB_BYTES / (f_ref * 1024) if f_ref else float("nan")
+    ws = CALIB_BYTES / (w_ref * 1024) if w_ref else float("nan")
+    lines = ["# HBM bytes per dispatch (rocprofv3 FETCH_SIZE / WRITE_SIZE)", "",
+             "command: " + command,
+             "source_hash: %s" % source_hash(),
+             "reference copy: %d bytes; FETCH_SIZE reads %.1f KiB -> scale %.4f; "
+             "WRITE_SIZE reads %.1f KiB -> scale %.4f" % (CALIB_BYTES, f_ref, fs, w_ref, ws), ""]
+    for k in sorted(set(f) & set(w)):
+        if not k.startswith("k_"):
+            continue
+        fb = statistics.mean(f[k]) * 1024 * fs
+        wb = statistics.mean(w[k]) * 1024 * ws
+        lines.append("kernel %s: dispatches %d, fetch_bytes %.0f, write_bytes %.0f"
+                     % (k, len(f[k]), fb, wb))
+    with open(out_path, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+
+
+def read_hbm_summary(path):
+    """(source_hash, {kernel: (dispatches, fetch_bytes, write_bytes)})."""
+    out, sh = {}, None
+    with open(path) as fh:
+        for ln in fh:
+            if ln.startswith("source_hash:"):
+                sh = ln.split(":", 1)[1].strip()
+            elif ln.startswith("kernel "):
+                name, rest = ln[len("kernel "):].rsplit(":", 1)
+                kv = dict(p.strip().split(" ", 1) for p in rest.split(","))
+                out[name.strip()] = (int(kv["dispatches"]), float(kv["fetch_bytes"]),
+                                     float(kv["write_bytes"]))
+    return sh, out
+
+
+def gemm_traffic_per_launch(path):
+    """Average HBM bytes (fetch + write) over all projection dispatches of a
+    summary, or None when the summary is missing or the kernel sources have
+    changed since it was taken."""
+    if not os.path.exists(path):
+        return None
+    sh, per = read_hbm_summary(path)
+    if sh != source_hash():
+        return None
+    n = sum(d for k, (d, f, w) in per.items() if k.startswith("k_gemm"))
+    if not n:
+        return None
+    return sum(d * (f + w) for k, (d, f, w) in per.items() if k.startswith("k_gemm")) / n
+
+
+if __name__ == "__main__":
+    if sys.argv[1] == "stats":
+        summarize_stats(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5])
+    elif sys.argv[1] == "hbm":
+        summarize_hbm(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5])
+    else:
+        raise SystemExit(__doc__)
