@@ -115,7 +115,7 @@ GemmPlan make_plan(int n_tiles, int K, int align, int mfma, int ks, GemmShape sh
     p.n_tiles = n_tiles;
     p.mfma = mfma;
     p.shape = shape;
-    if (mfma && n_tiles % shape.tp) p.shape.tp = 1;
+    if (mfma && n_tiles % shape.tp) p.shape = GemmShape{4, 8, 1};
     while (ks > 1 && K / ks < 4 * align) ks /= 2;
     int kps = round_up(ceil_div(K, ks), align);
     p.k_per_split = kps;
@@ -123,12 +123,25 @@ GemmPlan make_plan(int n_tiles, int K, int align, int mfma, int ks, GemmShape sh
     return p;
 }
 
+// Shape used for mt token tiles: four tiles per workgroup hold too many
+// accumulators beyond 32 tokens, so those steps use two.
+GemmShape shape_for(const GemmPlan &p, int mt)
+{
+    if (p.shape.tp > 2 && mt >= 3) return p.n_tiles % 2 ? GemmShape{4, 8, 1} : GemmShape{4, 8, 2};
+    return p.shape;
+}
+
+int gemm_units(const GemmPlan &p, int mt)
+{
+    return (p.mfma ? p.n_tiles / shape_for(p, mt).tp : p.n_tiles) * p.ks;
+}
+
 // Resident grid for a launch: every workgroup loops over an equal share of
 // the work units.
 int gemm_grid(const GemmPlan &p, int epi, int bf16, int mt, int n_cu)
 {
-    const int units = (p.mfma ? p.n_tiles / p.shape.tp : p.n_tiles) * p.ks;
-    const int cap = std::max(1, gemm_blocks_per_cu(epi, bf16, p.mfma, mt, p.shape) * n_cu);
+    const int units = gemm_units(p, mt);
+    const int cap = std::max(1, gemm_blocks_per_cu(epi, bf16, p.mfma, mt, shape_for(p, mt)) * n_cu);
     if (units <= cap) return units;
     const int per = ceil_div(units, cap);
     return ceil_div(units, per);
@@ -205,12 +218,14 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
 
     const size_t layer_kv = (size_t)H * kv->capacity * hd * h->esz;
     // attention: the P + M keys of each head are split evenly into
-    // tile-aligned ranges of about DV_ATTN_SPLIT_KEYS (one merge pass combines
-    // them); a context that fits one range needs no merge
+    // tile-aligned ranges, one workgroup each, so that heads x splits covers
+    // the compute units once (each workgroup streams its range with a
+    // two-tile pipeline per wave); the merge kernel combines the splits, and a
+    // single split writes the output itself
     const int total = P + M;
     int kps, n_split;
     if (h->bf16) {
-        n_split = std::min(ceil_div(total, DV_ATTN_SPLIT_KEYS), h->attn_split_max);
+        n_split = std::max(1, std::min(h->n_cu / H, h->attn_split_max));
         kps = round_up(ceil_div(total, n_split), DV_ATTN_TILE);
     } else {
         kps = round_up(ceil_div(total, h->attn_split_max), DV_ATTN_TILE);
@@ -271,12 +286,12 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
         a.n_tiles = p.n_tiles;
         a.ks = p.ks;
         a.k_per_split = p.k_per_split;
-        a.n_units = (p.mfma ? p.n_tiles / p.shape.tp : p.n_tiles) * p.ks;
+        a.n_units = gemm_units(p, Mpad / 16);
         a.x = x;
         a.out = out;
         const int grid = gemm_grid(p, epi, h->bf16, Mpad / 16, h->n_cu);
         ProfEv *ev = prof_pair(h, DV_K_GEMM);
-        hipError_t e = launch_gemm(a, grid, epi, h->bf16, p.mfma, p.shape, s, ev ? ev->a : nullptr,
+        hipError_t e = launch_gemm(a, grid, epi, h->bf16, p.mfma, shape_for(p, Mpad / 16), s, ev ? ev->a : nullptr,
                                    ev ? ev->b : nullptr);
         if (e != hipSuccess) return hip_fail(h, e, "gemm launch");
         if (epi == EPI_RESID) pending_ks = p.ks > 1 ? p.ks : 0;
@@ -458,12 +473,12 @@ int dv_verify_init(const dv_config *cfg, const dv_weights *w, void *stream, dv_h
     const int al = mf ? 32 : 8;
     // shapes and K splits measured on MI355X for the weight-streaming regime
     // (13B-sized projections, weights read once from HBM per step)
-    const GemmShape wide8{8, 4, 2}, wide4{4, 8, 2}, narrow{4, 8, 1};
+    const GemmShape wide8{8, 4, 2}, wide4{4, 8, 2}, quad{4, 4, 4}, narrow{4, 8, 1};
     h->p_qkv = make_plan(3 * d / DV_GEMM_TILE, d, al, mf, 1, wide8);
     h->p_o = make_plan(d / DV_GEMM_TILE, d, al, mf, 8, narrow);
-    h->p_gu = make_plan(F / 16, d, al, mf, 1, wide4);
+    h->p_gu = make_plan(F / 16, d, al, mf, 1, quad);
     const int mf_down = mf && (F % 32 == 0);
-    h->p_down = make_plan(d / DV_GEMM_TILE, F, mf_down ? 32 : 8, mf_down, 8, wide4);
+    h->p_down = make_plan(d / DV_GEMM_TILE, F, mf_down ? 32 : 8, mf_down, 16, wide8);
     h->p_lm = make_plan(V / DV_GEMM_TILE, d, al, mf, 1, wide4);
 
     const size_t part_elems = (size_t)std::max(h->p_o.ks, h->p_down.ks) * DV_TREE_MAX * d;

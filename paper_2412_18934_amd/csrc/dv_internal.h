@@ -8,8 +8,8 @@
 #define DV_TREE_MAX 64
 #define DV_GEMM_TILE 32     // logical output rows per workgroup tile
 #define DV_ATTN_TILE 32     // keys per attention tile
-#define DV_ATTN_WAVES 8     // waves per attention workgroup (MFMA path)
-#define DV_ATTN_SPLIT_KEYS 256   // keys per attention workgroup (one 32-key tile per wave)
+#define DV_ATTN_WAVES 4     // waves per attention workgroup (MFMA path)
+#define DV_ATTN_SPLIT_KEYS 256   // keys per workgroup of the fp32-cache attention
 
 // Per-step description of the draft tree, uploaded once per step.
 struct StepDesc {
@@ -45,6 +45,9 @@ enum GemmEpi { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LOGITS = 3 };
 
 // GEMM variants (MFMA path): waves per workgroup, k-steps per load batch
 // and tiles per work unit; supported: {8, 4, 2}, {4, 8, 2}, {4, 8, 1}
+// Workgroup shape of the MFMA projection kernel: nw waves, u k-steps per
+// batch of loads, tp tiles sharing the activation operand.  Instantiated
+// shapes: {8,4,2}, {4,8,2}, {4,4,4}, {4,8,1}.
 struct GemmShape {
     int nw;
     int u;

@@ -284,6 +284,17 @@ __global__ __launch_bounds__(128) void k_pack_tiles(GemmArgs a, int epi, uint16_
     }
 }
 
+#ifndef DV_WEIGHT_NT
+#define DV_WEIGHT_NT 1
+#endif
+// Weights are read exactly once per step: the non-temporal hint keeps them
+// from displacing reusable lines (activations) in the caches.
+__device__ __forceinline__ u32x4 load_weights(const u32x4 *p)
+{
+    if (DV_WEIGHT_NT) return __builtin_nontemporal_load(p);
+    return *p;
+}
+
 // N_STEPS k-steps for TP tiles: all weight and activation loads first, then
 // the MFMAs (TP tiles x 2 halves x MT token tiles x hi/lo).
 template <int MT, int TP, int N_STEPS>
@@ -298,7 +309,7 @@ __device__ __forceinline__ void mfma_steps(const uint16_t *wtile, size_t tile_st
         for (int p = 0; p < TP; ++p)
 #pragma unroll
             for (int h = 0; h < 2; ++h)
-                wa[u][p][h] = *reinterpret_cast<const u32x4 *>(wtile + p * tile_stride + (2 * u + h) * 512);
+                wa[u][p][h] = load_weights(reinterpret_cast<const u32x4 *>(wtile + p * tile_stride + (2 * u + h) * 512));
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -571,20 +582,27 @@ __global__ __launch_bounds__(256) void k_rmsnorm(NormArgs a)
 // and sum; k_attn_merge combines the splits (or, with one split, the
 // workgroup writes the normalised output itself).
 
-// bf16 cache, MFMA.  Queries are taken 16 at a time; the four waves take
+// bf16 cache, MFMA.  Queries are taken 16 at a time; the NW waves take
 // interleaved 32-key tiles and are combined in LDS at the end.
 //   S^T = K Q^T: A = 16 keys x 32 dims (16 bytes of one key row per lane),
-//   B = Q^T (fp32 queries split into bf16 hi + lo).  Tile "a" holds keys
-//   k0 + 8(r/4) + r%4 in row r, tile "b" the same + 4, so lane l ends up with
-//   the scores of token l%16 for the 8 consecutive keys k0 + 8(l/16) .. +8.
+//   B = Q^T (fp32 queries split into bf16 hi + lo, staged in LDS).  Tile "a"
+//   holds keys k0 + 8(r/4) + r%4 in row r, tile "b" the same + 4, so lane l
+//   ends up with the scores of token l%16 for the 8 consecutive keys
+//   k0 + 8(l/16) .. +8.
 //   O = P V: A = P (those 8 scores per lane, exponentiated, split hi + lo),
 //   B = V^T rows: 16 bytes = the same 8 consecutive keys of one dim.
+// Scores are kept in base-2 units (scaled by log2(e)/sqrt(hd)) so every
+// exponential is one exp2; the running max written for the merge is
+// converted back to natural units.  Each wave keeps two tiles of K and V in
+// registers (the next one loads while the current one is used); the
+// prologue issues the query, ancestor-mask and first-tile loads together.
 
 template <int HD, int NW>
 __global__ __launch_bounds__(64 * NW) void k_attn_mfma(AttnArgs a)
 {
     constexpr int NC = HD / 32;  // QK k-steps over dims
     constexpr int ND = HD / 16;  // PV output dim tiles
+    static_assert(64 * NW >= 2 * HD, "one thread per 8 query values");
     const int split = blockIdx.x, h = blockIdx.y;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int n = lane & 15, g = lane >> 4;
@@ -594,19 +612,18 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mfma(AttnArgs a)
     const int kend = min(total, kbeg + a.keys_per_split);
     const int ntile = (kend - kbeg + 31) / 32;
     const int D = a.H * HD;
-    const float scale = 1.0f / sqrtf((float)HD);
+    const float scale2 = 1.4426950408889634f / sqrtf((float)HD);
     const uint16_t *kc = reinterpret_cast<const uint16_t *>(a.kc) + (size_t)h * a.cap * HD;
     const uint16_t *vc = reinterpret_cast<const uint16_t *>(a.vc) + (size_t)h * HD * a.cap;
 
+    __shared__ u32x4 sm_q[NC * 2 * 64];  // [k-step][hi/lo][lane] B operands
     __shared__ float sm_m[NW][16], sm_l[NW][16];
     __shared__ float sm_o[NW][16][HD + 4];
 
-    // K rows (A operands of the two score tiles) and V^T columns of one
-    // 32-key tile for this lane
-    struct KTile {
-        u32x4 ka[NC], kb[NC];
+    struct Tile {
+        u32x4 ka[NC], kb[NC], v[ND];
     };
-    auto load_k = [&](int t, KTile &T) {
+    auto load = [&](int t, Tile &T) {
         const int k0 = kbeg + 32 * t;
         const int ka = min(k0 + 8 * (n >> 2) + (n & 3), kend - 1);
         const int kb = min(k0 + 8 * (n >> 2) + 4 + (n & 3), kend - 1);
@@ -615,79 +632,80 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mfma(AttnArgs a)
             T.ka[c] = *reinterpret_cast<const u32x4 *>(kc + (size_t)ka * HD + 32 * c + 8 * g);
             T.kb[c] = *reinterpret_cast<const u32x4 *>(kc + (size_t)kb * HD + 32 * c + 8 * g);
         }
-    };
-    auto load_v = [&](int t, u32x4 (&vv)[ND]) {
-        const int k0 = kbeg + 32 * t;
+        // columns past the last cache slot of the tile stay inside the
+        // allocation (capacity is a multiple of 32); they are masked below
 #pragma unroll
         for (int dt = 0; dt < ND; ++dt)
-            vv[dt] = *reinterpret_cast<const u32x4 *>(vc + (size_t)(dt * 16 + n) * a.cap + k0 + 8 * g);
+            T.v[dt] = *reinterpret_cast<const u32x4 *>(vc + (size_t)(dt * 16 + n) * a.cap + k0 + 8 * g);
     };
 
     for (int q0 = 0; q0 < M; q0 += 16) {
         const int tok = q0 + n;
         const bool tok_ok = tok < M;
-        KTile cur, nxt;
-        u32x4 vv[ND];
-        if (wave < ntile) load_k(wave, cur);  // in flight while q is prepared
-        const float *qrow = a.q + (size_t)min(tok, M - 1) * D + h * HD + g * 8;
-        bf16x8 qh[NC], ql[NC];
-#pragma unroll
-        for (int c = 0; c < NC; ++c) {
-            float4 x0 = *reinterpret_cast<const float4 *>(qrow + 32 * c);
-            float4 x1 = *reinterpret_cast<const float4 *>(qrow + 32 * c + 4);
-            if (!tok_ok) x0 = x1 = make_float4(0.f, 0.f, 0.f, 0.f);
-            split_hi_lo(x0, x1, qh[c], ql[c]);
+        // thread e < 2*HD converts 8 dims (c, group qg) of query row qt
+        const int e = threadIdx.x;
+        const int qt = e / (2 * NC * 2) % 16, qc = (e >> 2) % NC, qg = e & 3;
+        float4 x0 = make_float4(0.f, 0.f, 0.f, 0.f), x1 = x0;
+        if (e < 2 * HD) {
+            const float *qp = a.q + (size_t)min(q0 + qt, M - 1) * D + h * HD + qc * 32 + qg * 8;
+            x0 = *reinterpret_cast<const float4 *>(qp);
+            x1 = *reinterpret_cast<const float4 *>(qp + 4);
         }
-        const uint64_t anc = tok_ok ? sd->anc[tok] : 0ull;
+        const uint64_t anc_raw = sd->anc[min(tok, M - 1)];
+        Tile buf0, buf1;
+        if (wave < ntile) load(wave, buf0);
+        const uint64_t anc = tok_ok ? anc_raw : 0ull;
+        if (e < 2 * HD) {
+            const float qs = q0 + qt < M ? 1.f : 0.f;
+            x0.x *= qs; x0.y *= qs; x0.z *= qs; x0.w *= qs;
+            x1.x *= qs; x1.y *= qs; x1.z *= qs; x1.w *= qs;
+            bf16x8 hh, ll;
+            split_hi_lo(x0, x1, hh, ll);
+            sm_q[(qc * 2 + 0) * 64 + 16 * qg + qt] = __builtin_bit_cast(u32x4, hh);
+            sm_q[(qc * 2 + 1) * 64 + 16 * qg + qt] = __builtin_bit_cast(u32x4, ll);
+        }
+        __syncthreads();
+
         float m_run = -INFINITY, l_run = 0.f;
         f32x4 o[ND];
 #pragma unroll
         for (int dt = 0; dt < ND; ++dt) o[dt] = (f32x4){0.f, 0.f, 0.f, 0.f};
 
-        for (int t = wave; t < ntile; t += NW) {
-            load_v(t, vv);                              // needed after the softmax
-            if (t + NW < ntile) load_k(t + NW, nxt);    // the wave's next tile
+        auto process = [&](int t, Tile &cur) {
             const int k0 = kbeg + 32 * t;
             f32x4 sa = (f32x4){0.f, 0.f, 0.f, 0.f}, sb = sa;
 #pragma unroll
             for (int c = 0; c < NC; ++c) {
                 const bf16x8 ka8 = __builtin_bit_cast(bf16x8, cur.ka[c]);
                 const bf16x8 kb8 = __builtin_bit_cast(bf16x8, cur.kb[c]);
-                sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka8, qh[c], sa, 0, 0, 0);
-                sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka8, ql[c], sa, 0, 0, 0);
-                sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb8, qh[c], sb, 0, 0, 0);
-                sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb8, ql[c], sb, 0, 0, 0);
+                const bf16x8 qh = __builtin_bit_cast(bf16x8, sm_q[(c * 2 + 0) * 64 + lane]);
+                const bf16x8 ql = __builtin_bit_cast(bf16x8, sm_q[(c * 2 + 1) * 64 + lane]);
+                sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka8, qh, sa, 0, 0, 0);
+                sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb8, qh, sb, 0, 0, 0);
+                sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka8, ql, sa, 0, 0, 0);
+                sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb8, ql, sb, 0, 0, 0);
             }
             float sv[8];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                sv[j] = sa[j] * scale;
-                sv[4 + j] = sb[j] * scale;
-            }
             float mt = -INFINITY;
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
                 const int key = k0 + 8 * g + i;
-                bool vis = tok_ok && key < kend;
-                if (key >= P) vis = vis && ((anc >> (key - P)) & 1ull);
-                if (!vis) sv[i] = -INFINITY;
+                const int sh = key - P;
+                const bool tree_ok = sh < 0 || ((anc >> (sh & 63)) & 1ull);
+                const bool vis = key < kend && tree_ok;
+                const float sc = (i < 4 ? sa[i] : sb[i - 4]) * scale2;
+                sv[i] = vis ? sc : -INFINITY;
                 mt = fmaxf(mt, sv[i]);
             }
             mt = fmaxf(mt, __shfl_xor(mt, 16));
             mt = fmaxf(mt, __shfl_xor(mt, 32));
             const float mnew = fmaxf(m_run, mt);
-            float alpha = 1.f, ps = 0.f;
-            float pv[8];
-            if (mnew == -INFINITY) {
+            const float alpha = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - mnew);
+            float ps = 0.f, pv[8];
 #pragma unroll
-                for (int i = 0; i < 8; ++i) pv[i] = 0.f;
-            } else {
-                alpha = (m_run == -INFINITY) ? 0.f : expf(m_run - mnew);
-#pragma unroll
-                for (int i = 0; i < 8; ++i) {
-                    pv[i] = (sv[i] == -INFINITY) ? 0.f : expf(sv[i] - mnew);
-                    ps += pv[i];
-                }
+            for (int i = 0; i < 8; ++i) {
+                pv[i] = sv[i] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(sv[i] - mnew);
+                ps += pv[i];
             }
             ps += __shfl_xor(ps, 16);
             ps += __shfl_xor(ps, 32);
@@ -704,24 +722,31 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mfma(AttnArgs a)
 #pragma unroll
                     for (int w = 0; w < 4; ++w) {
                         const int key = k0 + 8 * g + 2 * w;
-                        uint32_t x = vv[dt][w];
+                        uint32_t x = cur.v[dt][w];
                         if (key >= kend) x &= 0xffff0000u;
                         if (key + 1 >= kend) x &= 0x0000ffffu;
-                        vv[dt][w] = x;
+                        cur.v[dt][w] = x;
                     }
             }
             bf16x8 ph, pl;
-            split_hi_lo(make_float4(pv[0], pv[1], pv[2], pv[3]), make_float4(pv[4], pv[5], pv[6], pv[7]),
-                        ph, pl);
+            split_hi_lo(make_float4(pv[0], pv[1], pv[2], pv[3]), make_float4(pv[4], pv[5], pv[6], pv[7]), ph, pl);
 #pragma unroll
             for (int dt = 0; dt < ND; ++dt) {
 #pragma unroll
                 for (int j = 0; j < 4; ++j) o[dt][j] *= al[j];
-                const bf16x8 v8 = __builtin_bit_cast(bf16x8, vv[dt]);
+                const bf16x8 v8 = __builtin_bit_cast(bf16x8, cur.v[dt]);
                 o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph, v8, o[dt], 0, 0, 0);
                 o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pl, v8, o[dt], 0, 0, 0);
             }
-            cur = nxt;
+        };
+        // two register buffers used in turn (no copies between them, so a
+        // load in flight is never waited on before its tile is used)
+        for (int t = wave; t < ntile; t += 2 * NW) {
+            if (t + NW < ntile) load(t + NW, buf1);
+            process(t, buf0);
+            if (t + NW >= ntile) break;
+            if (t + 2 * NW < ntile) load(t + 2 * NW, buf0);
+            process(t + NW, buf1);
         }
 
         // combine the waves (fixed wave order)
@@ -734,8 +759,8 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mfma(AttnArgs a)
 #pragma unroll
             for (int j = 0; j < 4; ++j) sm_o[wave][4 * g + j][dt * 16 + n] = o[dt][j];
         __syncthreads();
-        for (int e = threadIdx.x; e < 16 * HD; e += 64 * NW) {
-            const int i = e / HD, dd = e % HD;
+        for (int e2 = threadIdx.x; e2 < 16 * HD; e2 += 64 * NW) {
+            const int i = e2 / HD, dd = e2 % HD;
             const int ti = q0 + i;
             float mx = -INFINITY;
 #pragma unroll
@@ -744,8 +769,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mfma(AttnArgs a)
 #pragma unroll
             for (int w = 0; w < NW; ++w) {
                 const float mw = sm_m[w][i];
-                if (mw == -INFINITY) continue;
-                const float wgt = expf(mw - mx);
+                const float wgt = mw == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mw - mx);
                 l = fmaf(wgt, sm_l[w][i], l);
                 ov = fmaf(wgt, sm_o[w][i][dd], ov);
             }
@@ -759,7 +783,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mfma(AttnArgs a)
                 const size_t pb = ((size_t)h * a.n_split + split) * DV_TREE_MAX + ti;
                 a.part_o[pb * HD + dd] = ov;
                 if (dd == 0) {
-                    a.part_m[pb] = mx;
+                    a.part_m[pb] = mx * 0.6931471805599453f;  // back to natural-log units
                     a.part_l[pb] = l;
                 }
             }
@@ -1044,22 +1068,37 @@ __global__ __launch_bounds__(256) void k_kv_commit(CommitArgs a)
 template <int EPI, typename KV, int NW, int U, int TP>
 static const void *gemm_kernel_mfma(int mt)
 {
+    // more token tiles hold more accumulators: fewer k-steps per batch
     switch (mt) {
     case 1: return (const void *)k_gemm_mfma<1, EPI, KV, NW, U, TP>;
     case 2: return (const void *)k_gemm_mfma<2, EPI, KV, NW, (U > 4 ? U / 2 : 2), TP>;
     case 3: return (const void *)k_gemm_mfma<3, EPI, KV, 4, 2, TP>;
-    case 4: return (const void *)k_gemm_mfma<4, EPI, KV, 4, 2, TP>;
+    case 4: return (const void *)k_gemm_mfma<4, EPI, KV, 4, (TP > 2 ? 1 : 2), TP>;
     default: return nullptr;
     }
+}
+
+// index of an instantiated shape, -1 if none
+static int shape_index(GemmShape sh)
+{
+    if (sh.nw == 8 && sh.u == 4 && sh.tp == 2) return 0;
+    if (sh.nw == 4 && sh.u == 8 && sh.tp == 2) return 1;
+    if (sh.nw == 4 && sh.u == 4 && sh.tp == 4) return 2;
+    if (sh.nw == 4 && sh.u == 8 && sh.tp == 1) return 3;
+    return -1;
 }
 
 template <int EPI>
 static const void *gemm_kernel(int weight_bf16, int use_mfma, int mt, GemmShape sh)
 {
     if (weight_bf16 && use_mfma) {
-        if (sh.nw == 8 && sh.tp == 2) return gemm_kernel_mfma<EPI, uint16_t, 8, 4, 2>(mt);
-        if (sh.tp == 2) return gemm_kernel_mfma<EPI, uint16_t, 4, 8, 2>(mt);
-        return gemm_kernel_mfma<EPI, uint16_t, 4, 8, 1>(mt);
+        switch (shape_index(sh)) {
+        case 0: return gemm_kernel_mfma<EPI, uint16_t, 8, 4, 2>(mt);
+        case 1: return gemm_kernel_mfma<EPI, uint16_t, 4, 8, 2>(mt);
+        case 2: return gemm_kernel_mfma<EPI, uint16_t, 4, 4, 4>(mt);
+        case 3: return gemm_kernel_mfma<EPI, uint16_t, 4, 8, 1>(mt);
+        default: return nullptr;
+        }
     }
     if (weight_bf16) return (const void *)k_gemm_valu<uint16_t, EPI, uint16_t>;
     return (const void *)k_gemm_valu<float, EPI, float>;
@@ -1084,9 +1123,9 @@ static int gemm_threads(int weight_bf16, int use_mfma, int mt, GemmShape sh)
 
 int gemm_blocks_per_cu(int epi, int weight_bf16, int use_mfma, int mt, GemmShape sh)
 {
-    static int cache[4][2][2][5][2][2];
+    static int cache[4][2][2][5][5];
     int &c = cache[epi & 3][weight_bf16 ? 1 : 0][use_mfma ? 1 : 0][(mt >= 1 && mt <= 4) ? mt : 0]
-                  [sh.nw == 8 ? 1 : 0][sh.tp == 2 ? 1 : 0];
+                  [shape_index(sh) + 1];
     if (c == 0) {
         const void *k = gemm_kernel_any(epi, weight_bf16, use_mfma, mt, sh);
         int n = 0;
@@ -1126,6 +1165,7 @@ static hipError_t rmsnorm_dispatch_ks(const NormArgs &a, int Mpad, hipStream_t s
     case 2: hipLaunchKernelGGL((k_rmsnorm<W, NV, 2>), grid, block, 0, s, a); break;
     case 4: hipLaunchKernelGGL((k_rmsnorm<W, NV, 4>), grid, block, 0, s, a); break;
     case 8: hipLaunchKernelGGL((k_rmsnorm<W, NV, 8>), grid, block, 0, s, a); break;
+    case 16: hipLaunchKernelGGL((k_rmsnorm<W, NV, 16>), grid, block, 0, s, a); break;
     default: hipLaunchKernelGGL((k_rmsnorm<W, NV, -1>), grid, block, 0, s, a); break;
     }
     return hipGetLastError();
