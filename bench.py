@@ -27,6 +27,7 @@ import synth  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0
 # rocprofv3 FETCH_SIZE/WRITE_SIZE summary of the default workload (bytes per dispatch)
+HBM_WORKLOAD = "llama13b-bf16-m16-ctx1024"
 HBM_PROFILE = "verify_step_llama13b_m16_ctx1024_hbm_bytes.txt"
 
 
@@ -95,7 +96,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="llama13b-bf16-m16-ctx1024",
+    ap.add_argument("--workload", default=HBM_WORKLOAD,
                     help="one of %s, or sweep-M" % ", ".join(synth.WORKLOADS))
     ap.add_argument("--cpu-baseline", choices=["on", "off"], default="on")
     ap.add_argument("--roofline-events", choices=["inline", "off"], default="inline",
@@ -190,7 +191,9 @@ def main():
             per_launch = gbytes / glaunch
             achieved = per_launch / (avg_ms * 1e-3) / 1e9
             from paper_2412_18934_amd import profiling
-            traffic = profiling.gemm_traffic_per_launch(os.path.join(ROOT, "profiles", HBM_PROFILE))
+            # the committed counter summary covers the default workload only
+            traffic = (profiling.gemm_traffic_per_launch(os.path.join(ROOT, "profiles", HBM_PROFILE))
+                       if wl.name == HBM_WORKLOAD else None)
             roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                     "traffic": None if traffic is None else round(traffic),

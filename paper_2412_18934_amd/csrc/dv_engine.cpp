@@ -136,15 +136,16 @@ int gemm_units(const GemmPlan &p, int mt)
     return (p.mfma ? p.n_tiles / shape_for(p, mt).tp : p.n_tiles) * p.ks;
 }
 
-// Resident grid for a launch: every workgroup loops over an equal share of
-// the work units.
+// Resident grid for a launch.  Unit u runs on workgroup u % grid and the
+// workgroups of a resident grid are spread round-robin over the compute
+// units, so a grid of (workgroups per CU) x (CUs) gives every CU the same
+// number of units (within one); a grid sized to equalise units per
+// workgroup instead would leave some CUs with an extra workgroup.
 int gemm_grid(const GemmPlan &p, int epi, int bf16, int mt, int n_cu)
 {
     const int units = gemm_units(p, mt);
     const int cap = std::max(1, gemm_blocks_per_cu(epi, bf16, p.mfma, mt, shape_for(p, mt)) * n_cu);
-    if (units <= cap) return units;
-    const int per = ceil_div(units, cap);
-    return ceil_div(units, per);
+    return std::min(units, cap);
 }
 
 // Event pair for the next launch of class cls, or nullptr when that class is

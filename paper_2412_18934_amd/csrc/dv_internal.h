@@ -87,7 +87,8 @@ struct GemmArgs {
 // gather or split-K fold), writes x * gain and the sum of squares of each of
 // DV_NORM_SLICES column slices; the consuming projection multiplies its
 // outputs by 1/sqrt(sum/d + eps), a per-token scalar that commutes with W.
-#define DV_NORM_SLICES 4
+#define DV_NORM_SLICES 16
+#define DV_NORM_THREADS 128
 
 struct NormArgs {
     float *x;                  // [Mpad][d] residual stream

@@ -480,9 +480,9 @@ __global__ __launch_bounds__(256) void k_gemm_valu(GemmArgs a)
 // 256 threads x 4 consecutive floats per pass.
 
 template <typename W, int NV, int KS>
-__global__ __launch_bounds__(256) void k_rmsnorm(NormArgs a)
+__global__ __launch_bounds__(DV_NORM_THREADS) void k_rmsnorm(NormArgs a)
 {
-    constexpr int NT = 256, SPAN = 4 * NT;
+    constexpr int NT = DV_NORM_THREADS, SPAN = 4 * NT;
     const int m = blockIdx.x, sl = blockIdx.y, tid = threadIdx.x, d = a.d;
     const int c0 = sl * (d / DV_NORM_SLICES), c1 = c0 + d / DV_NORM_SLICES;
     float *urow = a.u + (size_t)m * d;
@@ -1159,7 +1159,7 @@ hipError_t launch_pack(const GemmArgs &a, int epi, uint16_t *dst, hipStream_t s)
 template <typename W, int NV>
 static hipError_t rmsnorm_dispatch_ks(const NormArgs &a, int Mpad, hipStream_t s)
 {
-    const dim3 grid(Mpad, DV_NORM_SLICES), block(256);
+    const dim3 grid(Mpad, DV_NORM_SLICES), block(DV_NORM_THREADS);
     switch (a.ks) {
     case 0: hipLaunchKernelGGL((k_rmsnorm<W, NV, 0>), grid, block, 0, s, a); break;
     case 2: hipLaunchKernelGGL((k_rmsnorm<W, NV, 2>), grid, block, 0, s, a); break;
@@ -1176,7 +1176,7 @@ static hipError_t rmsnorm_dispatch(const NormArgs &a, int Mpad, hipStream_t s)
 {
     const int slice = a.d / DV_NORM_SLICES;
     if (a.d % (4 * DV_NORM_SLICES)) return hipErrorInvalidValue;
-    switch ((slice + 1023) / 1024) {
+    switch ((slice + 4 * DV_NORM_THREADS - 1) / (4 * DV_NORM_THREADS)) {
     case 1: return rmsnorm_dispatch_ks<W, 1>(a, Mpad, s);
     case 2: return rmsnorm_dispatch_ks<W, 2>(a, Mpad, s);
     default: return hipErrorInvalidValue;
