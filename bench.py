@@ -37,14 +37,16 @@ def log(msg):
 
 def gemm_bytes(mc, m, esz):
     """Algorithmic bytes of the projection kernels in one step: weights once,
-    fp32 activations in once, outputs written once (residual: read + write)."""
+    activations in once (split bf16 hi + lo: 4 bytes per value), outputs out
+    once; the residual projections also read and write their rows of the
+    fp32 residual stream and write the next RMSNorm's input."""
     d, f, v, L = mc.d_model, mc.d_ffn, mc.vocab, mc.n_layers
     w = esz * (L * (4 * d * d + 3 * d * f) + v * d)
     per_layer = 4 * m * (d + d + 2 * d * esz / 4      # QKV: in, q out, k/v cache write
-                         + d + 2 * d                  # O: in, residual read+write
+                         + d + 2 * d + d              # O: in, residual read+write, next input
                          + d + f                      # gate/up: in, h out
-                         + f + 2 * d)                 # down: in, residual read+write
-    head = 4 * m * d + 8 * m * (v // 32)              # lm_head: in, per-tile argmax partials
+                         + f + 2 * d + d)             # down: in, residual read+write, next input
+    head = 4 * m * d + 8 * m * (v // 64)              # lm_head: in, per-group argmax partials
     return w + L * per_layer + head, 4 * L + 1
 
 
@@ -197,7 +199,7 @@ def main():
             roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                     "traffic": None if traffic is None else round(traffic),
-                    "kernel": "k_gemm_mfma (QKV, O, gate/up, down, lm_head projections)",
+                    "kernel": "k_proj (QKV, O, gate/up, down, lm_head projections)",
                     "bytes_per_launch": int(per_launch), "avg_launch_us": round(avg_ms * 1e3, 2),
                     "launches_per_step": glaunch, "ms_per_step_with_events": round(ms_r, 3)}
     sbytes = step_bytes(mc, m, p, esz)

@@ -24,8 +24,11 @@ struct LayerW {
 };
 
 struct GemmPlan {
-    int n_tiles = 0, ks = 1, k_per_split = 0, mfma = 0;
-    GemmShape shape{4, 8, 1};
+    int n_tiles = 0;   // 32-row tiles
+    int mfma = 0;      // MFMA kernel (bf16 weights, K % 32 == 0) or VALU
+    int rb = 0;        // MFMA: 16-row blocks per row group
+    int n_groups = 0;  // row groups (VALU: tiles)
+    int ks = 1;        // K splits per row group (residual projections)
 };
 
 struct ProfEv {
@@ -45,11 +48,13 @@ struct dv_handle {
 
     // workspace (device)
     float *x = nullptr, *u = nullptr, *q = nullptr, *attn = nullptr, *hbuf = nullptr;
-    float *ssq = nullptr;  // per-token sums of squares, [64][DV_NORM_SLICES]
+    float *ssq = nullptr;  // per-token partial sums of squares, [64][ssq_max]
+    int ssq_max = 0;
+    float *part_gemm = nullptr;  // split-K partials of the residual projections
+    uint32_t *cnt = nullptr;     // their per-row-group arrival counters
     uint16_t *u_s = nullptr, *attn_s = nullptr, *h_s = nullptr;  // split-layout activations
     float *part_o = nullptr, *part_m = nullptr, *part_l = nullptr;
     int attn_split_max = 0;
-    float *part_gemm = nullptr;
     float *arg_val = nullptr;
     int32_t *arg_idx = nullptr;
     float *rope_cos = nullptr, *rope_sin = nullptr;
@@ -106,46 +111,40 @@ int hip_fail(dv_handle *h, hipError_t e, const char *what)
 int ceil_div(int a, int b) { return (a + b - 1) / b; }
 int round_up(int a, int b) { return ceil_div(a, b) * b; }
 
-// Split-K is used only for projections that add into the residual stream
-// (their partials are folded in by the next RMSNorm).  ks is the requested
-// split count, reduced until each split keeps at least 4 load batches of k.
-GemmPlan make_plan(int n_tiles, int K, int align, int mfma, int ks, GemmShape shape)
+// Row groups of 4 blocks (2 where the block count is not a multiple of 4): a
+// workgroup then streams 4 KB of weights per 2 KB of shared activations per
+// k-step.  Residual projections (d_model rows, too few groups to cover the
+// CUs) split K so that groups x splits covers the CUs about once, keeping at
+// least 4 k-steps per wave and split; the last split to finish folds them.
+GemmPlan make_plan(int n_tiles, int K, int mfma, bool resid, int n_cu)
 {
     GemmPlan p;
     p.n_tiles = n_tiles;
     p.mfma = mfma;
-    p.shape = shape;
-    if (mfma && n_tiles % shape.tp) p.shape = GemmShape{4, 8, 1};
-    while (ks > 1 && K / ks < 4 * align) ks /= 2;
-    int kps = round_up(ceil_div(K, ks), align);
-    p.k_per_split = kps;
-    p.ks = ceil_div(K, kps);
+    if (mfma) {
+        const int blocks = 2 * n_tiles;
+        p.rb = blocks % 4 == 0 ? 4 : 2;
+        p.n_groups = blocks / p.rb;
+        if (resid) {
+            const int S = K / 32, nw = gemm_shape(p.rb).nw;
+            int ks = std::max(1, (n_cu + p.n_groups / 2) / p.n_groups);
+            ks = std::min(ks, std::max(1, S / (4 * nw)));
+            p.ks = std::min(ks, 16);
+        }
+    } else {
+        p.n_groups = n_tiles;
+    }
     return p;
 }
 
-// Shape used for mt token tiles: four tiles per workgroup hold too many
-// accumulators beyond 32 tokens, so those steps use two.
-GemmShape shape_for(const GemmPlan &p, int mt)
-{
-    if (p.shape.tp > 2 && mt >= 3) return p.n_tiles % 2 ? GemmShape{4, 8, 1} : GemmShape{4, 8, 2};
-    return p.shape;
-}
+int gemm_units(const GemmPlan &p) { return p.n_groups * p.ks; }
 
-int gemm_units(const GemmPlan &p, int mt)
-{
-    return (p.mfma ? p.n_tiles / shape_for(p, mt).tp : p.n_tiles) * p.ks;
-}
-
-// Resident grid for a launch.  Unit u runs on workgroup u % grid and the
-// workgroups of a resident grid are spread round-robin over the compute
-// units, so a grid of (workgroups per CU) x (CUs) gives every CU the same
-// number of units (within one); a grid sized to equalise units per
-// workgroup instead would leave some CUs with an extra workgroup.
+// Grid of a launch: every unit its own workgroup, capped at what the CUs hold
+// at once (the workgroups then loop over the units).
 int gemm_grid(const GemmPlan &p, int epi, int bf16, int mt, int n_cu)
 {
-    const int units = gemm_units(p, mt);
-    const int cap = std::max(1, gemm_blocks_per_cu(epi, bf16, p.mfma, mt, shape_for(p, mt)) * n_cu);
-    return std::min(units, cap);
+    const int cap = std::max(1, gemm_blocks_per_cu(epi, bf16, p.mfma, mt, p.rb) * n_cu);
+    return std::min(gemm_units(p), cap);
 }
 
 // Event pair for the next launch of class cls, or nullptr when that class is
@@ -242,21 +241,17 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
     g.rope_cos = h->rope_cos;
     g.rope_sin = h->rope_sin;
     g.pos = h->d_sd->pos;
-    g.part = h->part_gemm;
-    g.ssq = h->ssq;
     g.eps = c.rms_eps;
     g.dn = d;
+    g.resid = h->x;
+    g.u = h->u;
+    g.us = h->bf16 ? h->u_s : nullptr;  // x * gain feeds QKV, gate/up and lm_head
+    g.ssq_out = h->ssq;
+    g.part = h->part_gemm;
+    g.cnt = h->cnt;
     g.out_split = h->p_down.mfma ? h->h_s : nullptr;  // SWIGLU output feeds the down projection
-
-    NormArgs na{};
-    na.d = d;
-    na.ssq = h->ssq;
-    na.M = M;
-    na.tokens = h->d_sd->tokens;
-    na.u = h->u;
-    na.x = h->x;
-    na.part = h->part_gemm;
-    na.us = h->bf16 ? h->u_s : nullptr;  // norm output feeds QKV, gate/up and lm_head
+    g.ssq_in = h->ssq;
+    g.n_ssq_in = DV_NORM_SLICES;  // the embedding norm's slices feed the first QKV
 
     AttnArgs aa{};
     aa.q = h->q;
@@ -272,10 +267,9 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
     aa.out = h->attn;
     aa.out_split = h->p_o.mfma ? h->attn_s : nullptr;
 
-    int pending_ks = 0;  // split-K partials of the last residual projection, not yet folded
     auto gemm = [&](const GemmPlan &p, int epi, const void *w0, const void *w1, const void *w2,
                     const uint16_t *packed, int N, int K, const float *x, const uint16_t *xs,
-                    float *out) -> int {
+                    float *out, const void *gain) -> int {
         GemmArgs a = g;
         a.packed = packed;
         a.xs = xs;
@@ -285,39 +279,44 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
         a.N = N;
         a.K = K;
         a.n_tiles = p.n_tiles;
+        a.rb = p.rb;
+        a.n_groups = p.n_groups;
         a.ks = p.ks;
-        a.k_per_split = p.k_per_split;
-        a.n_units = gemm_units(p, Mpad / 16);
+        a.n_units = gemm_units(p);
         a.x = x;
         a.out = out;
+        a.gain = gain;
         const int grid = gemm_grid(p, epi, h->bf16, Mpad / 16, h->n_cu);
         ProfEv *ev = prof_pair(h, DV_K_GEMM);
-        hipError_t e = launch_gemm(a, grid, epi, h->bf16, p.mfma, shape_for(p, Mpad / 16), s, ev ? ev->a : nullptr,
-                                   ev ? ev->b : nullptr);
+        hipError_t e = launch_gemm(a, grid, epi, h->bf16, p.mfma, s, ev ? ev->a : nullptr, ev ? ev->b : nullptr);
         if (e != hipSuccess) return hip_fail(h, e, "gemm launch");
-        if (epi == EPI_RESID) pending_ks = p.ks > 1 ? p.ks : 0;
-        return DV_OK;
-    };
-    auto norm = [&](const void *gain, const void *embed) -> int {
-        NormArgs a = na;
-        a.gain = gain;
-        a.embed = embed;
-        a.ks = embed ? 0 : pending_ks;
-        pending_ks = 0;
-        prof_begin(h, DV_K_NORM);
-        hipError_t e = launch_rmsnorm(a, Mpad, h->bf16, s);
-        prof_end(h);
-        if (e != hipSuccess) return hip_fail(h, e, "rmsnorm launch");
+        // the next projection normalises with this one's sums of squares
+        if (epi == EPI_RESID) g.n_ssq_in = p.n_groups;
         return DV_OK;
     };
 
+    {
+        NormArgs na{};
+        na.x = h->x;
+        na.embed = h->embed;
+        na.gain = h->layers[0].attn_norm;
+        na.u = h->u;
+        na.us = h->bf16 ? h->u_s : nullptr;
+        na.ssq = h->ssq;
+        na.d = d;
+        na.M = M;
+        na.tokens = h->d_sd->tokens;
+        prof_begin(h, DV_K_NORM);
+        hipError_t e = launch_embed_norm(na, Mpad, h->bf16, s);
+        prof_end(h);
+        if (e != hipSuccess) return hip_fail(h, e, "embedding norm launch");
+    }
     int rc;
     for (int l = 0; l < c.n_layers; ++l) {
         const LayerW &w = h->layers[l];
-        if ((rc = norm(w.attn_norm, l == 0 ? h->embed : nullptr))) return rc;
         g.kc = (char *)kv->k + l * layer_kv;
         g.vc = (char *)kv->v + l * layer_kv;
-        if ((rc = gemm(h->p_qkv, EPI_QKV, w.wq, w.wk, w.wv, w.pk_qkv, d, d, h->u, h->u_s, h->q)))
+        if ((rc = gemm(h->p_qkv, EPI_QKV, w.wq, w.wk, w.wv, w.pk_qkv, d, d, h->u, h->u_s, h->q, nullptr)))
             return rc;
         aa.kc = g.kc;
         aa.vc = g.vc;
@@ -326,32 +325,27 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
         if (e == hipSuccess && n_split > 1) e = launch_attn_merge(aa, Mpad, s);
         prof_end(h);
         if (e != hipSuccess) return hip_fail(h, e, "attention launch");
-        if ((rc = gemm(h->p_o, EPI_RESID, w.wo, nullptr, nullptr, w.pk_o, d, d, h->attn, h->attn_s,
-                       h->x)))
+        if ((rc = gemm(h->p_o, EPI_RESID, w.wo, nullptr, nullptr, w.pk_o, d, d, h->attn, h->attn_s, nullptr,
+                       w.ffn_norm)))
             return rc;
-        if ((rc = norm(w.ffn_norm, nullptr))) return rc;
-        if ((rc = gemm(h->p_gu, EPI_SWIGLU, w.w_gate, w.w_up, nullptr, w.pk_gu, F, d, h->u, h->u_s,
-                       h->hbuf)))
+        if ((rc = gemm(h->p_gu, EPI_SWIGLU, w.w_gate, w.w_up, nullptr, w.pk_gu, F, d, h->u, h->u_s, h->hbuf,
+                       nullptr)))
             return rc;
-        if ((rc = gemm(h->p_down, EPI_RESID, w.w_down, nullptr, nullptr, w.pk_down, d, F, h->hbuf,
-                       h->h_s, h->x)))
+        const void *next_gain = l + 1 < c.n_layers ? h->layers[l + 1].attn_norm : h->final_norm;
+        if ((rc = gemm(h->p_down, EPI_RESID, w.w_down, nullptr, nullptr, w.pk_down, d, F, h->hbuf, h->h_s,
+                       nullptr, next_gain)))
             return rc;
     }
     if (!with_head) return DV_OK;
-    if ((rc = norm(h->final_norm, nullptr))) return rc;
-    {
-        GemmArgs a = g;
-        a.arg_val = h->arg_val;
-        a.arg_idx = h->arg_idx;
-        g = a;
-    }
-    if ((rc = gemm(h->p_lm, EPI_LOGITS, h->lm_head, nullptr, nullptr, h->pk_lm, c.vocab, d, h->u,
-                   h->u_s, out_logits)))
+    g.arg_val = h->arg_val;
+    g.arg_idx = h->arg_idx;
+    if ((rc = gemm(h->p_lm, EPI_LOGITS, h->lm_head, nullptr, nullptr, h->pk_lm, c.vocab, d, h->u, h->u_s,
+                   out_logits, nullptr)))
         return rc;
     AcceptArgs ac{};
     ac.arg_val = h->arg_val;
     ac.arg_idx = h->arg_idx;
-    ac.n_tiles = h->p_lm.n_tiles;
+    ac.n_parts = h->p_lm.n_groups;
     ac.sd = h->d_sd;
     ac.acc = h->d_acc;
     prof_begin(h, DV_K_OTHER);
@@ -471,18 +465,22 @@ int dv_verify_init(const dv_config *cfg, const dv_weights *w, void *stream, dv_h
             ncu > 0)
             h->n_cu = ncu;
     }
-    const int al = mf ? 32 : 8;
-    // shapes and K splits measured on MI355X for the weight-streaming regime
-    // (13B-sized projections, weights read once from HBM per step)
-    const GemmShape wide8{8, 4, 2}, wide4{4, 8, 2}, quad{4, 4, 4}, narrow{4, 8, 1};
-    h->p_qkv = make_plan(3 * d / DV_GEMM_TILE, d, al, mf, 1, wide8);
-    h->p_o = make_plan(d / DV_GEMM_TILE, d, al, mf, 8, narrow);
-    h->p_gu = make_plan(F / 16, d, al, mf, 1, quad);
     const int mf_down = mf && (F % 32 == 0);
-    h->p_down = make_plan(d / DV_GEMM_TILE, F, mf_down ? 32 : 8, mf_down, 16, wide8);
-    h->p_lm = make_plan(V / DV_GEMM_TILE, d, al, mf, 1, wide4);
+    h->p_qkv = make_plan(3 * d / DV_GEMM_TILE, d, mf, false, h->n_cu);
+    h->p_o = make_plan(d / DV_GEMM_TILE, d, mf, true, h->n_cu);
+    h->p_gu = make_plan(F / 16, d, mf, false, h->n_cu);
+    h->p_down = make_plan(d / DV_GEMM_TILE, F, mf_down, true, h->n_cu);
+    h->p_lm = make_plan(V / DV_GEMM_TILE, d, mf, false, h->n_cu);
 
-    const size_t part_elems = (size_t)std::max(h->p_o.ks, h->p_down.ks) * DV_TREE_MAX * d;
+    // split-K partials: units x rb x (64 tokens / 16) x 64 lanes x 4 floats
+    size_t part_elems = 16;
+    int cnt_n = 1;
+    for (const GemmPlan *p : {&h->p_o, &h->p_down})
+        if (p->ks > 1) {
+            part_elems = std::max(part_elems, (size_t)gemm_units(*p) * p->rb * 4 * 64 * 4);
+            cnt_n = std::max(cnt_n, p->n_groups);
+        }
+    h->ssq_max = std::max({DV_NORM_SLICES, h->p_o.n_groups, h->p_down.n_groups});
     h->attn_split_max = std::max(ceil_div(c.max_ctx, DV_ATTN_SPLIT_KEYS), ceil_div(512, H));
 
     auto dalloc = [&](void **p, size_t bytes) -> bool {
@@ -493,7 +491,8 @@ int dv_verify_init(const dv_config *cfg, const dv_weights *w, void *stream, dv_h
     bool ok = dalloc((void **)&h->x, rows * d * 4) && dalloc((void **)&h->u, rows * d * 4) &&
               dalloc((void **)&h->q, rows * d * 4) && dalloc((void **)&h->attn, rows * d * 4) &&
               dalloc((void **)&h->hbuf, rows * F * 4) &&
-              dalloc((void **)&h->ssq, rows * DV_NORM_SLICES * 4) &&
+              dalloc((void **)&h->ssq, rows * h->ssq_max * 4) &&
+              dalloc((void **)&h->cnt, (size_t)cnt_n * 4) &&
               dalloc((void **)&h->u_s, (size_t)d * 2 * rows * 2) &&
               dalloc((void **)&h->attn_s, (size_t)d * 2 * rows * 2) &&
               dalloc((void **)&h->h_s, (size_t)F * 2 * rows * 2) &&
@@ -501,8 +500,8 @@ int dv_verify_init(const dv_config *cfg, const dv_weights *w, void *stream, dv_h
               dalloc((void **)&h->part_m, (size_t)H * h->attn_split_max * rows * 4) &&
               dalloc((void **)&h->part_l, (size_t)H * h->attn_split_max * rows * 4) &&
               dalloc((void **)&h->part_gemm, part_elems * 4) &&
-              dalloc((void **)&h->arg_val, (size_t)h->p_lm.n_tiles * rows * 4) &&
-              dalloc((void **)&h->arg_idx, (size_t)h->p_lm.n_tiles * rows * 4) &&
+              dalloc((void **)&h->arg_val, (size_t)h->p_lm.n_groups * rows * 4) &&
+              dalloc((void **)&h->arg_idx, (size_t)h->p_lm.n_groups * rows * 4) &&
               dalloc((void **)&h->rope_cos, (size_t)c.max_ctx * (hd / 2) * 4) &&
               dalloc((void **)&h->rope_sin, (size_t)c.max_ctx * (hd / 2) * 4) &&
               dalloc((void **)&h->d_sd, sizeof(StepDesc)) &&
@@ -548,6 +547,8 @@ int dv_verify_init(const dv_config *cfg, const dv_weights *w, void *stream, dv_h
             a.N = N;
             a.K = K;
             a.n_tiles = p.n_tiles;
+            a.rb = p.rb;
+            a.n_groups = p.n_groups;
             a.hd = hd;
             return launch_pack(a, epi, *dst, nullptr) == hipSuccess;
         };
@@ -701,7 +702,7 @@ void dv_verify_free(dv_handle *h)
     else (void)hipDeviceSynchronize();
     for (void *p : {(void *)h->x, (void *)h->u, (void *)h->q, (void *)h->attn, (void *)h->hbuf,
                     (void *)h->u_s, (void *)h->attn_s, (void *)h->h_s, (void *)h->ssq,
-                    (void *)h->part_o, (void *)h->part_m, (void *)h->part_l,  (void *)h->part_gemm,
+                    (void *)h->part_o, (void *)h->part_m, (void *)h->part_l, (void *)h->part_gemm, (void *)h->cnt,
                     (void *)h->arg_val, (void *)h->arg_idx, (void *)h->rope_cos,
                     (void *)h->rope_sin, (void *)h->d_sd, (void *)h->d_acc})
         if (p) (void)hipFree(p);

@@ -43,58 +43,74 @@ enum GemmEpi { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LOGITS = 3 };
 // Block (s, mt, p) starts at element ((s MT + mt) 2 + p) 512.
 // Size: K/32 * MT * 2 * 512 bf16 = 64 K MT bytes.
 
-// GEMM variants (MFMA path): waves per workgroup, k-steps per load batch
-// and tiles per work unit; supported: {8, 4, 2}, {4, 8, 2}, {4, 8, 1}
-// Workgroup shape of the MFMA projection kernel: nw waves, u k-steps per
-// batch of loads, tp tiles sharing the activation operand.  Instantiated
-// shapes: {8,4,2}, {4,8,2}, {4,4,4}, {4,8,1}.
-struct GemmShape {
-    int nw;
-    int u;
-    int tp;
-};
-
+// Projection weights, MFMA path.  The output rows are cut into 16-row
+// blocks; rb consecutive blocks form a row group (one work unit, or ks units
+// when the reduction is split).  Weights are stored k-major: the 1 KB block
+// of (k-step s, group g, block b) -- 16 rows x 32 columns in A-operand lane
+// order, lane l holding row l%16, columns 32 s + 8 (l/16) .. +8 -- starts at
+// element ((s G + g) rb + b) 512.  Blocks pair up into 32-row tiles (b even,
+// b + 1) whose halves the epilogues combine:
+//   QKV:    dims [j0, j0+16) of one head | dims j0+hd/2+[0,16) (rotary pairs),
+//           segments q | k | v one after another;
+//   SWIGLU: gate rows [16t, 16t+16) | the same up rows;
+//   else:   rows [32t, 32t+16) | [32t+16, 32t+32).
 struct GemmArgs {
     const void *w0, *w1, *w2;  // QKV: wq, wk, wv; SWIGLU: w_gate, w_up; else w0
-    const uint16_t *packed;    // bf16 MFMA path: the matrices in tile order (see
-                               // k_pack_tiles), read instead of w0..w2
+    const uint16_t *packed;    // MFMA path: the weights in block order (above)
     int32_t N;                 // rows of one matrix (d_model, d_ffn or vocab)
     int32_t K;                 // reduction length (row length of the matrices)
-    int32_t n_tiles;           // tiles of DV_GEMM_TILE logical rows
-    int32_t ks;                // split-K factor (RESID only; partials go to `part`)
-    int32_t k_per_split;       // reduction elements per split (multiple of 32)
-    int32_t n_units;           // n_tiles * ks work units, looped over by the grid
-    const float *x;            // VALU path: activations [Mpad][K], rows >= M are zero
-    const uint16_t *xs;        // MFMA path: the same activations pre-split (split layout)
+    int32_t n_tiles;           // 32-row tiles (QKV counts the three matrices)
+    int32_t rb;                // MFMA path: 16-row blocks per row group (2 or 4)
+    int32_t n_groups;          // row groups: MFMA 2 n_tiles / rb; VALU n_tiles
+    int32_t ks;                // K splits per row group (RESID, MFMA path only)
+    int32_t n_units;           // n_groups * ks
+    const float *x;            // VALU path: activations [Mpad][K], fp32
+    const uint16_t *xs;        // MFMA path: the same activations in split layout
     int32_t M, Mpad;
-    float *out;                // QKV: q [Mpad][d]; RESID (ks == 1): x [.][N];
-                               // SWIGLU: h [Mpad][N]; LOGITS: logits [M][N] or null
-    uint16_t *out_split;       // SWIGLU: h in split layout instead of `out` when set
-    void *kc, *vc;             // QKV: this layer's K/V cache [H][cap][hd]
+    float *out;                // QKV: q [Mpad][d]; SWIGLU: h [Mpad][N] (VALU
+                               // consumer); LOGITS: logits [M][N] or null
+    uint16_t *out_split;       // SWIGLU: h in split layout (MFMA consumer)
+    void *kc, *vc;             // QKV: this layer's K/V cache
     int32_t cap, P, hd;
     const float *rope_cos, *rope_sin;  // [max_ctx][hd/2]
     const int32_t *pos;        // QKV: device StepDesc.pos
-    float *part;               // RESID, ks > 1: partial sums [ks][64][N], folded
-                               // into the residual stream by the next k_rmsnorm
-    const float *ssq;          // QKV, SWIGLU, LOGITS: sums of squares from k_rmsnorm;
-    float eps;                 // outputs are scaled by 1/sqrt(sum/dn + eps) per token
+    // input normalisation (QKV, SWIGLU, LOGITS): the activations are x * gain
+    // of an RMSNorm whose 1/rms, a per-token scalar that commutes with W, is
+    // applied to the outputs: 1/sqrt(sum_j ssq_in[m][j] / dn + eps)
+    const float *ssq_in;       // [Mpad][n_ssq_in] partial sums of squares
+    int32_t n_ssq_in;
+    float eps;
     int32_t dn;
-    float *arg_val;            // LOGITS: per-tile max    [64][n_tiles]
-    int32_t *arg_idx;          // LOGITS: per-tile argmax [64][n_tiles]
+    // RESID: the residual stream x [Mpad][N] += W a; then the next RMSNorm's
+    // numerator x * gain is written for the consuming projection, with the
+    // per-group sums of squares of x
+    float *resid;
+    const void *gain;          // [N], weight dtype
+    float *u;                  // x * gain, fp32 [Mpad][N] (VALU consumer), or
+    uint16_t *us;              // in split layout (MFMA consumer)
+    float *ssq_out;            // [Mpad][n_groups]
+    float *part;               // ks > 1: per-unit partial sums
+    uint32_t *cnt;             // ks > 1: arrivals per row group, 0 between launches
+    float *arg_val;            // LOGITS: per-group max    [64][n_groups]
+    int32_t *arg_idx;          // LOGITS: per-group argmax [64][n_groups]
 };
 
-// RMSNorm is split in two: k_rmsnorm completes the residual row (embedding
-// gather or split-K fold), writes x * gain and the sum of squares of each of
-// DV_NORM_SLICES column slices; the consuming projection multiplies its
-// outputs by 1/sqrt(sum/d + eps), a per-token scalar that commutes with W.
+// Workgroup shape of the MFMA projection kernel: nw waves, u k-steps of loads
+// in flight per wave.  Instantiated: {4, 2} with rb 4, {4, 4} with rb 2.
+struct GemmShape {
+    int nw;
+    int u;
+};
+
+// The first RMSNorm of a step (on the token embeddings): k_embed_norm
+// gathers the rows into the residual stream, writes x * gain for the first
+// projection and the sums of squares of DV_NORM_SLICES column slices.
 #define DV_NORM_SLICES 16
 #define DV_NORM_THREADS 128
 
 struct NormArgs {
-    float *x;                  // [Mpad][d] residual stream
-    const void *embed;         // when set: x = embedding rows of the tokens first
-    const float *part;         // when ks > 0: x += sum_s part[s][m][:] first
-    int32_t ks;
+    float *x;                  // [Mpad][d] residual stream (written)
+    const void *embed;         // [V][d] token embeddings, weight dtype
     const void *gain;          // [d] weight dtype
     float *u;                  // [Mpad][d] x * gain (fp32), or
     uint16_t *us;              // the same in split layout when set
@@ -117,9 +133,9 @@ struct AttnArgs {
 };
 
 struct AcceptArgs {
-    const float *arg_val;      // [64][n_tiles]
+    const float *arg_val;      // [64][n_parts] per-group (max, argmax) of the logits
     const int32_t *arg_idx;
-    int32_t n_tiles;
+    int32_t n_parts;
     const StepDesc *sd;
     DevAccept *acc;
 };
@@ -131,14 +147,16 @@ struct CommitArgs {
 };
 
 // launchers (dv_kernels.hip); each returns the launch status
-// copy a projection's bf16 rows into MFMA tile order (init time)
+// copy a projection's bf16 rows into MFMA block order (init time)
 hipError_t launch_pack(const GemmArgs &a, int epi, uint16_t *dst, hipStream_t s);
-// workgroups of 256 threads one CU can hold for a GEMM variant (cached)
-int gemm_blocks_per_cu(int epi, int weight_bf16, int use_mfma, int mt, GemmShape sh);
+// the MFMA workgroup shape used for row groups of rb blocks
+GemmShape gemm_shape(int rb);
+// workgroups one CU can hold for a GEMM variant (cached)
+int gemm_blocks_per_cu(int epi, int weight_bf16, int use_mfma, int mt, int rb);
 // ev_start/ev_stop (optional, both or neither): timestamps of this launch
 hipError_t launch_gemm(const GemmArgs &a, int grid, int epi, int weight_bf16, int use_mfma,
-                       GemmShape sh, hipStream_t s, hipEvent_t ev_start, hipEvent_t ev_stop);
-hipError_t launch_rmsnorm(const NormArgs &a, int Mpad, int weight_bf16, hipStream_t s);
+                       hipStream_t s, hipEvent_t ev_start, hipEvent_t ev_stop);
+hipError_t launch_embed_norm(const NormArgs &a, int Mpad, int weight_bf16, hipStream_t s);
 hipError_t launch_attention(const AttnArgs &a, int kv_bf16, hipStream_t s);
 hipError_t launch_attn_merge(const AttnArgs &a, int Mpad, hipStream_t s);
 hipError_t launch_accept(const AcceptArgs &a, hipStream_t s);

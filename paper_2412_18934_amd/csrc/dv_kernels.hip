@@ -2,12 +2,13 @@
 //
 // Step structure (Section 3.1 of the paper: one forward pass of the target
 // over the candidate tokens, then the acceptance rule):
-//   k_rmsnorm        embedding gather (first layer) + RMSNorm -> fp32 rows
-//   k_gemm_*         weight-streaming projections with fused epilogues:
-//                      QKV    -> rotary embedding, q store, K/V cache write
+//   k_embed_norm     embedding gather + the first RMSNorm
+//   k_proj / k_gemm_valu  weight-streaming projections with fused epilogues:
+//                      QKV    -> 1/rms, rotary embedding, q store, K/V cache write
 //                      RESID  -> residual add into the fp32 stream (O, down)
-//                      SWIGLU -> silu(gate) * up
-//                      LOGITS -> logits + per-tile argmax
+//                                and the next RMSNorm's x * gain and sums of squares
+//                      SWIGLU -> 1/rms, silu(gate) * up
+//                      LOGITS -> 1/rms, logits + per-group argmax
 //   k_attn / merge   tree-masked attention over the cache, split over keys
 //   k_accept         vocab-wide argmax reduce + greedy acceptance walk
 //   k_kv_commit      in-place compaction of the accepted path
@@ -104,15 +105,9 @@ __device__ __forceinline__ void store_split4(uint16_t *xs, int m, int k, int MT,
 }
 
 // ---------------------------------------------------------------------------
-// GEMM tile -> weight rows
-//
-// A workgroup tile has DV_GEMM_TILE = 32 logical rows made of two halves of
-// 16.  The halves map to physical rows so that each epilogue finds the pair
-// of values it needs in the same tile:
-//   QKV:    half 0 = dims [j0, j0+16) of one head, half 1 = dims j0+hd/2+..
-//           (the rotary pairs), segments q | k | v one after another;
-//   SWIGLU: half 0 = gate rows [16t, 16t+16), half 1 = the same up rows;
-//   else:   rows [32t, 32t+32) of w0.
+// Projection rows.  A 32-row tile is two 16-row halves (MFMA blocks) mapped to
+// physical rows so that each epilogue finds the pair of values it needs in
+// the same tile (see GemmArgs in dv_internal.h).
 
 struct RowMap {
     const void *ptr[2];
@@ -143,58 +138,105 @@ __device__ __forceinline__ RowMap row_map(const GemmArgs &a, int epi, int t)
     return m;
 }
 
-// ---------------------------------------------------------------------------
-// GEMM epilogues on the tile in LDS
-//
-// tileY[m][r] (m < Mpad, r < 32) holds one work unit's sums.  A tile is
-// owned by exactly one workgroup unless the projection is split over K
-// (RESID only): then each split stores its partial tile and the next
-// k_rmsnorm adds the splits into the residual stream in split order, so no
-// workgroup ever waits for another and the sum order is fixed.
-
-#define TILE_LD (DV_GEMM_TILE + 1)
-
 __device__ __forceinline__ float silu(float z) { return z / (1.0f + expf(-z)); }
 
-template <int EPI, typename KV>
-__device__ void gemm_epilogue(const GemmArgs &a, float (*tileY)[TILE_LD], int t, int ksl)
+// ---------------------------------------------------------------------------
+// Projection epilogues.  Y[m * ld + r] (m < Mpad, r < rows) holds the
+// complete sums of one row group's rows for token m.
+
+// 1/rms of each token of the input from the producer's partial sums of
+// squares, in a fixed order: thread 4 m + c sums partials c, c + 4, ...
+// (loads issued together), then the four chains are combined by shuffles.
+// Needs 4 Mpad <= blockDim.x; writes rinv[0..Mpad).
+__device__ __forceinline__ void input_rinv(const GemmArgs &a, float *rinv)
 {
-    const int tid = threadIdx.x;
-    if (EPI != EPI_RESID) {
-        // 1/rms of each token (the normalisation the input skipped)
-        __shared__ float rinv[DV_TREE_MAX];
-        if (tid < a.Mpad) {
-            float r = 0.f;
-            if (tid < a.M) {
-                float sq = 0.f;
+    constexpr int NJ = 32;  // loads in flight per thread
+    const int tid = threadIdx.x, m = tid >> 2, c = tid & 3;
+    float s = 0.f;
+    if (m < a.Mpad) {
+        const float *p = a.ssq_in + (size_t)m * a.n_ssq_in;
+        for (int base = 0; base < a.n_ssq_in; base += 4 * NJ) {
+            float v[NJ];
 #pragma unroll
-                for (int sl = 0; sl < DV_NORM_SLICES; ++sl) sq += a.ssq[tid * DV_NORM_SLICES + sl];
-                r = 1.0f / sqrtf(sq / (float)a.dn + a.eps);
+            for (int j = 0; j < NJ; ++j) {
+                const int i = base + c + 4 * j;
+                v[j] = i < a.n_ssq_in ? p[i] : 0.f;
             }
-            rinv[tid] = r;
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) s += v[j];
         }
-        __syncthreads();
-        for (int e = tid; e < a.Mpad * DV_GEMM_TILE; e += blockDim.x)
-            tileY[e / DV_GEMM_TILE][e % DV_GEMM_TILE] *= rinv[e / DV_GEMM_TILE];
-        __syncthreads();
     }
-    if (EPI == EPI_RESID) {
-        if (a.ks > 1) {
-            float *dst = a.part + (size_t)ksl * DV_TREE_MAX * a.N + t * DV_GEMM_TILE;
-            for (int e = tid; e < a.M * DV_GEMM_TILE; e += blockDim.x) {
-                const int m = e / DV_GEMM_TILE, r = e % DV_GEMM_TILE;
-                dst[(size_t)m * a.N + r] = tileY[m][r];
-            }
-        } else {
-            for (int e = tid; e < a.M * DV_GEMM_TILE; e += blockDim.x) {
-                const int m = e / DV_GEMM_TILE, r = e % DV_GEMM_TILE;
-                a.out[(size_t)m * a.N + t * DV_GEMM_TILE + r] += tileY[m][r];
-            }
+    s += __shfl_xor(s, 1);
+    s += __shfl_xor(s, 2);
+    if (m < a.Mpad && c == 0) rinv[m] = m < a.M ? 1.0f / sqrtf(s / (float)a.dn + a.eps) : 0.f;
+}
+
+// Residual projections: x += sums, then the next RMSNorm's numerator
+// u = x * gain (split layout or fp32) and the group's sums of squares.
+// Rows [row0, row0 + nrows) of the stream.  With y_is_x, Y already holds the
+// updated rows x + sums and gain_s the gains of the rows (both staged in LDS
+// by the caller); otherwise Y holds the sums and both are read here.  Y ends
+// up holding x.
+template <typename W>
+__device__ void resid_epilogue(const GemmArgs &a, float *Y, int ld, int row0, int nrows, int group, bool y_is_x,
+                               const float *gain_s)
+{
+    const int tid = threadIdx.x, nt = blockDim.x;
+    const W *gp = reinterpret_cast<const W *>(a.gain);
+    for (int e = tid; e < a.Mpad * nrows; e += nt) {
+        const int m = e / nrows, r = e - m * nrows;
+        float v = 0.f;
+        if (m < a.M) {
+            float *xp = a.resid + (size_t)m * a.N + row0 + r;
+            v = y_is_x ? Y[m * ld + r] : *xp + Y[m * ld + r];
+            *xp = v;
         }
-    } else if (EPI == EPI_SWIGLU) {
-        for (int e = tid; e < a.Mpad * 16; e += blockDim.x) {
+        Y[m * ld + r] = v;
+    }
+    __syncthreads();
+    auto gain = [&](int r) -> float { return gain_s ? gain_s[r] : Elem<W>::load(gp, row0 + r); };
+    if (a.us) {
+        // 8 consecutive rows of one token per thread: one 16-byte hi and lo store
+        const int MT = a.Mpad >> 4, nc = nrows >> 3;
+        for (int e = tid; e < a.Mpad * nc; e += nt) {
+            const int m = e / nc, c = e - m * nc;
+            const float *y = Y + m * ld + 8 * c;
+            const int r = 8 * c;
+            const float4 v0 = make_float4(y[0] * gain(r), y[1] * gain(r + 1), y[2] * gain(r + 2), y[3] * gain(r + 3));
+            const float4 v1 = make_float4(y[4] * gain(r + 4), y[5] * gain(r + 5), y[6] * gain(r + 6), y[7] * gain(r + 7));
+            bf16x8 hi, lo;
+            split_hi_lo(v0, v1, hi, lo);
+            const size_t i = split_index(m, row0 + r, MT);
+            *reinterpret_cast<bf16x8 *>(a.us + i) = hi;
+            *reinterpret_cast<bf16x8 *>(a.us + i + 512) = lo;
+        }
+    } else {
+        for (int e = tid; e < a.Mpad * nrows; e += nt) {
+            const int m = e / nrows, r = e - m * nrows;
+            a.u[(size_t)m * a.N + row0 + r] = Y[m * ld + r] * gain(r);
+        }
+    }
+    // sums of squares: 4 threads per token, fixed order
+    if (tid < 4 * a.Mpad) {
+        const int m = tid >> 2, c = tid & 3;
+        float s = 0.f;
+        for (int r = c; r < nrows; r += 4) s = fmaf(Y[m * ld + r], Y[m * ld + r], s);
+        s += __shfl_xor(s, 1);
+        s += __shfl_xor(s, 2);
+        if (c == 0) a.ssq_out[(size_t)m * a.n_groups + group] = s;
+    }
+}
+
+// Non-residual epilogues for the 32-row tile t held in Y[m * ld + 0..32).
+template <int EPI, typename KV>
+__device__ void tile_epilogue(const GemmArgs &a, const float *Y, int ld, int t, const float *rinv)
+{
+    const int tid = threadIdx.x, nt = blockDim.x;
+    if (EPI == EPI_SWIGLU) {
+        for (int e = tid; e < a.Mpad * 16; e += nt) {
             const int m = e / 16, r = e % 16;
-            const float hv = silu(tileY[m][r]) * tileY[m][16 + r];
+            const float g = Y[m * ld + r] * rinv[m], up = Y[m * ld + 16 + r] * rinv[m];
+            const float hv = silu(g) * up;
             if (a.out_split) store_split(a.out_split, m, t * 16 + r, a.Mpad >> 4, hv);
             else a.out[(size_t)m * a.N + t * 16 + r] = hv;
         }
@@ -204,10 +246,10 @@ __device__ void gemm_epilogue(const GemmArgs &a, float (*tileY)[TILE_LD], int t,
         const int per_head = a.hd / DV_GEMM_TILE;
         const int h = tt / per_head, j0 = (tt - h * per_head) * 16;
         const int half = a.hd / 2;
-        for (int e = tid; e < a.M * 16; e += blockDim.x) {
+        for (int e = tid; e < a.M * 16; e += nt) {
             const int m = e / 16, r = e % 16;
             const int j = j0 + r;
-            float y1 = tileY[m][r], y2 = tileY[m][16 + r];
+            float y1 = Y[m * ld + r] * rinv[m], y2 = Y[m * ld + 16 + r] * rinv[m];
             if (seg < 2) {
                 const int pos = a.pos[m];  // P + depth(m) - 1
                 const float c = a.rope_cos[(size_t)pos * half + j];
@@ -231,178 +273,274 @@ __device__ void gemm_epilogue(const GemmArgs &a, float (*tileY)[TILE_LD], int t,
                 Elem<KV>::store(c, col + (size_t)(j + half) * a.cap, y2);
             }
         }
-    } else {  // EPI_LOGITS
-        if (a.out) {
-            for (int e = tid; e < a.M * DV_GEMM_TILE; e += blockDim.x) {
-                const int m = e / DV_GEMM_TILE, r = e % DV_GEMM_TILE;
-                a.out[(size_t)m * a.N + t * DV_GEMM_TILE + r] = tileY[m][r];
-            }
+    }
+}
+
+// LOGITS: logits of rows [row0, row0 + nrows) and their per-token
+// (max, argmax), lowest row on ties.
+__device__ void logits_epilogue(const GemmArgs &a, const float *Y, int ld, int row0, int nrows, int group,
+                                const float *rinv)
+{
+    const int tid = threadIdx.x, nt = blockDim.x;
+    if (a.out) {
+        for (int e = tid; e < a.M * nrows; e += nt) {
+            const int m = e / nrows, r = e - m * nrows;
+            a.out[(size_t)m * a.N + row0 + r] = Y[m * ld + r] * rinv[m];
         }
-        if (tid < a.M) {
-            float best = tileY[tid][0];
-            int bi = 0;
-            for (int r = 1; r < DV_GEMM_TILE; ++r) {
-                const float v = tileY[tid][r];
-                if (v > best) { best = v; bi = r; }
-            }
-            a.arg_val[(size_t)tid * a.n_tiles + t] = best;
-            a.arg_idx[(size_t)tid * a.n_tiles + t] = t * DV_GEMM_TILE + bi;
+    }
+    if (tid < a.M) {
+        const float ri = rinv[tid];
+        float best = Y[tid * ld] * ri;
+        int bi = 0;
+        for (int r = 1; r < nrows; ++r) {
+            const float v = Y[tid * ld + r] * ri;
+            if (v > best) { best = v; bi = r; }
         }
+        a.arg_val[(size_t)tid * a.n_groups + group] = best;
+        a.arg_idx[(size_t)tid * a.n_groups + group] = row0 + bi;
     }
 }
 
 // ---------------------------------------------------------------------------
-// MFMA GEMM for bf16 weights.
+// MFMA projection for bf16 weights (block layout) and split-layout
+// activations.
 //
 // v_mfma_f32_16x16x32_bf16: A = 16 weight rows x 32 k, B = 32 k x 16 tokens.
 // Lane l supplies A[l%16][8(l/16)..+8] (16 contiguous bytes of one weight
-// row) and B[8(l/16)..+8][l%16] (8 fp32 activations of token l%16, split
-// into bf16 hi + lo so the product keeps ~16 mantissa bits; two MFMAs per
-// operand pair).  D: lane l holds rows 4(l/16)..+4 of token l%16.
+// row) and B[8(l/16)..+8][l%16] for the bf16 hi and lo parts of the
+// activations (two MFMAs per pair, so every product keeps ~16 mantissa bits
+// of the fp32 activation).  D: lane l holds rows 4(l/16)..+4 of token l%16.
 //
-// Work unit = (tile, K split).  The grid is sized to stay resident and
-// loops over units; within a unit the four waves take contiguous quarters
-// of the K range, U k-steps per batch of loads, and their accumulators are
-// summed in LDS in wave order.
-
-// Weight tiles in MFMA order.  For tile t, k-step s (32 columns) and half h,
-// the 16 x 32 block is stored as 1 KB in lane order: lane l's 16 bytes are
-// row row0[h] + l%16, columns 32 s + 8 (l/16) .. +8.  Blocks are ordered
-// (t, s, h), so one wave's load instruction reads 1 KB contiguous and a
-// wave walking its k range streams one contiguous region.
-
-__global__ __launch_bounds__(128) void k_pack_tiles(GemmArgs a, int epi, uint16_t *dst)
-{
-    const int t = blockIdx.x, h = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int S = a.K / 32;
-    const RowMap rm = row_map(a, epi, t);
-    const uint16_t *src = reinterpret_cast<const uint16_t *>(rm.ptr[h]) +
-                          (size_t)(rm.row0[h] + (lane & 15)) * a.K + (lane >> 4) * 8;
-    for (int s = blockIdx.y; s < S; s += gridDim.y) {
-        const uint4 v = *reinterpret_cast<const uint4 *>(src + 32 * s);
-        *reinterpret_cast<uint4 *>(dst + (((size_t)t * S + s) * 2 + h) * 512 + lane * 8) = v;
-    }
-}
+// Work unit = (row group g of RB blocks, K split ks); the NW waves take the
+// unit's k-steps in turn (s = sb + wave, sb + wave + NW, ...), so a
+// workgroup reads one RB KB stretch of each k-major slab; each wave keeps U
+// k-steps of loads in flight (a new step is requested as soon as one is
+// consumed).  The wave partials are summed in LDS in wave order.  A split
+// unit stores its partial with device-coherent stores; the last unit of a
+// row group to arrive (counted with a device-scope atomic, nobody waits) sums
+// the ks partials in split order and runs the epilogue, so every sum has a
+// fixed order and no workgroup ever waits for another.
+//
+// Loads: weights are read once per step (non-temporal hint), activations
+// (MT KB hi + MT KB lo per k-step) are shared by every workgroup and stay in
+// the caches.
 
 #ifndef DV_WEIGHT_NT
 #define DV_WEIGHT_NT 1
 #endif
-// Weights are read exactly once per step: the non-temporal hint keeps them
-// from displacing reusable lines (activations) in the caches.
 __device__ __forceinline__ u32x4 load_weights(const u32x4 *p)
 {
     if (DV_WEIGHT_NT) return __builtin_nontemporal_load(p);
     return *p;
 }
 
-// N_STEPS k-steps for TP tiles: all weight and activation loads first, then
-// the MFMAs (TP tiles x 2 halves x MT token tiles x hi/lo).
-template <int MT, int TP, int N_STEPS>
-__device__ __forceinline__ void mfma_steps(const uint16_t *wtile, size_t tile_stride,
-                                           const uint16_t *xtile, f32x4 (&acc)[TP][2][MT])
+__global__ __launch_bounds__(64) void k_pack_blocks(GemmArgs a, int epi, uint16_t *dst)
 {
-    u32x4 wa[N_STEPS][TP][2];
-    u32x4 xa[N_STEPS][MT][2];
-#pragma unroll
-    for (int u = 0; u < N_STEPS; ++u) {
-#pragma unroll
-        for (int p = 0; p < TP; ++p)
-#pragma unroll
-            for (int h = 0; h < 2; ++h)
-                wa[u][p][h] = load_weights(reinterpret_cast<const u32x4 *>(wtile + p * tile_stride + (2 * u + h) * 512));
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-            for (int q = 0; q < 2; ++q)
-                xa[u][mt][q] = *reinterpret_cast<const u32x4 *>(xtile + ((u * MT + mt) * 2 + q) * 512);
-    }
-#pragma unroll
-    for (int u = 0; u < N_STEPS; ++u) {
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-            const bf16x8 hi = __builtin_bit_cast(bf16x8, xa[u][mt][0]);
-            const bf16x8 lo = __builtin_bit_cast(bf16x8, xa[u][mt][1]);
-#pragma unroll
-            for (int p = 0; p < TP; ++p)
-#pragma unroll
-                for (int h = 0; h < 2; ++h) {
-                    const bf16x8 w = __builtin_bit_cast(bf16x8, wa[u][p][h]);
-                    acc[p][h][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, hi, acc[p][h][mt], 0, 0, 0);
-                    acc[p][h][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, lo, acc[p][h][mt], 0, 0, 0);
-                }
-        }
+    // grid: (row groups x rb blocks, k-step chunks)
+    const int gb = blockIdx.x, lane = threadIdx.x;
+    const int rb = a.rb, G = a.n_groups, S = a.K / 32;
+    const int g = gb / rb, b = gb - g * rb;
+    const RowMap rm = row_map(a, epi, gb >> 1);
+    const int h = gb & 1;
+    const uint16_t *src = reinterpret_cast<const uint16_t *>(rm.ptr[h]) +
+                          (size_t)(rm.row0[h] + (lane & 15)) * a.K + (lane >> 4) * 8;
+    for (int s = blockIdx.y; s < S; s += gridDim.y) {
+        const uint4 v = *reinterpret_cast<const uint4 *>(src + 32 * s);
+        *reinterpret_cast<uint4 *>(dst + (((size_t)s * G + g) * rb + b) * 512 + lane * 8) = v;
     }
 }
 
-// MFMA GEMM for bf16 weights (packed tiles) and split-layout activations.
-// v_mfma_f32_16x16x32_bf16: A = 16 weight rows x 32 k, B = 32 k x 16 tokens;
-// each activation is the sum of its bf16 hi and lo parts, so every product
-// keeps ~16 mantissa bits of the fp32 activation (two MFMAs per pair).
-// D: lane l holds rows 4(l/16)..+4 of token l%16.
-// Work unit = (TP consecutive tiles sharing the activation operand, K split).
-// The grid is sized to stay resident and loops over units; within a unit the
-// NW waves take contiguous shares of the k-steps, U k-steps per batch of
-// loads, and their accumulators are summed in LDS in wave order.
-
-template <int MT, int EPI, typename KV, int NW, int U, int TP>
-__global__ __launch_bounds__(64 * NW) void k_gemm_mfma(GemmArgs a)
+template <int MT, int EPI, typename KV, int NW, int U, int RB>
+__global__ __launch_bounds__(64 * NW) void k_proj(GemmArgs a)
 {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int K = a.K, S = K / 32;
-    __shared__ float red[NW][2][MT][4][64];
-    __shared__ float tileY[DV_TREE_MAX][TILE_LD];
-    const int n_groups = a.n_tiles / TP;
-    const size_t tile_stride = (size_t)S * 1024;
+    constexpr int ROWS = RB * 16, LD = ROWS + 1, NE = RB * MT * 64;
+    static_assert(64 * NW >= 4 * 16 * MT, "input_rinv needs 4 threads per token");
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, tid = threadIdx.x;
+    const int S = a.K / 32, G = a.n_groups, KS = a.ks;
+    __shared__ f32x4 red[NW][NE / 64][64];
+    __shared__ float Y[16 * MT * LD];
+    __shared__ float rinv[DV_TREE_MAX];
+    __shared__ int last_s;
+    // RESID: the unit's rows of x (into Y) and their gains, staged while the
+    // weights stream
+    __shared__ float stage_s[EPI == EPI_RESID ? ROWS : 1];
+    const u32x4 *Wb = reinterpret_cast<const u32x4 *>(a.packed);
+    const u32x4 *Xb = reinterpret_cast<const u32x4 *>(a.xs);
+    bool have_rinv = false;
 
-    for (int unit = blockIdx.x; unit < n_groups * a.ks; unit += gridDim.x) {
-        const int tg = unit / a.ks, ksl = unit - tg * a.ks;
-        const int sb = ksl * (a.k_per_split / 32);
-        const int nsteps = min(S - sb, a.k_per_split / 32);
-        const int s0 = sb + (wave * nsteps) / NW, s1 = sb + ((wave + 1) * nsteps) / NW;
-        const uint16_t *wt = a.packed + (size_t)(tg * TP) * tile_stride + lane * 8;
-        const uint16_t *xt = a.xs + lane * 8;
+    // epilogue operands of unit (g), RESID: x rows into Y and the gains;
+    // issued after the unit's first weight loads
+    auto stage = [&](int g) {
+        if (EPI == EPI_RESID) {
+            for (int e = tid; e < 16 * MT * ROWS; e += 64 * NW) {
+                const int m = e / ROWS, r = e - m * ROWS;
+                Y[m * LD + r] = m < a.M ? a.resid[(size_t)m * a.N + g * ROWS + r] : 0.f;
+            }
+            for (int r = tid; r < ROWS; r += 64 * NW)
+                stage_s[r] = Elem<uint16_t>::load(reinterpret_cast<const uint16_t *>(a.gain), g * ROWS + r);
+        }
+    };
 
-        f32x4 acc[TP][2][MT];
+    for (int unit = blockIdx.x; unit < a.n_units; unit += gridDim.x) {
+        const int g = unit / KS, ks = unit - g * KS;
+        const int sb = (ks * S) / KS, se = ((ks + 1) * S) / KS;
+        const int s0 = sb + wave;
+        const int n = s0 < se ? (se - s0 + NW - 1) / NW : 0;
+        auto wp = [&](int i, int b) -> const u32x4 * {
+            return Wb + (((size_t)(s0 + NW * i) * G + g) * RB + b) * 64 + lane;
+        };
+        auto xp = [&](int i, int mt, int q) -> const u32x4 * {
+            return Xb + (((size_t)(s0 + NW * i) * MT + mt) * 2 + q) * 64 + lane;
+        };
+        f32x4 acc[RB][MT];
 #pragma unroll
-        for (int p = 0; p < TP; ++p)
+        for (int b = 0; b < RB; ++b)
 #pragma unroll
-            for (int h = 0; h < 2; ++h)
+            for (int mt = 0; mt < MT; ++mt) acc[b][mt] = (f32x4){0.f, 0.f, 0.f, 0.f};
+        if (n > 0) {
+            u32x4 wb[U][RB], xb[U][MT][2];
+            auto fetch = [&](int j, int i) {
 #pragma unroll
-                for (int mt = 0; mt < MT; ++mt) acc[p][h][mt] = (f32x4){0.f, 0.f, 0.f, 0.f};
-        int s = s0;
-        for (; s + U <= s1; s += U)
-            mfma_steps<MT, TP, U>(wt + (size_t)s * 1024, tile_stride, xt + (size_t)s * MT * 1024, acc);
-        for (; s < s1; ++s)
-            mfma_steps<MT, TP, 1>(wt + (size_t)s * 1024, tile_stride, xt + (size_t)s * MT * 1024, acc);
+                for (int b = 0; b < RB; ++b) wb[j][b] = load_weights(wp(i, b));
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) {
+                    xb[j][mt][0] = *xp(i, mt, 0);
+                    xb[j][mt][1] = *xp(i, mt, 1);
+                }
+            };
+            auto mfma = [&](int j) {
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) {
+                    const bf16x8 hi = __builtin_bit_cast(bf16x8, xb[j][mt][0]);
+                    const bf16x8 lo = __builtin_bit_cast(bf16x8, xb[j][mt][1]);
+#pragma unroll
+                    for (int b = 0; b < RB; ++b) {
+                        const bf16x8 w = __builtin_bit_cast(bf16x8, wb[j][b]);
+                        acc[b][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, hi, acc[b][mt], 0, 0, 0);
+                        acc[b][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, lo, acc[b][mt], 0, 0, 0);
+                    }
+                }
+            };
+            // prologue: U steps in flight (indices past the end re-read the
+            // last step and are dropped)
+#pragma unroll
+            for (int j = 0; j < U; ++j) fetch(j, min(j, n - 1));
+            stage(g);
+            if (EPI != EPI_RESID && !have_rinv) {
+                // the first unit's loads are in flight; the norm scalars of
+                // the input arrive meanwhile
+                input_rinv(a, rinv);
+                have_rinv = true;
+            }
+            int i = 0;
+            for (; i + U < n; i += U) {
+#pragma unroll
+                for (int j = 0; j < U; ++j) {
+                    mfma(j);
+                    fetch(j, min(i + j + U, n - 1));
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < U; ++j)
+                if (i + j < n) mfma(j);
+        } else {
+            stage(g);
+            if (EPI != EPI_RESID && !have_rinv) {
+                input_rinv(a, rinv);
+                have_rinv = true;
+            }
+        }
 
+        // wave partials -> unit sums (fixed wave order)
 #pragma unroll
-        for (int p = 0; p < TP; ++p) {
+        for (int b = 0; b < RB; ++b)
 #pragma unroll
-            for (int h = 0; h < 2; ++h)
+            for (int mt = 0; mt < MT; ++mt) red[wave][b * MT + mt][lane] = acc[b][mt];
+        __syncthreads();
+        f32x4 v[(NE + 64 * NW - 1) / (64 * NW)];
 #pragma unroll
-                for (int mt = 0; mt < MT; ++mt)
+        for (int c = 0; c < (NE + 64 * NW - 1) / (64 * NW); ++c) {
+            const int e = tid + 64 * NW * c;
+            v[c] = (f32x4){0.f, 0.f, 0.f, 0.f};
+            if (e < NE) {
+                v[c] = red[0][e >> 6][e & 63];
 #pragma unroll
-                    for (int j = 0; j < 4; ++j) red[wave][h][mt][j][lane] = acc[p][h][mt][j];
+                for (int w = 1; w < NW; ++w) v[c] += red[w][e >> 6][e & 63];
+            }
+        }
+        bool mine = true;
+        if (EPI == EPI_RESID && KS > 1) {
+            // publish this split's partial; the last arriver folds them
+            float *pp = a.part + (size_t)unit * NE * 4;
+#pragma unroll
+            for (int c = 0; c < (NE + 64 * NW - 1) / (64 * NW); ++c) {
+                const int e = tid + 64 * NW * c;
+                if (e < NE) {
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        __hip_atomic_store(pp + e * 4 + q, v[c][q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                }
+            }
+            // the partial is globally visible once the stores completed
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
             __syncthreads();
-            for (int e = threadIdx.x; e < 2 * MT * 4 * 64; e += 64 * NW) {
-                const int l = e & 63, j = (e >> 6) & 3, mt = (e >> 8) % MT, h = (e >> 8) / MT;
-                float v = red[0][h][mt][j][l];
-#pragma unroll
-                for (int w = 1; w < NW; ++w) v += red[w][h][mt][j][l];
-                tileY[mt * 16 + (l & 15)][h * 16 + 4 * (l >> 4) + j] = v;
+            if (tid == 0) {
+                const uint32_t old = __hip_atomic_fetch_add(a.cnt + g, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                last_s = old == (uint32_t)(KS - 1);
             }
             __syncthreads();
-            gemm_epilogue<EPI, KV>(a, tileY, tg * TP + p, ksl);
-            __syncthreads();
+            mine = last_s != 0;
+            if (mine) {
+#pragma unroll
+                for (int c = 0; c < (NE + 64 * NW - 1) / (64 * NW); ++c) {
+                    const int e = tid + 64 * NW * c;
+                    v[c] = (f32x4){0.f, 0.f, 0.f, 0.f};
+                    if (e < NE) {
+                        for (int k = 0; k < KS; ++k) {
+                            const float *q = a.part + ((size_t)(g * KS + k) * NE + e) * 4;
+#pragma unroll
+                            for (int j = 0; j < 4; ++j)
+                                v[c][j] += __hip_atomic_load(q + j, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        }
+                    }
+                }
+                if (tid == 0) __hip_atomic_store(a.cnt + g, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
         }
+        if (mine) {
+            // D layout -> Y[token][row]
+#pragma unroll
+            for (int c = 0; c < (NE + 64 * NW - 1) / (64 * NW); ++c) {
+                const int e = tid + 64 * NW * c;
+                if (e < NE) {
+                    const int l = e & 63, bm = e >> 6, b = bm / MT, mt = bm - b * MT;
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        float &y = Y[(mt * 16 + (l & 15)) * LD + b * 16 + 4 * (l >> 4) + j];
+                        y = EPI == EPI_RESID ? y + v[c][j] : v[c][j];
+                    }
+                }
+            }
+            __syncthreads();
+            if (EPI == EPI_RESID) {
+                resid_epilogue<uint16_t>(a, Y, LD, g * ROWS, ROWS, g, true, stage_s);
+            } else if (EPI == EPI_LOGITS) {
+                logits_epilogue(a, Y, LD, g * ROWS, ROWS, g, rinv);
+            } else {
+#pragma unroll
+                for (int p = 0; p < RB / 2; ++p)
+                    tile_epilogue<EPI, KV>(a, Y + 32 * p, LD, g * (RB / 2) + p, rinv);
+            }
+        }
+        __syncthreads();
     }
 }
 
 // ---------------------------------------------------------------------------
-// VALU GEMM (fp32 weights, or bf16 where K is not a multiple of 32).
-// Thread (row r = tid/8, lane-in-row kl = tid%8) walks k = kb + 8 kl + 64 i,
-// 8 weights per load; 16 tokens per pass; the 8 partial sums of a row are
-// combined with butterfly shuffles.
+// VALU GEMM (fp32 weights, or bf16 where K is not a multiple of 32).  One
+// 32-row tile per unit, full K.  Thread (row r = tid/8, lane-in-row kl =
+// tid%8) walks k = 8 kl + 64 i, 8 weights per load; 16 tokens per pass; the 8
+// partial sums of a row are combined with butterfly shuffles.
 
 template <typename W> struct Load8;
 template <> struct Load8<float> {
@@ -430,21 +568,24 @@ template <> struct Load8<uint16_t> {
 template <typename W, int EPI, typename KV>
 __global__ __launch_bounds__(256) void k_gemm_valu(GemmArgs a)
 {
+    constexpr int LD = DV_GEMM_TILE + 1;
     const int r = threadIdx.x >> 3, kl = threadIdx.x & 7;
     const int K = a.K;
-    __shared__ float tileY[DV_TREE_MAX][TILE_LD];
-    for (int unit = blockIdx.x; unit < a.n_units; unit += gridDim.x) {
-        const int t = unit / a.ks, ksl = unit - t * a.ks;
+    __shared__ float Y[DV_TREE_MAX * LD];
+    __shared__ float rinv[DV_TREE_MAX];
+    if (EPI != EPI_RESID) {
+        input_rinv(a, rinv);
+        __syncthreads();
+    }
+    for (int t = blockIdx.x; t < a.n_tiles; t += gridDim.x) {
         const RowMap rm = row_map(a, EPI, t);
         const int hsel = r >> 4;
         const W *wrow = reinterpret_cast<const W *>(rm.ptr[hsel]) + (size_t)(rm.row0[hsel] + (r & 15)) * K;
-        const int kb = ksl * a.k_per_split;
-        const int ke = min(K, kb + a.k_per_split);
         for (int m0 = 0; m0 < a.Mpad; m0 += 16) {
             float acc[16];
 #pragma unroll
             for (int m = 0; m < 16; ++m) acc[m] = 0.f;
-            for (int k = kb + kl * 8; k < ke; k += 64) {
+            for (int k = kl * 8; k < K; k += 64) {
                 float w[8];
                 Load8<W>::get(wrow + k, w);
 #pragma unroll
@@ -463,24 +604,24 @@ __global__ __launch_bounds__(256) void k_gemm_valu(GemmArgs a)
                 v += __shfl_xor(v, 1);
                 v += __shfl_xor(v, 2);
                 v += __shfl_xor(v, 4);
-                if (kl == 0) tileY[m0 + m][r] = v;
+                if (kl == 0) Y[(m0 + m) * LD + r] = v;
             }
         }
         __syncthreads();
-        gemm_epilogue<EPI, KV>(a, tileY, t, ksl);
+        if (EPI == EPI_RESID) resid_epilogue<W>(a, Y, LD, t * DV_GEMM_TILE, DV_GEMM_TILE, t, false, nullptr);
+        else if (EPI == EPI_LOGITS) logits_epilogue(a, Y, LD, t * DV_GEMM_TILE, DV_GEMM_TILE, t, rinv);
+        else tile_epilogue<EPI, KV>(a, Y, LD, t, rinv);
         __syncthreads();
     }
 }
 
 // ---------------------------------------------------------------------------
-// RMSNorm, one workgroup per token row (rows in [M, Mpad) are written as 0).
-// Before normalising, the row of the residual stream is completed: either
-// gathered from the embedding table (first layer) or incremented by the
-// split-K partial sums of the projection that produced it, in split order.
-// 256 threads x 4 consecutive floats per pass.
+// First RMSNorm of the step: grid (Mpad rows, DV_NORM_SLICES column slices),
+// rows in [M, Mpad) are written as 0.  x = embedding row of the token; u = x
+// * gain; the slice's sum of squares.
 
-template <typename W, int NV, int KS>
-__global__ __launch_bounds__(DV_NORM_THREADS) void k_rmsnorm(NormArgs a)
+template <typename W, int NV>
+__global__ __launch_bounds__(DV_NORM_THREADS) void k_embed_norm(NormArgs a)
 {
     constexpr int NT = DV_NORM_THREADS, SPAN = 4 * NT;
     const int m = blockIdx.x, sl = blockIdx.y, tid = threadIdx.x, d = a.d;
@@ -493,59 +634,29 @@ __global__ __launch_bounds__(DV_NORM_THREADS) void k_rmsnorm(NormArgs a)
             const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
             if (a.us) store_split4(a.us, m, i, MT, z);
             else *reinterpret_cast<float4 *>(urow + i) = z;
-            if (a.embed) *reinterpret_cast<float4 *>(xrow + i) = z;
+            *reinterpret_cast<float4 *>(xrow + i) = z;
         }
         if (tid == 0) a.ssq[m * DV_NORM_SLICES + sl] = 0.f;
         return;
     }
-    // NV = ceil(slice / SPAN) float4 per thread; KS = number of split-K
-    // partials to add (compile-time, so that all loads of the slice are
-    // issued together; KS < 0: a runtime count).  Addresses are clamped, not
-    // branched on: lanes past the slice end re-read its last float4 and drop it.
+    // NV = ceil(slice / SPAN) float4 per thread; addresses are clamped, not
+    // branched on: lanes past the slice end re-read its last float4 and drop it
     int idx[NV];
 #pragma unroll
     for (int c = 0; c < NV; ++c) idx[c] = min(c0 + 4 * tid + SPAN * c, c1 - 4);
     float4 v[NV];
-    if (a.embed) {
-        const W *e = reinterpret_cast<const W *>(a.embed) + (size_t)a.tokens[m] * d;
+    const W *e = reinterpret_cast<const W *>(a.embed) + (size_t)a.tokens[m] * d;
 #pragma unroll
-        for (int c = 0; c < NV; ++c)
-            v[c] = make_float4(Elem<W>::load(e, idx[c]), Elem<W>::load(e, idx[c] + 1),
-                               Elem<W>::load(e, idx[c] + 2), Elem<W>::load(e, idx[c] + 3));
-    } else {
-#pragma unroll
-        for (int c = 0; c < NV; ++c) v[c] = *reinterpret_cast<const float4 *>(xrow + idx[c]);
-    }
-    const int ks = KS >= 0 ? KS : a.ks;
-    if (KS > 0) {
-        float4 q[KS > 0 ? KS : 1][NV];
-#pragma unroll
-        for (int s = 0; s < (KS > 0 ? KS : 1); ++s)
-#pragma unroll
-            for (int c = 0; c < NV; ++c)
-                q[s][c] = *reinterpret_cast<const float4 *>(a.part + ((size_t)s * DV_TREE_MAX + m) * d + idx[c]);
-#pragma unroll
-        for (int s = 0; s < (KS > 0 ? KS : 1); ++s)
-#pragma unroll
-            for (int c = 0; c < NV; ++c) {
-                v[c].x += q[s][c].x; v[c].y += q[s][c].y; v[c].z += q[s][c].z; v[c].w += q[s][c].w;
-            }
-    } else {
-        for (int s = 0; s < ks; ++s) {
-#pragma unroll
-            for (int c = 0; c < NV; ++c) {
-                const float4 q = *reinterpret_cast<const float4 *>(a.part + ((size_t)s * DV_TREE_MAX + m) * d + idx[c]);
-                v[c].x += q.x; v[c].y += q.y; v[c].z += q.z; v[c].w += q.w;
-            }
-        }
-    }
+    for (int c = 0; c < NV; ++c)
+        v[c] = make_float4(Elem<W>::load(e, idx[c]), Elem<W>::load(e, idx[c] + 1),
+                           Elem<W>::load(e, idx[c] + 2), Elem<W>::load(e, idx[c] + 3));
     const W *gp = reinterpret_cast<const W *>(a.gain);
     float ss = 0.f;
 #pragma unroll
     for (int c = 0; c < NV; ++c) {
         const int i = idx[c];
         if (c0 + 4 * tid + SPAN * c < c1) {
-            if (a.embed || ks) *reinterpret_cast<float4 *>(xrow + i) = v[c];
+            *reinterpret_cast<float4 *>(xrow + i) = v[c];
             ss = fmaf(v[c].x, v[c].x, ss);
             ss = fmaf(v[c].y, v[c].y, ss);
             ss = fmaf(v[c].z, v[c].z, ss);
@@ -978,10 +1089,10 @@ __global__ __launch_bounds__(1024) void k_accept(AcceptArgs a)
     const int tpt = sd->Mpad <= 16 ? 64 : (sd->Mpad <= 32 ? 32 : 16);
     const int m = tid / tpt, sub = tid % tpt;
     if (m < M) {
-        const float *val = a.arg_val + (size_t)m * a.n_tiles;
-        const int32_t *idx = a.arg_idx + (size_t)m * a.n_tiles;
-        const int chunk = (a.n_tiles + tpt - 1) / tpt;
-        const int t0 = sub * chunk, t1 = min(a.n_tiles, t0 + chunk);
+        const float *val = a.arg_val + (size_t)m * a.n_parts;
+        const int32_t *idx = a.arg_idx + (size_t)m * a.n_parts;
+        const int chunk = (a.n_parts + tpt - 1) / tpt;
+        const int t0 = sub * chunk, t1 = min(a.n_parts, t0 + chunk);
         float best = -INFINITY;
         int bi = 0x7fffffff;
         for (int t = t0; t < t1; t += 16) {
@@ -1063,88 +1174,73 @@ __global__ __launch_bounds__(256) void k_kv_commit(CommitArgs a)
 // ---------------------------------------------------------------------------
 // launchers
 
-// Load batch per variant: U k-steps for one token tile, fewer as MT grows
-// (register budget); waves per workgroup capped at 4 for MT >= 3.
-template <int EPI, typename KV, int NW, int U, int TP>
-static const void *gemm_kernel_mfma(int mt)
+GemmShape gemm_shape(int rb) { return rb == 4 ? GemmShape{4, 2} : GemmShape{4, 4}; }
+
+// more token tiles hold more accumulators and operands: fewer steps in flight
+template <int EPI, typename KV, int RB>
+static const void *proj_kernel_mt(int mt)
 {
-    // more token tiles hold more accumulators: fewer k-steps per batch
+    constexpr int U1 = RB == 4 ? 2 : 4;
     switch (mt) {
-    case 1: return (const void *)k_gemm_mfma<1, EPI, KV, NW, U, TP>;
-    case 2: return (const void *)k_gemm_mfma<2, EPI, KV, NW, (U > 4 ? U / 2 : 2), TP>;
-    case 3: return (const void *)k_gemm_mfma<3, EPI, KV, 4, 2, TP>;
-    case 4: return (const void *)k_gemm_mfma<4, EPI, KV, 4, (TP > 2 ? 1 : 2), TP>;
+    case 1: return (const void *)k_proj<1, EPI, KV, 4, U1, RB>;
+    case 2: return (const void *)k_proj<2, EPI, KV, 4, 2, RB>;
+    case 3: return (const void *)k_proj<3, EPI, KV, 4, 1, RB>;
+    case 4: return (const void *)k_proj<4, EPI, KV, 4, 1, RB>;
     default: return nullptr;
     }
 }
 
-// index of an instantiated shape, -1 if none
-static int shape_index(GemmShape sh)
-{
-    if (sh.nw == 8 && sh.u == 4 && sh.tp == 2) return 0;
-    if (sh.nw == 4 && sh.u == 8 && sh.tp == 2) return 1;
-    if (sh.nw == 4 && sh.u == 4 && sh.tp == 4) return 2;
-    if (sh.nw == 4 && sh.u == 8 && sh.tp == 1) return 3;
-    return -1;
-}
-
 template <int EPI>
-static const void *gemm_kernel(int weight_bf16, int use_mfma, int mt, GemmShape sh)
+static const void *gemm_kernel(int weight_bf16, int use_mfma, int mt, int rb)
 {
     if (weight_bf16 && use_mfma) {
-        switch (shape_index(sh)) {
-        case 0: return gemm_kernel_mfma<EPI, uint16_t, 8, 4, 2>(mt);
-        case 1: return gemm_kernel_mfma<EPI, uint16_t, 4, 8, 2>(mt);
-        case 2: return gemm_kernel_mfma<EPI, uint16_t, 4, 4, 4>(mt);
-        case 3: return gemm_kernel_mfma<EPI, uint16_t, 4, 8, 1>(mt);
-        default: return nullptr;
-        }
+        if (rb == 4) return proj_kernel_mt<EPI, uint16_t, 4>(mt);
+        if (rb == 2) return proj_kernel_mt<EPI, uint16_t, 2>(mt);
+        return nullptr;
     }
     if (weight_bf16) return (const void *)k_gemm_valu<uint16_t, EPI, uint16_t>;
     return (const void *)k_gemm_valu<float, EPI, float>;
 }
 
-static const void *gemm_kernel_any(int epi, int weight_bf16, int use_mfma, int mt, GemmShape sh)
+static const void *gemm_kernel_any(int epi, int weight_bf16, int use_mfma, int mt, int rb)
 {
     switch (epi) {
-    case EPI_QKV: return gemm_kernel<EPI_QKV>(weight_bf16, use_mfma, mt, sh);
-    case EPI_RESID: return gemm_kernel<EPI_RESID>(weight_bf16, use_mfma, mt, sh);
-    case EPI_SWIGLU: return gemm_kernel<EPI_SWIGLU>(weight_bf16, use_mfma, mt, sh);
-    case EPI_LOGITS: return gemm_kernel<EPI_LOGITS>(weight_bf16, use_mfma, mt, sh);
+    case EPI_QKV: return gemm_kernel<EPI_QKV>(weight_bf16, use_mfma, mt, rb);
+    case EPI_RESID: return gemm_kernel<EPI_RESID>(weight_bf16, use_mfma, mt, rb);
+    case EPI_SWIGLU: return gemm_kernel<EPI_SWIGLU>(weight_bf16, use_mfma, mt, rb);
+    case EPI_LOGITS: return gemm_kernel<EPI_LOGITS>(weight_bf16, use_mfma, mt, rb);
     }
     return nullptr;
 }
 
-static int gemm_threads(int weight_bf16, int use_mfma, int mt, GemmShape sh)
+static int gemm_threads(int weight_bf16, int use_mfma, int rb)
 {
-    if (!(weight_bf16 && use_mfma)) return 256;
-    return mt >= 3 ? 256 : 64 * sh.nw;
+    return (weight_bf16 && use_mfma) ? 64 * gemm_shape(rb).nw : 256;
 }
 
-int gemm_blocks_per_cu(int epi, int weight_bf16, int use_mfma, int mt, GemmShape sh)
+int gemm_blocks_per_cu(int epi, int weight_bf16, int use_mfma, int mt, int rb)
 {
-    static int cache[4][2][2][5][5];
-    int &c = cache[epi & 3][weight_bf16 ? 1 : 0][use_mfma ? 1 : 0][(mt >= 1 && mt <= 4) ? mt : 0]
-                  [shape_index(sh) + 1];
+    static int cache[4][2][2][5][2];
+    int &c = cache[epi & 3][weight_bf16 ? 1 : 0][use_mfma ? 1 : 0][(mt >= 1 && mt <= 4) ? mt : 0][rb == 4];
     if (c == 0) {
-        const void *k = gemm_kernel_any(epi, weight_bf16, use_mfma, mt, sh);
+        const void *k = gemm_kernel_any(epi, weight_bf16, use_mfma, mt, rb);
         int n = 0;
-        if (!k || hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k, gemm_threads(weight_bf16, use_mfma, mt, sh),
-                                                               0) != hipSuccess || n < 1)
+        if (!k || hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k, gemm_threads(weight_bf16, use_mfma, rb), 0) !=
+                      hipSuccess || n < 1)
             n = 1;
         c = n;
     }
     return c;
 }
 
-hipError_t launch_gemm(const GemmArgs &a, int grid, int epi, int weight_bf16, int use_mfma,
-                       GemmShape sh, hipStream_t s, hipEvent_t ev_start, hipEvent_t ev_stop)
+hipError_t launch_gemm(const GemmArgs &a, int grid, int epi, int weight_bf16, int use_mfma, hipStream_t s,
+                       hipEvent_t ev_start, hipEvent_t ev_stop)
 {
-    const void *k = gemm_kernel_any(epi, weight_bf16, use_mfma, a.Mpad / 16, sh);
+    const void *k = gemm_kernel_any(epi, weight_bf16, use_mfma, a.Mpad / 16, a.rb);
     if (!k || grid < 1) return hipErrorInvalidValue;
     GemmArgs arg = a;
     void *params[] = {&arg};
-    const dim3 block(gemm_threads(weight_bf16, use_mfma, a.Mpad / 16, sh));
+    const dim3 block(gemm_threads(weight_bf16, use_mfma, a.rb));
     // with events: timestamps taken by the dispatch itself (no extra packets)
     if (ev_start && ev_stop) return hipExtLaunchKernel(k, dim3(grid), block, params, 0, s, ev_start, ev_stop, 0);
     return hipLaunchKernel(k, dim3(grid), block, params, 0, s);
@@ -1152,40 +1248,28 @@ hipError_t launch_gemm(const GemmArgs &a, int grid, int epi, int weight_bf16, in
 
 hipError_t launch_pack(const GemmArgs &a, int epi, uint16_t *dst, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_pack_tiles, dim3(a.n_tiles, std::min(a.K / 32, 64)), dim3(128), 0, s, a, epi, dst);
-    return hipGetLastError();
-}
-
-template <typename W, int NV>
-static hipError_t rmsnorm_dispatch_ks(const NormArgs &a, int Mpad, hipStream_t s)
-{
-    const dim3 grid(Mpad, DV_NORM_SLICES), block(DV_NORM_THREADS);
-    switch (a.ks) {
-    case 0: hipLaunchKernelGGL((k_rmsnorm<W, NV, 0>), grid, block, 0, s, a); break;
-    case 2: hipLaunchKernelGGL((k_rmsnorm<W, NV, 2>), grid, block, 0, s, a); break;
-    case 4: hipLaunchKernelGGL((k_rmsnorm<W, NV, 4>), grid, block, 0, s, a); break;
-    case 8: hipLaunchKernelGGL((k_rmsnorm<W, NV, 8>), grid, block, 0, s, a); break;
-    case 16: hipLaunchKernelGGL((k_rmsnorm<W, NV, 16>), grid, block, 0, s, a); break;
-    default: hipLaunchKernelGGL((k_rmsnorm<W, NV, -1>), grid, block, 0, s, a); break;
-    }
+    if (a.rb != 2 && a.rb != 4) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_pack_blocks, dim3(a.n_groups * a.rb, std::min(a.K / 32, 64)), dim3(64), 0, s, a, epi, dst);
     return hipGetLastError();
 }
 
 template <typename W>
-static hipError_t rmsnorm_dispatch(const NormArgs &a, int Mpad, hipStream_t s)
+static hipError_t embed_norm_dispatch(const NormArgs &a, int Mpad, hipStream_t s)
 {
     const int slice = a.d / DV_NORM_SLICES;
     if (a.d % (4 * DV_NORM_SLICES)) return hipErrorInvalidValue;
+    const dim3 grid(Mpad, DV_NORM_SLICES), block(DV_NORM_THREADS);
     switch ((slice + 4 * DV_NORM_THREADS - 1) / (4 * DV_NORM_THREADS)) {
-    case 1: return rmsnorm_dispatch_ks<W, 1>(a, Mpad, s);
-    case 2: return rmsnorm_dispatch_ks<W, 2>(a, Mpad, s);
+    case 1: hipLaunchKernelGGL((k_embed_norm<W, 1>), grid, block, 0, s, a); break;
+    case 2: hipLaunchKernelGGL((k_embed_norm<W, 2>), grid, block, 0, s, a); break;
     default: return hipErrorInvalidValue;
     }
+    return hipGetLastError();
 }
 
-hipError_t launch_rmsnorm(const NormArgs &a, int Mpad, int weight_bf16, hipStream_t s)
+hipError_t launch_embed_norm(const NormArgs &a, int Mpad, int weight_bf16, hipStream_t s)
 {
-    return weight_bf16 ? rmsnorm_dispatch<uint16_t>(a, Mpad, s) : rmsnorm_dispatch<float>(a, Mpad, s);
+    return weight_bf16 ? embed_norm_dispatch<uint16_t>(a, Mpad, s) : embed_norm_dispatch<float>(a, Mpad, s);
 }
 
 hipError_t launch_attention(const AttnArgs &a, int kv_bf16, hipStream_t s)

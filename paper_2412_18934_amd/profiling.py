@@ -4,7 +4,7 @@
     python -m paper_2412_18934_amd.profiling hbm <fetch counter_collection.csv> <write counter_collection.csv> <out.txt> <command>
 
 ``stats`` writes a per-kernel table (calls, average, share) plus the average
-duration of the projection kernels (k_gemm_*), the figure bench.py's roofline
+duration of the projection kernels (k_proj, k_gemm_valu), the figure bench.py's roofline
 uses.  ``hbm`` turns FETCH_SIZE / WRITE_SIZE (KiB per dispatch) into bytes per
 dispatch, scaled by what the same counters read for a reference copy of known
 size (the 256 MiB device copy bench.py --calibrate-copy issues: 256 MiB read
@@ -22,6 +22,11 @@ import sys
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 KERNEL_SOURCES = ("csrc/dv_kernels.hip", "csrc/dv_engine.cpp", "csrc/dv_internal.h")
+PROJ_PREFIXES = ("k_proj", "k_gemm")
+
+
+def is_projection(name: str) -> bool:
+    return name.startswith(PROJ_PREFIXES)
 CALIB_BYTES = 256 << 20
 
 
@@ -48,10 +53,10 @@ def summarize_stats(stats_csv, trace_csv, out_path, command):
         n = int(r["Calls"])
         avg = float(r["AverageNs"]) / 1e3
         lines.append("| `%s` | %d | %.2f | %.1f%% |" % (name, n, avg, float(r["Percentage"])))
-        if name.startswith("k_gemm"):
+        if is_projection(name):
             gemm_ns += float(r["TotalDurationNs"])
             gemm_n += n
-    lines += ["", "Projection kernels (k_gemm_*): %d launches, average %.2f us."
+    lines += ["", "Projection kernels (k_proj, k_gemm_valu): %d launches, average %.2f us."
               % (gemm_n, gemm_ns / max(gemm_n, 1) / 1e3)]
     # one full step from the trace: the span between two k_accept dispatches
     trace = list(csv.DictReader(open(trace_csv)))
@@ -125,10 +130,10 @@ def gemm_traffic_per_launch(path):
     sh, per = read_hbm_summary(path)
     if sh != source_hash():
         return None
-    n = sum(d for k, (d, f, w) in per.items() if k.startswith("k_gemm"))
+    n = sum(d for k, (d, f, w) in per.items() if is_projection(k))
     if not n:
         return None
-    return sum(d * (f + w) for k, (d, f, w) in per.items() if k.startswith("k_gemm")) / n
+    return sum(d * (f + w) for k, (d, f, w) in per.items() if is_projection(k)) / n
 
 
 if __name__ == "__main__":

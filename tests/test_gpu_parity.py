@@ -136,6 +136,28 @@ def test_bf16_head_dim_64_parity():
         case.close()
 
 
+def test_bf16_split_k_fold_parity():
+    """d_model 1024 / d_ffn 2816: the O and down projections split K (2 and 5
+    ways on 256 CUs) and the last split of each row group folds the partials,
+    adds the residual and writes the next norm's input; bitwise repeatable."""
+    cfg = small_cfg(n_layers=2, d_model=1024, n_heads=8, head_dim=128, d_ffn=2816, vocab=4096,
+                    weight_dtype="bf16", init_std=0.045)
+    case = GpuCase(cfg, seed=111, capacity=320)
+    try:
+        om = case.w.oracle()
+        kv = case.new_kv()
+        kv_o = case.synthetic_context(kv, 112, 200)
+        for m in (16, 40):
+            toks, par = synth.random_tree(113 + m, m, 6, cfg.vocab)
+            ref = _ref(om, kv_o, toks, par)
+            acc, lg = case.step(kv, toks, par)
+            compare_step(acc, lg, ref, 2e-2)
+            acc2, lg2 = case.step(kv, toks, par)
+            assert np.array_equal(lg, lg2)
+    finally:
+        case.close()
+
+
 def test_step_is_deterministic_and_ignores_stale_slots(bf16_case):
     """Same step twice -> bitwise equal; NaN in unused cache slots changes nothing."""
     case = bf16_case
