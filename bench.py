@@ -190,6 +190,7 @@ def main():
         gemm_ms, gemm_n = dv.dv_profile_read(h, dv.DV_K_GEMM, reset=True)
         if gemm_n:
             avg_ms = gemm_ms / gemm_n
+            glaunch = gemm_n / args.steps
             per_launch = gbytes / glaunch
             achieved = per_launch / (avg_ms * 1e-3) / 1e9
             from paper_2412_18934_amd import profiling
@@ -201,7 +202,7 @@ def main():
                     "traffic": None if traffic is None else round(traffic),
                     "kernel": "k_proj (QKV, O, gate/up, down, lm_head projections)",
                     "bytes_per_launch": int(per_launch), "avg_launch_us": round(avg_ms * 1e3, 2),
-                    "launches_per_step": glaunch, "ms_per_step_with_events": round(ms_r, 3)}
+                    "launches_per_step": round(glaunch, 2), "ms_per_step_with_events": round(ms_r, 3)}
     sbytes = step_bytes(mc, m, p, esz)
     step_gbs = sbytes / (ms * 1e-3) / 1e9
 

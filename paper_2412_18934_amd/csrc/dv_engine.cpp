@@ -54,6 +54,7 @@ struct dv_handle {
     uint32_t *cnt = nullptr;     // their per-row-group arrival counters
     uint16_t *u_s = nullptr, *attn_s = nullptr, *h_s = nullptr;  // split-layout activations
     float *part_o = nullptr, *part_m = nullptr, *part_l = nullptr;
+    uint32_t *attn_cnt = nullptr;  // per-head arrivals of the attention splits
     int attn_split_max = 0;
     float *arg_val = nullptr;
     int32_t *arg_idx = nullptr;
@@ -220,8 +221,9 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
     // attention: the P + M keys of each head are split evenly into
     // tile-aligned ranges, one workgroup each, so that heads x splits covers
     // the compute units once (each workgroup streams its range with a
-    // two-tile pipeline per wave); the merge kernel combines the splits, and a
-    // single split writes the output itself
+    // two-tile pipeline per wave); the last split of a head to finish merges
+    // them (bf16 cache; the fp32 path uses the merge kernel), and a single
+    // split writes the output itself
     const int total = P + M;
     int kps, n_split;
     if (h->bf16) {
@@ -264,6 +266,7 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
     aa.part_o = h->part_o;
     aa.part_m = h->part_m;
     aa.part_l = h->part_l;
+    aa.cnt = h->attn_cnt;
     aa.out = h->attn;
     aa.out_split = h->p_o.mfma ? h->attn_s : nullptr;
 
@@ -322,7 +325,8 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
         aa.vc = g.vc;
         prof_begin(h, DV_K_ATTN);
         hipError_t e = launch_attention(aa, h->bf16, s);
-        if (e == hipSuccess && n_split > 1) e = launch_attn_merge(aa, Mpad, s);
+        // (the bf16 kernel merges its splits itself)
+        if (e == hipSuccess && n_split > 1 && !h->bf16) e = launch_attn_merge(aa, Mpad, s);
         prof_end(h);
         if (e != hipSuccess) return hip_fail(h, e, "attention launch");
         if ((rc = gemm(h->p_o, EPI_RESID, w.wo, nullptr, nullptr, w.pk_o, d, d, h->attn, h->attn_s, nullptr,
@@ -499,6 +503,7 @@ int dv_verify_init(const dv_config *cfg, const dv_weights *w, void *stream, dv_h
               dalloc((void **)&h->part_o, (size_t)H * h->attn_split_max * rows * hd * 4) &&
               dalloc((void **)&h->part_m, (size_t)H * h->attn_split_max * rows * 4) &&
               dalloc((void **)&h->part_l, (size_t)H * h->attn_split_max * rows * 4) &&
+              dalloc((void **)&h->attn_cnt, (size_t)H * 4) &&
               dalloc((void **)&h->part_gemm, part_elems * 4) &&
               dalloc((void **)&h->arg_val, (size_t)h->p_lm.n_groups * rows * 4) &&
               dalloc((void **)&h->arg_idx, (size_t)h->p_lm.n_groups * rows * 4) &&
@@ -702,7 +707,7 @@ void dv_verify_free(dv_handle *h)
     else (void)hipDeviceSynchronize();
     for (void *p : {(void *)h->x, (void *)h->u, (void *)h->q, (void *)h->attn, (void *)h->hbuf,
                     (void *)h->u_s, (void *)h->attn_s, (void *)h->h_s, (void *)h->ssq,
-                    (void *)h->part_o, (void *)h->part_m, (void *)h->part_l, (void *)h->part_gemm, (void *)h->cnt,
+                    (void *)h->part_o, (void *)h->part_m, (void *)h->part_l, (void *)h->attn_cnt, (void *)h->part_gemm, (void *)h->cnt,
                     (void *)h->arg_val, (void *)h->arg_idx, (void *)h->rope_cos,
                     (void *)h->rope_sin, (void *)h->d_sd, (void *)h->d_acc})
         if (p) (void)hipFree(p);

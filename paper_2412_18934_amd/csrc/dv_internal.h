@@ -8,7 +8,7 @@
 #define DV_TREE_MAX 64
 #define DV_GEMM_TILE 32     // logical output rows per workgroup tile
 #define DV_ATTN_TILE 32     // keys per attention tile
-#define DV_ATTN_WAVES 4     // waves per attention workgroup (MFMA path)
+
 #define DV_ATTN_SPLIT_KEYS 256   // keys per workgroup of the fp32-cache attention
 
 // Per-step description of the draft tree, uploaded once per step.
@@ -126,8 +126,9 @@ struct AttnArgs {
     int32_t cap, hd, H;
     int32_t keys_per_split, n_split;
     const StepDesc *sd;
-    float *part_o;             // [H][n_split][64][hd]
-    float *part_m, *part_l;    // [H][n_split][64]
+    float *part_o;             // [H][n_split][64][hd] unnormalised split outputs
+    float *part_m, *part_l;    // [H][n_split][64] their running max (base 2) and sum
+    uint32_t *cnt;             // [H] arrivals of the splits, 0 between launches
     float *out;                // [Mpad][H*hd] fp32 output, or
     uint16_t *out_split;       // the output in split layout when set
 };

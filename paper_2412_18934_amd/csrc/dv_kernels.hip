@@ -227,20 +227,44 @@ __device__ void resid_epilogue(const GemmArgs &a, float *Y, int ld, int row0, in
     }
 }
 
-// Non-residual epilogues for the 32-row tile t held in Y[m * ld + 0..32).
-template <int EPI, typename KV>
-__device__ void tile_epilogue(const GemmArgs &a, const float *Y, int ld, int t, const float *rinv)
+// SWIGLU on ntile consecutive tiles t0.. held in Y (tile p: gate rows at
+// columns 32 p + [0,16), up rows at 32 p + 16 + [0,16)): h columns
+// [16 t0, 16 (t0 + ntile)) of every token; in split layout 8 columns per
+// thread (one 16-byte hi and one lo store).
+__device__ void swiglu_epilogue(const GemmArgs &a, const float *Y, int ld, int t0, int ntile, const float *rinv)
 {
     const int tid = threadIdx.x, nt = blockDim.x;
-    if (EPI == EPI_SWIGLU) {
-        for (int e = tid; e < a.Mpad * 16; e += nt) {
-            const int m = e / 16, r = e % 16;
-            const float g = Y[m * ld + r] * rinv[m], up = Y[m * ld + 16 + r] * rinv[m];
-            const float hv = silu(g) * up;
-            if (a.out_split) store_split(a.out_split, m, t * 16 + r, a.Mpad >> 4, hv);
-            else a.out[(size_t)m * a.N + t * 16 + r] = hv;
+    if (a.out_split) {
+        const int MT = a.Mpad >> 4, nc = 2 * ntile;
+        for (int e = tid; e < a.Mpad * nc; e += nt) {
+            const int m = e / nc, c = e - m * nc, p = c >> 1, r0 = 8 * (c & 1);
+            const float *g = Y + m * ld + 32 * p + r0, *u = g + 16;
+            float hv[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) hv[i] = silu(g[i] * rinv[m]) * (u[i] * rinv[m]);
+            bf16x8 hi, lo;
+            split_hi_lo(make_float4(hv[0], hv[1], hv[2], hv[3]), make_float4(hv[4], hv[5], hv[6], hv[7]), hi, lo);
+            const size_t i = split_index(m, 16 * t0 + 8 * c, MT);
+            *reinterpret_cast<bf16x8 *>(a.out_split + i) = hi;
+            *reinterpret_cast<bf16x8 *>(a.out_split + i + 512) = lo;
         }
-    } else if (EPI == EPI_QKV) {
+    } else {
+        for (int e = tid; e < a.Mpad * 16 * ntile; e += nt) {
+            const int m = e / (16 * ntile), c = e - m * 16 * ntile, p = c >> 4, r = c & 15;
+            const float hv = silu(Y[m * ld + 32 * p + r] * rinv[m]) * (Y[m * ld + 32 * p + 16 + r] * rinv[m]);
+            a.out[(size_t)m * a.N + 16 * t0 + c] = hv;
+        }
+    }
+}
+
+// QKV on the 32-row tile t held in Y[m * ld + 0..32): rotary embedding of q
+// and k at each token's position, q to the query buffer, k and v (rounded to
+// the cache type) to cache slots P + m.
+template <typename KV>
+__device__ void qkv_epilogue(const GemmArgs &a, const float *Y, int ld, int t, const float *rinv)
+{
+    const int tid = threadIdx.x, nt = blockDim.x;
+    {
         const int per_seg = a.N / DV_GEMM_TILE;
         const int seg = t / per_seg, tt = t - seg * per_seg;
         const int per_head = a.hd / DV_GEMM_TILE;
@@ -288,16 +312,27 @@ __device__ void logits_epilogue(const GemmArgs &a, const float *Y, int ld, int r
             a.out[(size_t)m * a.N + row0 + r] = Y[m * ld + r] * rinv[m];
         }
     }
-    if (tid < a.M) {
-        const float ri = rinv[tid];
-        float best = Y[tid * ld] * ri;
-        int bi = 0;
-        for (int r = 1; r < nrows; ++r) {
-            const float v = Y[tid * ld + r] * ri;
+    // 4 threads per token scan interleaved rows; combined by shuffles
+    // (larger value, then lower row)
+    if (tid < 4 * a.Mpad) {
+        const int m = tid >> 2, c = tid & 3;
+        const float ri = rinv[m];
+        float best = -INFINITY;
+        int bi = nrows;
+        for (int r = c; r < nrows; r += 4) {
+            const float v = Y[m * ld + r] * ri;
             if (v > best) { best = v; bi = r; }
         }
-        a.arg_val[(size_t)tid * a.n_groups + group] = best;
-        a.arg_idx[(size_t)tid * a.n_groups + group] = row0 + bi;
+#pragma unroll
+        for (int off = 1; off < 4; off <<= 1) {
+            const float v2 = __shfl_xor(best, off);
+            const int i2 = __shfl_xor(bi, off);
+            if (v2 > best || (v2 == best && i2 < bi)) { best = v2; bi = i2; }
+        }
+        if (c == 0 && m < a.M) {
+            a.arg_val[(size_t)m * a.n_groups + group] = best;
+            a.arg_idx[(size_t)m * a.n_groups + group] = row0 + bi;
+        }
     }
 }
 
@@ -526,10 +561,11 @@ __global__ __launch_bounds__(64 * NW) void k_proj(GemmArgs a)
                 resid_epilogue<uint16_t>(a, Y, LD, g * ROWS, ROWS, g, true, stage_s);
             } else if (EPI == EPI_LOGITS) {
                 logits_epilogue(a, Y, LD, g * ROWS, ROWS, g, rinv);
+            } else if (EPI == EPI_SWIGLU) {
+                swiglu_epilogue(a, Y, LD, g * (RB / 2), RB / 2, rinv);
             } else {
 #pragma unroll
-                for (int p = 0; p < RB / 2; ++p)
-                    tile_epilogue<EPI, KV>(a, Y + 32 * p, LD, g * (RB / 2) + p, rinv);
+                for (int p = 0; p < RB / 2; ++p) qkv_epilogue<KV>(a, Y + 32 * p, LD, g * (RB / 2) + p, rinv);
             }
         }
         __syncthreads();
@@ -610,7 +646,8 @@ __global__ __launch_bounds__(256) void k_gemm_valu(GemmArgs a)
         __syncthreads();
         if (EPI == EPI_RESID) resid_epilogue<W>(a, Y, LD, t * DV_GEMM_TILE, DV_GEMM_TILE, t, false, nullptr);
         else if (EPI == EPI_LOGITS) logits_epilogue(a, Y, LD, t * DV_GEMM_TILE, DV_GEMM_TILE, t, rinv);
-        else tile_epilogue<EPI, KV>(a, Y, LD, t, rinv);
+        else if (EPI == EPI_SWIGLU) swiglu_epilogue(a, Y, LD, t, 1, rinv);
+        else qkv_epilogue<KV>(a, Y, LD, t, rinv);
         __syncthreads();
     }
 }
@@ -690,8 +727,9 @@ __global__ __launch_bounds__(DV_NORM_THREADS) void k_embed_norm(NormArgs a)
 // cache slots; the tree's own keys/values were written to slots P.. by the
 // QKV epilogue.  Key j is visible to node i iff j < P or bit (j-P) of
 // anc(i).  Each split writes its unnormalised output with the running max
-// and sum; k_attn_merge combines the splits (or, with one split, the
-// workgroup writes the normalised output itself).
+// and sum; the splits are combined by the last split of the head to finish
+// (bf16 cache) or by k_attn_merge (fp32 cache); with one split the workgroup
+// writes the normalised output itself.
 
 // bf16 cache, MFMA.  Queries are taken 16 at a time; the NW waves take
 // interleaved 32-key tiles and are combined in LDS at the end.
@@ -703,12 +741,15 @@ __global__ __launch_bounds__(DV_NORM_THREADS) void k_embed_norm(NormArgs a)
 //   O = P V: A = P (those 8 scores per lane, exponentiated, split hi + lo),
 //   B = V^T rows: 16 bytes = the same 8 consecutive keys of one dim.
 // Scores are kept in base-2 units (scaled by log2(e)/sqrt(hd)) so every
-// exponential is one exp2; the running max written for the merge is
-// converted back to natural units.  Each wave keeps two tiles of K and V in
+// exponential is one exp2 (the running max handed to the merge stays in
+// base-2 units).  Each wave keeps two tiles of K and V in
 // registers (the next one loads while the current one is used); the
 // prologue issues the query, ancestor-mask and first-tile loads together.
 
-template <int HD, int NW>
+// DB: two register tiles per wave (next tile loads while the current one is
+// used; for long key ranges); without DB every wave holds one tile, which
+// leaves room for 8 waves when a split has at most one tile per wave.
+template <int HD, int NW, bool DB>
 __global__ __launch_bounds__(64 * NW) void k_attn_mfma(AttnArgs a)
 {
     constexpr int NC = HD / 32;  // QK k-steps over dims
@@ -763,7 +804,8 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mfma(AttnArgs a)
             x1 = *reinterpret_cast<const float4 *>(qp + 4);
         }
         const uint64_t anc_raw = sd->anc[min(tok, M - 1)];
-        Tile buf0, buf1;
+        Tile buf0;
+        Tile buf1;  // used with DB only
         if (wave < ntile) load(wave, buf0);
         const uint64_t anc = tok_ok ? anc_raw : 0ull;
         if (e < 2 * HD) {
@@ -850,14 +892,21 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mfma(AttnArgs a)
                 o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pl, v8, o[dt], 0, 0, 0);
             }
         };
-        // two register buffers used in turn (no copies between them, so a
-        // load in flight is never waited on before its tile is used)
-        for (int t = wave; t < ntile; t += 2 * NW) {
-            if (t + NW < ntile) load(t + NW, buf1);
-            process(t, buf0);
-            if (t + NW >= ntile) break;
-            if (t + 2 * NW < ntile) load(t + 2 * NW, buf0);
-            process(t + NW, buf1);
+        if (DB) {
+            // two register buffers used in turn (no copies between them, so a
+            // load in flight is never waited on before its tile is used)
+            for (int t = wave; t < ntile; t += 2 * NW) {
+                if (t + NW < ntile) load(t + NW, buf1);
+                process(t, buf0);
+                if (t + NW >= ntile) break;
+                if (t + 2 * NW < ntile) load(t + 2 * NW, buf0);
+                process(t + NW, buf1);
+            }
+        } else {
+            for (int t = wave; t < ntile; t += NW) {
+                if (t != wave) load(t, buf0);
+                process(t, buf0);
+            }
         }
 
         // combine the waves (fixed wave order)
@@ -891,16 +940,82 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mfma(AttnArgs a)
                     else a.out[(size_t)ti * D + h * HD + dd] = r;
                 }
             } else if (ti < M) {
+                // published with device-coherent stores for the merging workgroup
                 const size_t pb = ((size_t)h * a.n_split + split) * DV_TREE_MAX + ti;
-                a.part_o[pb * HD + dd] = ov;
+                __hip_atomic_store(a.part_o + pb * HD + dd, ov, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 if (dd == 0) {
-                    a.part_m[pb] = mx * 0.6931471805599453f;  // back to natural-log units
-                    a.part_l[pb] = l;
+                    __hip_atomic_store(a.part_m + pb, mx, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    __hip_atomic_store(a.part_l + pb, l, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 }
             }
         }
         __syncthreads();
     }
+    if (a.n_split == 1) return;
+
+    // The last split of this head to finish (device-scope counter; nobody
+    // waits) merges the splits of every node in split order: a softmax-
+    // weighted sum with a running maximum (base-2 units), then the output in
+    // split layout, 8 dims of one node per thread.
+    __shared__ int last_s;
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const uint32_t old = __hip_atomic_fetch_add(a.cnt + h, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        last_s = old == (uint32_t)(a.n_split - 1);
+    }
+    __syncthreads();
+    if (!last_s) return;
+    const int Mpad = sd->Mpad, MT = Mpad >> 4;
+    const __amdgpu_buffer_rsrc_t po = __builtin_amdgcn_make_buffer_rsrc(a.part_o, (short)0, 0x7fffffff, 0x00020000);
+    constexpr int CH = 8;  // splits whose loads are in flight together
+    for (int e2 = threadIdx.x; e2 < Mpad * (HD / 8); e2 += 64 * NW) {
+        const int i = e2 / (HD / 8), d0 = 8 * (e2 % (HD / 8));
+        float ov[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+        float run_m = -INFINITY, l = 0.f;
+        if (i < M) {
+            for (int s0 = 0; s0 < a.n_split; s0 += CH) {
+                float ms[CH], ls[CH];
+                f32x4 oa[CH], ob[CH];
+#pragma unroll
+                for (int c = 0; c < CH; ++c) {
+                    const size_t pb = ((size_t)h * a.n_split + min(s0 + c, a.n_split - 1)) * DV_TREE_MAX + i;
+                    ms[c] = __hip_atomic_load(a.part_m + pb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    ls[c] = __hip_atomic_load(a.part_l + pb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    const uint32_t off = (uint32_t)((pb * HD + d0) * 4);
+                    oa[c] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(po, off, 0, 16));
+                    ob[c] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(po, off + 16, 0, 16));
+                }
+#pragma unroll
+                for (int c = 0; c < CH; ++c) {
+                    if (s0 + c >= a.n_split || ms[c] == -INFINITY) continue;
+                    const float mx = fmaxf(run_m, ms[c]);
+                    const float sc = run_m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(run_m - mx);
+                    const float w = __builtin_amdgcn_exp2f(ms[c] - mx);
+                    l = fmaf(w, ls[c], l * sc);
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        ov[j] = fmaf(w, oa[c][j], ov[j] * sc);
+                        ov[4 + j] = fmaf(w, ob[c][j], ov[4 + j] * sc);
+                    }
+                    run_m = mx;
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < 8; ++j) ov[j] /= l;
+        }
+        if (a.out_split) {
+            bf16x8 hi, lo;
+            split_hi_lo(make_float4(ov[0], ov[1], ov[2], ov[3]), make_float4(ov[4], ov[5], ov[6], ov[7]), hi, lo);
+            const size_t si = split_index(i, h * HD + d0, MT);
+            *reinterpret_cast<bf16x8 *>(a.out_split + si) = hi;
+            *reinterpret_cast<bf16x8 *>(a.out_split + si + 512) = lo;
+        } else {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) a.out[(size_t)i * D + h * HD + d0 + j] = ov[j];
+        }
+    }
+    if (threadIdx.x == 0) __hip_atomic_store(a.cnt + h, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // fp32 cache (VALU).  K/V tiles of 32 keys sit in LDS as fp32; 16 queries
@@ -1275,13 +1390,18 @@ hipError_t launch_embed_norm(const NormArgs &a, int Mpad, int weight_bf16, hipSt
 hipError_t launch_attention(const AttnArgs &a, int kv_bf16, hipStream_t s)
 {
     const dim3 grid(a.n_split, a.H), block(256);
-    const dim3 block8(64 * DV_ATTN_WAVES);
+    // up to 8 key tiles per split: 8 waves holding one tile each; longer
+    // splits: 4 waves with two tiles in flight each
+    const bool short_split = a.keys_per_split <= 8 * DV_ATTN_TILE;
+    const dim3 b8(512), b4(256);
     if (a.hd == 128) {
-        if (kv_bf16) hipLaunchKernelGGL((k_attn_mfma<128, DV_ATTN_WAVES>), grid, block8, 0, s, a);
-        else hipLaunchKernelGGL(k_attn_f32<128>, grid, block, 0, s, a);
+        if (!kv_bf16) hipLaunchKernelGGL(k_attn_f32<128>, grid, block, 0, s, a);
+        else if (short_split) hipLaunchKernelGGL((k_attn_mfma<128, 8, false>), grid, b8, 0, s, a);
+        else hipLaunchKernelGGL((k_attn_mfma<128, 4, true>), grid, b4, 0, s, a);
     } else if (a.hd == 64) {
-        if (kv_bf16) hipLaunchKernelGGL((k_attn_mfma<64, DV_ATTN_WAVES>), grid, block8, 0, s, a);
-        else hipLaunchKernelGGL(k_attn_f32<64>, grid, block, 0, s, a);
+        if (!kv_bf16) hipLaunchKernelGGL(k_attn_f32<64>, grid, block, 0, s, a);
+        else if (short_split) hipLaunchKernelGGL((k_attn_mfma<64, 8, false>), grid, b8, 0, s, a);
+        else hipLaunchKernelGGL((k_attn_mfma<64, 4, true>), grid, b4, 0, s, a);
     } else {
         return hipErrorInvalidValue;
     }
