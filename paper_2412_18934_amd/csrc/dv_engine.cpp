@@ -60,7 +60,7 @@ struct dv_handle {
     int32_t *arg_idx = nullptr;
     float *rope_cos = nullptr, *rope_sin = nullptr;
     uint16_t *pk_lm = nullptr;
-    StepDesc *d_sd = nullptr, *h_sd = nullptr;
+    StepDesc *h_sd = nullptr;  // the step's tree (kernels get it by value)
     DevAccept *d_acc = nullptr, *h_acc = nullptr;
     GemmPlan p_qkv, p_o, p_gu, p_down, p_lm;
     int n_cu = 256;
@@ -215,7 +215,6 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
     const int M = sd->M, Mpad = sd->Mpad, P = sd->P;
     const int d = c.d_model, hd = c.head_dim, H = c.n_heads, F = c.d_ffn;
     hipStream_t s = h->stream;
-    HIPCHK(h, hipMemcpyAsync(h->d_sd, h->h_sd, sizeof(StepDesc), hipMemcpyHostToDevice, s));
 
     const size_t layer_kv = (size_t)H * kv->capacity * hd * h->esz;
     // attention: the P + M keys of each head are split evenly into
@@ -242,7 +241,7 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
     g.hd = hd;
     g.rope_cos = h->rope_cos;
     g.rope_sin = h->rope_sin;
-    g.pos = h->d_sd->pos;
+    std::memcpy(g.pos, sd->pos, sizeof g.pos);
     g.eps = c.rms_eps;
     g.dn = d;
     g.resid = h->x;
@@ -262,7 +261,10 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
     aa.H = H;
     aa.keys_per_split = kps;
     aa.n_split = n_split;
-    aa.sd = h->d_sd;
+    aa.tm.M = M;
+    aa.tm.P = P;
+    aa.tm.Mpad = Mpad;
+    std::memcpy(aa.tm.anc, sd->anc, sizeof aa.tm.anc);
     aa.part_o = h->part_o;
     aa.part_m = h->part_m;
     aa.part_l = h->part_l;
@@ -308,7 +310,7 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
         na.ssq = h->ssq;
         na.d = d;
         na.M = M;
-        na.tokens = h->d_sd->tokens;
+        std::memcpy(na.tokens, sd->tokens, sizeof na.tokens);
         prof_begin(h, DV_K_NORM);
         hipError_t e = launch_embed_norm(na, Mpad, h->bf16, s);
         prof_end(h);
@@ -350,7 +352,11 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
     ac.arg_val = h->arg_val;
     ac.arg_idx = h->arg_idx;
     ac.n_parts = h->p_lm.n_groups;
-    ac.sd = h->d_sd;
+    ac.M = M;
+    ac.Mpad = Mpad;
+    std::memcpy(ac.tokens, sd->tokens, sizeof ac.tokens);
+    std::memcpy(ac.parents, sd->parents, sizeof ac.parents);
+    std::memcpy(ac.depth, sd->depth, sizeof ac.depth);
     ac.acc = h->d_acc;
     prof_begin(h, DV_K_OTHER);
     hipError_t e = launch_accept(ac, s);
@@ -486,6 +492,11 @@ int dv_verify_init(const dv_config *cfg, const dv_weights *w, void *stream, dv_h
         }
     h->ssq_max = std::max({DV_NORM_SLICES, h->p_o.n_groups, h->p_down.n_groups});
     h->attn_split_max = std::max(ceil_div(c.max_ctx, DV_ATTN_SPLIT_KEYS), ceil_div(512, H));
+    // the attention partials are addressed with 32-bit byte offsets
+    if ((double)H * h->attn_split_max * DV_TREE_MAX * hd * 4 >= 2147483648.0) {
+        dv_verify_free(h);
+        return set_err(nullptr, DV_EINVAL, "max_ctx too large for the attention split buffers");
+    }
 
     auto dalloc = [&](void **p, size_t bytes) -> bool {
         if (hipMalloc(p, bytes) != hipSuccess) return false;
@@ -509,10 +520,9 @@ int dv_verify_init(const dv_config *cfg, const dv_weights *w, void *stream, dv_h
               dalloc((void **)&h->arg_idx, (size_t)h->p_lm.n_groups * rows * 4) &&
               dalloc((void **)&h->rope_cos, (size_t)c.max_ctx * (hd / 2) * 4) &&
               dalloc((void **)&h->rope_sin, (size_t)c.max_ctx * (hd / 2) * 4) &&
-              dalloc((void **)&h->d_sd, sizeof(StepDesc)) &&
               dalloc((void **)&h->d_acc, sizeof(DevAccept));
-    ok = ok && hipHostMalloc((void **)&h->h_sd, sizeof(StepDesc), hipHostMallocDefault) == hipSuccess &&
-         hipHostMalloc((void **)&h->h_acc, sizeof(DevAccept), hipHostMallocDefault) == hipSuccess;
+    h->h_sd = new StepDesc();
+    ok = ok && hipHostMalloc((void **)&h->h_acc, sizeof(DevAccept), hipHostMallocDefault) == hipSuccess;
     if (!ok) {
         std::string msg = std::string("workspace allocation failed: ") + hipGetErrorString(hipGetLastError());
         dv_verify_free(h);
@@ -689,7 +699,6 @@ int dv_prefill(dv_handle *h, const int32_t *tokens, int32_t n, dv_kv *kv, int32_
         fill_desc(h->h_sd, tokens + done, parents, c, kv->len, pos, depth, anc);
         if ((rc = enqueue_forward(h, kv, nullptr, last))) return rc;
         if (last) HIPCHK(h, hipMemcpyAsync(h->h_acc, h->d_acc, sizeof(DevAccept), hipMemcpyDeviceToHost, h->stream));
-        // the staging descriptor is reused by the next chunk
         HIPCHK(h, hipStreamSynchronize(h->stream));
         prof_collect(h);
         kv->len += c;  // a chain's nodes already sit at slots len + k
@@ -709,13 +718,13 @@ void dv_verify_free(dv_handle *h)
                     (void *)h->u_s, (void *)h->attn_s, (void *)h->h_s, (void *)h->ssq,
                     (void *)h->part_o, (void *)h->part_m, (void *)h->part_l, (void *)h->attn_cnt, (void *)h->part_gemm, (void *)h->cnt,
                     (void *)h->arg_val, (void *)h->arg_idx, (void *)h->rope_cos,
-                    (void *)h->rope_sin, (void *)h->d_sd, (void *)h->d_acc})
+                    (void *)h->rope_sin, (void *)h->d_acc})
         if (p) (void)hipFree(p);
     for (auto &w : h->layers)
         for (void *p : {(void *)w.pk_qkv, (void *)w.pk_o, (void *)w.pk_gu, (void *)w.pk_down})
             if (p) (void)hipFree(p);
     if (h->pk_lm) (void)hipFree(h->pk_lm);
-    if (h->h_sd) (void)hipHostFree(h->h_sd);
+    delete h->h_sd;
     if (h->h_acc) (void)hipHostFree(h->h_acc);
     for (auto &e : h->ev_live) { (void)hipEventDestroy(e.a); (void)hipEventDestroy(e.b); }
     for (auto e : h->ev_pool) (void)hipEventDestroy(e);

@@ -11,7 +11,9 @@
 
 #define DV_ATTN_SPLIT_KEYS 256   // keys per workgroup of the fp32-cache attention
 
-// Per-step description of the draft tree, uploaded once per step.
+// Per-step description of the draft tree (host side; the kernels receive
+// the parts they need by value in their arguments, so no kernel reads it
+// from memory before it can address its inputs).
 struct StepDesc {
     int32_t M;        // tree nodes
     int32_t P;        // committed length before the step
@@ -22,6 +24,12 @@ struct StepDesc {
     int32_t pos[DV_TREE_MAX];
     int32_t depth[DV_TREE_MAX];
     uint64_t anc[DV_TREE_MAX];  // bit j set: node j is on node i's root path
+};
+
+// The tree as attention needs it (by value).
+struct TreeMask {
+    int32_t M, P, Mpad, pad0;
+    uint64_t anc[DV_TREE_MAX];
 };
 
 // Result written by the acceptance kernel, copied back to the host.
@@ -73,7 +81,7 @@ struct GemmArgs {
     void *kc, *vc;             // QKV: this layer's K/V cache
     int32_t cap, P, hd;
     const float *rope_cos, *rope_sin;  // [max_ctx][hd/2]
-    const int32_t *pos;        // QKV: device StepDesc.pos
+    int32_t pos[DV_TREE_MAX];  // QKV: position P + depth - 1 of each node
     // input normalisation (QKV, SWIGLU, LOGITS): the activations are x * gain
     // of an RMSNorm whose 1/rms, a per-token scalar that commutes with W, is
     // applied to the outputs: 1/sqrt(sum_j ssq_in[m][j] / dn + eps)
@@ -117,7 +125,7 @@ struct NormArgs {
     float *ssq;                // [Mpad][DV_NORM_SLICES] sums of squares of x
     int32_t d;
     int32_t M;
-    const int32_t *tokens;     // device: StepDesc.tokens
+    int32_t tokens[DV_TREE_MAX];  // token ids of the nodes
 };
 
 struct AttnArgs {
@@ -125,7 +133,7 @@ struct AttnArgs {
     const void *kc, *vc;       // layer cache [H][cap][hd]
     int32_t cap, hd, H;
     int32_t keys_per_split, n_split;
-    const StepDesc *sd;
+    TreeMask tm;
     float *part_o;             // [H][n_split][64][hd] unnormalised split outputs
     float *part_m, *part_l;    // [H][n_split][64] their running max (base 2) and sum
     uint32_t *cnt;             // [H] arrivals of the splits, 0 between launches
@@ -137,7 +145,8 @@ struct AcceptArgs {
     const float *arg_val;      // [64][n_parts] per-group (max, argmax) of the logits
     const int32_t *arg_idx;
     int32_t n_parts;
-    const StepDesc *sd;
+    int32_t M, Mpad;
+    int32_t tokens[DV_TREE_MAX], parents[DV_TREE_MAX], depth[DV_TREE_MAX];
     DevAccept *acc;
 };
 

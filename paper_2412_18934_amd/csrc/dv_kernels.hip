@@ -758,8 +758,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mfma(AttnArgs a)
     const int split = blockIdx.x, h = blockIdx.y;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int n = lane & 15, g = lane >> 4;
-    const StepDesc *sd = a.sd;
-    const int M = sd->M, P = sd->P, total = P + M;
+    const int M = a.tm.M, P = a.tm.P, total = P + M;
     const int kbeg = split * a.keys_per_split;
     const int kend = min(total, kbeg + a.keys_per_split);
     const int ntile = (kend - kbeg + 31) / 32;
@@ -767,10 +766,12 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mfma(AttnArgs a)
     const float scale2 = 1.4426950408889634f / sqrtf((float)HD);
     const uint16_t *kc = reinterpret_cast<const uint16_t *>(a.kc) + (size_t)h * a.cap * HD;
     const uint16_t *vc = reinterpret_cast<const uint16_t *>(a.vc) + (size_t)h * HD * a.cap;
+    // split partials (device-coherent 16-byte stores and loads)
+    const __amdgpu_buffer_rsrc_t po = __builtin_amdgcn_make_buffer_rsrc(a.part_o, (short)0, 0x7fffffff, 0x00020000);
 
     __shared__ u32x4 sm_q[NC * 2 * 64];  // [k-step][hi/lo][lane] B operands
     __shared__ float sm_m[NW][16], sm_l[NW][16];
-    __shared__ float sm_o[NW][16][HD + 4];
+    __shared__ __align__(16) float sm_o[NW][16][HD + 4];
 
     struct Tile {
         u32x4 ka[NC], kb[NC], v[ND];
@@ -803,7 +804,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mfma(AttnArgs a)
             x0 = *reinterpret_cast<const float4 *>(qp);
             x1 = *reinterpret_cast<const float4 *>(qp + 4);
         }
-        const uint64_t anc_raw = sd->anc[min(tok, M - 1)];
+        const uint64_t anc_raw = a.tm.anc[min(tok, M - 1)];
         Tile buf0;
         Tile buf1;  // used with DB only
         if (wave < ntile) load(wave, buf0);
@@ -919,31 +920,39 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mfma(AttnArgs a)
 #pragma unroll
             for (int j = 0; j < 4; ++j) sm_o[wave][4 * g + j][dt * 16 + n] = o[dt][j];
         __syncthreads();
-        for (int e2 = threadIdx.x; e2 < 16 * HD; e2 += 64 * NW) {
-            const int i = e2 / HD, dd = e2 % HD;
+        // 4 consecutive dims of one node per thread
+        for (int e4 = threadIdx.x; e4 < 16 * (HD / 4); e4 += 64 * NW) {
+            const int i = e4 / (HD / 4), d0 = 4 * (e4 % (HD / 4));
             const int ti = q0 + i;
             float mx = -INFINITY;
 #pragma unroll
             for (int w = 0; w < NW; ++w) mx = fmaxf(mx, sm_m[w][i]);
-            float l = 0.f, ov = 0.f;
+            float l = 0.f;
+            f32x4 ov = (f32x4){0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int w = 0; w < NW; ++w) {
                 const float mw = sm_m[w][i];
                 const float wgt = mw == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mw - mx);
                 l = fmaf(wgt, sm_l[w][i], l);
-                ov = fmaf(wgt, sm_o[w][i][dd], ov);
+                const f32x4 o4 = *reinterpret_cast<const f32x4 *>(&sm_o[w][i][d0]);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) ov[j] = fmaf(wgt, o4[j], ov[j]);
             }
             if (a.n_split == 1) {
-                if (ti < sd->Mpad) {
-                    const float r = ti < M ? ov / l : 0.f;
-                    if (a.out_split) store_split(a.out_split, ti, h * HD + dd, sd->Mpad >> 4, r);
-                    else a.out[(size_t)ti * D + h * HD + dd] = r;
+                if (ti < a.tm.Mpad) {
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const float r = ti < M ? ov[j] / l : 0.f;
+                        if (a.out_split) store_split(a.out_split, ti, h * HD + d0 + j, a.tm.Mpad >> 4, r);
+                        else a.out[(size_t)ti * D + h * HD + d0 + j] = r;
+                    }
                 }
             } else if (ti < M) {
                 // published with device-coherent stores for the merging workgroup
                 const size_t pb = ((size_t)h * a.n_split + split) * DV_TREE_MAX + ti;
-                __hip_atomic_store(a.part_o + pb * HD + dd, ov, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                if (dd == 0) {
+                __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, ov), po, (uint32_t)((pb * HD + d0) * 4),
+                                                       0, 16);
+                if (d0 == 0) {
                     __hip_atomic_store(a.part_m + pb, mx, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                     __hip_atomic_store(a.part_l + pb, l, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 }
@@ -966,8 +975,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mfma(AttnArgs a)
     }
     __syncthreads();
     if (!last_s) return;
-    const int Mpad = sd->Mpad, MT = Mpad >> 4;
-    const __amdgpu_buffer_rsrc_t po = __builtin_amdgcn_make_buffer_rsrc(a.part_o, (short)0, 0x7fffffff, 0x00020000);
+    const int Mpad = a.tm.Mpad, MT = Mpad >> 4;
     constexpr int CH = 8;  // splits whose loads are in flight together
     for (int e2 = threadIdx.x; e2 < Mpad * (HD / 8); e2 += 64 * NW) {
         const int i = e2 / (HD / 8), d0 = 8 * (e2 % (HD / 8));
@@ -1026,8 +1034,7 @@ __global__ __launch_bounds__(256) void k_attn_f32(AttnArgs a)
 {
     constexpr int DPT = HD / 16;  // output dims per thread
     const int split = blockIdx.x, h = blockIdx.y, tid = threadIdx.x;
-    const StepDesc *sd = a.sd;
-    const int M = sd->M, P = sd->P, total = P + M;
+    const int M = a.tm.M, P = a.tm.P, total = P + M;
     const int kb = split * a.keys_per_split;
     const int ke = min(total, kb + a.keys_per_split);
     const float scale = 1.0f / sqrtf((float)HD);
@@ -1067,7 +1074,7 @@ __global__ __launch_bounds__(256) void k_attn_f32(AttnArgs a)
                 const int i = e / DV_ATTN_TILE, j = e % DV_ATTN_TILE;
                 const int key = t0 + j;
                 bool vis = i < nq && j < nk;
-                if (vis && key >= P) vis = (sd->anc[q0 + i] >> (key - P)) & 1ull;
+                if (vis && key >= P) vis = (a.tm.anc[q0 + i] >> (key - P)) & 1ull;
                 float s = -INFINITY;
                 if (vis) {
                     float acc = 0.f;
@@ -1112,11 +1119,11 @@ __global__ __launch_bounds__(256) void k_attn_f32(AttnArgs a)
             __syncthreads();
         }
         if (a.n_split == 1) {
-            if (q0 + qi < sd->Mpad) {
+            if (q0 + qi < a.tm.Mpad) {
 #pragma unroll
                 for (int c = 0; c < DPT; ++c) {
                     const float r = qi < nq ? o[c] / lrun[qi] : 0.f;
-                    if (a.out_split) store_split(a.out_split, q0 + qi, h * HD + dd + c, sd->Mpad >> 4, r);
+                    if (a.out_split) store_split(a.out_split, q0 + qi, h * HD + dd + c, a.tm.Mpad >> 4, r);
                     else a.out[(size_t)(q0 + qi) * D + h * HD + dd + c] = r;
                 }
             }
@@ -1143,7 +1150,7 @@ __global__ __launch_bounds__(128) void k_attn_merge(AttnArgs a)
 {
     constexpr int CH = 16;
     const int i = blockIdx.x, h = blockIdx.y, d = threadIdx.x, HD = a.hd;
-    const int M = a.sd->M, MT = gridDim.x >> 4;
+    const int M = a.tm.M, MT = gridDim.x >> 4;
     if (i >= M) {
         if (a.out_split) store_split(a.out_split, i, h * HD + d, MT, 0.f);
         else a.out[(size_t)i * a.H * HD + h * HD + d] = 0.f;
@@ -1197,25 +1204,23 @@ __global__ __launch_bounds__(1024) void k_accept(AcceptArgs a)
 {
     __shared__ int32_t amax[DV_TREE_MAX];
     __shared__ int32_t ok[DV_TREE_MAX];
-    const StepDesc *sd = a.sd;
-    const int M = sd->M, tid = threadIdx.x;
-    // tpt threads per node (64, 32 or 16), each scanning a contiguous chunk of
-    // the tiles 16 loads at a time (clamped indices only repeat a real entry)
-    const int tpt = sd->Mpad <= 16 ? 64 : (sd->Mpad <= 32 ? 32 : 16);
+    const int M = a.M, tid = threadIdx.x;
+    // tpt threads per node (64, 32 or 16) scan the partials with stride tpt
+    // (neighbouring lanes read neighbouring entries), 16 loads in flight
+    // (clamped indices only repeat a real entry)
+    const int tpt = a.Mpad <= 16 ? 64 : (a.Mpad <= 32 ? 32 : 16);
     const int m = tid / tpt, sub = tid % tpt;
     if (m < M) {
         const float *val = a.arg_val + (size_t)m * a.n_parts;
         const int32_t *idx = a.arg_idx + (size_t)m * a.n_parts;
-        const int chunk = (a.n_parts + tpt - 1) / tpt;
-        const int t0 = sub * chunk, t1 = min(a.n_parts, t0 + chunk);
         float best = -INFINITY;
         int bi = 0x7fffffff;
-        for (int t = t0; t < t1; t += 16) {
+        for (int t = sub; t < a.n_parts; t += 16 * tpt) {
             float v[16];
             int ix[16];
 #pragma unroll
             for (int c = 0; c < 16; ++c) {
-                const int tt = min(t + c, t1 - 1);
+                const int tt = min(t + c * tpt, a.n_parts - 1);
                 v[c] = val[tt];
                 ix[c] = idx[tt];
             }
@@ -1235,9 +1240,9 @@ __global__ __launch_bounds__(1024) void k_accept(AcceptArgs a)
     // the tree in LDS, so the serial walk below makes no global round trips
     __shared__ int32_t par_s[DV_TREE_MAX], tok_s[DV_TREE_MAX], dep_s[DV_TREE_MAX];
     if (tid < M) {
-        par_s[tid] = sd->parents[tid];
-        tok_s[tid] = sd->tokens[tid];
-        dep_s[tid] = sd->depth[tid];
+        par_s[tid] = a.parents[tid];
+        tok_s[tid] = a.tokens[tid];
+        dep_s[tid] = a.depth[tid];
     }
     __syncthreads();
     if (tid == 0) {
