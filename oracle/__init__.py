@@ -12,10 +12,11 @@ Pinned (see ``tests/test_oracle_*.py``): every function here is checked against
 something other than itself: an independent Llama implementation from the
 ``transformers`` library, ``torch.nn.functional.scaled_dot_product_attention``,
 sequential decoding, per-path decoding, brute-force acceptance, greedy-decoding
-losslessness and hand-derived closed forms.
+losslessness, hand-derived closed forms and, for sampled acceptance, the
+distribution it must reproduce (Monte Carlo) and its greedy limit.
 """
 from .verify import (  # noqa: F401
     OracleModel, TreeInfo, tree_info, round_cache, bf16_to_f64, rmsnorm, rope,
     attention_node, forward_tree, argmax_lowest, greedy_accept, verify_step, commit,
-    prefill, greedy_decode,
+    prefill, greedy_decode, softmax_t, sample_inverse_cdf, accept_sampled,
 )

@@ -272,6 +272,58 @@ def greedy_accept(tokens, parents, amax):
     return int(info.depth[best]), path, int(amax[best])
 
 
+def softmax_t(z: np.ndarray, temperature: float) -> np.ndarray:
+    """Target distribution at temperature T > 0: softmax(z / T), float64."""
+    z = np.asarray(z, dtype=np.float64) / float(temperature)
+    e = np.exp(z - z.max())
+    return e / e.sum()
+
+
+def sample_inverse_cdf(p: np.ndarray, u: float) -> int:
+    """The smallest token id v with cumsum(p)[v] > u * sum(p) (u in [0, 1))."""
+    c = np.cumsum(np.asarray(p, dtype=np.float64))
+    return int(np.searchsorted(c, u * c[-1], side="right"))
+
+
+def accept_sampled(logits, tokens, parents, q, temperature, u_accept, u_bonus):
+    """Stochastic tree verification (temperature T > 0): recursive rejection
+    sampling over each accepted node's children, the speculative sampling rule
+    the paper applies (Section 3.1) and credits with preserving the target's
+    output distribution (Section 5, "Verifying Draft Tokens").
+
+    Reading used here (the paper gives no formula): the children of node u are
+    independent draws from the draft distribution q[u]; the target
+    distribution at u is p = softmax(logits[u] / T).  Starting at the root,
+    the children of the current node are tried in index order; child c (token
+    t) is accepted when u_accept[c] * q[u][t] < p[t]; a rejected child
+    replaces p by the residual max(p - q[u], 0), renormalised.  When a child
+    is accepted it becomes the current node; when none is, the bonus token is
+    drawn from the current p by inverse CDF with u_bonus[current].
+    Returns (accept_len, path root->last, bonus)."""
+    info = tree_info(parents)
+    tokens = np.asarray(tokens)
+    m = len(tokens)
+    children = [[c for c in range(m) if info.parents[c] == u] for u in range(m)]
+    cur, path = 0, [0]
+    while True:
+        p = softmax_t(logits[cur], temperature)
+        qu = np.asarray(q[cur], dtype=np.float64)
+        moved = False
+        for c in children[cur]:
+            t = int(tokens[c])
+            if float(u_accept[c]) * qu[t] < p[t]:
+                path.append(c)
+                cur = c
+                moved = True
+                break
+            r = np.maximum(p - qu, 0.0)
+            s = r.sum()
+            if s > 0:
+                p = r / s
+        if not moved:
+            return len(path), np.array(path), sample_inverse_cdf(p, float(u_bonus[cur]))
+
+
 def verify_step(model, kv, tokens, parents, dtype=np.float64, kv_dtype=None):
     """One verification step: forward pass + argmax + greedy acceptance."""
     out = forward_tree(model, kv, tokens, parents, dtype=dtype, kv_dtype=kv_dtype)
