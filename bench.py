@@ -103,6 +103,8 @@ def main():
     ap.add_argument("--cpu-baseline", choices=["on", "off"], default="on")
     ap.add_argument("--roofline-events", choices=["inline", "off"], default="inline",
                     help="HIP events around the projection kernels inside the timed region")
+    ap.add_argument("--sampled", choices=["on", "off"], default="on",
+                    help="also time the temperature-1 step (speculative sampling acceptance)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run one 256 MiB device-to-device copy before warm-up (a known-size "
                          "reference dispatch for HBM byte counters)")
@@ -203,6 +205,32 @@ def main():
                     "kernel": "k_proj (QKV, O, gate/up, down, lm_head projections)",
                     "bytes_per_launch": int(per_launch), "avg_launch_us": round(avg_ms * 1e3, 2),
                     "launches_per_step": round(glaunch, 2), "ms_per_step_with_events": round(ms_r, 3)}
+    # sampled leg (after the headline timing): the same forward pass with the
+    # speculative sampling rule at T = 1 over seeded draft distributions, and
+    # that rule alone on the step's logits
+    sampled = None
+    if args.sampled == "on":
+        q = torch.from_numpy(synth.draft_rows(sd["tree"], m, mc.vocab)).to("cuda:0")
+        ua, ub = synth.sampling_uniforms(sd["tree"], m)
+        logits = torch.empty((m, mc.vocab), dtype=torch.float32, device="cuda:0")
+        for _ in range(2):
+            dv.dv_verify_step_sampled(h, toks, par, kv.c, q.data_ptr(), 1.0, ua, ub, logits.data_ptr())
+        torch.cuda.synchronize()
+        t_s = time.perf_counter()
+        for _ in range(args.steps):
+            acc_s = dv.dv_verify_step_sampled(h, toks, par, kv.c, q.data_ptr(), 1.0, ua, ub, logits.data_ptr())
+        torch.cuda.synchronize()
+        ms_s = (time.perf_counter() - t_s) / args.steps * 1e3
+        dv.dv_profile_enable(h, 1 << dv.DV_K_OTHER)
+        dv.dv_profile_read(h, dv.DV_K_OTHER, reset=True)
+        for _ in range(args.steps):
+            dv.dv_accept_sampled(h, logits.data_ptr(), toks, par, q.data_ptr(), 1.0, ua, ub)
+        dv.dv_profile_enable(h, 0)
+        acc_ms, acc_n = dv.dv_profile_read(h, dv.DV_K_OTHER, reset=True)
+        sampled = {"temperature": 1.0, "ms_per_step": round(ms_s, 4), "accept_len": acc_s.accept_len,
+                   "accept_kernel_us": round(acc_ms / max(acc_n, 1) * 1e3, 2)}
+        log("sampled step: %.3f ms, accept kernel %.1f us" % (ms_s, sampled["accept_kernel_us"]))
+        del q, logits
     sbytes = step_bytes(mc, m, p, esz)
     step_gbs = sbytes / (ms * 1e-3) / 1e9
 
@@ -221,6 +249,7 @@ def main():
                      "frac": round(step_gbs / HBM_PEAK_GBS, 4)},
         "roofline": roof,
         "accept_len": acc.accept_len,
+        "sampled": sampled,
     }
     dv.dv_verify_free(h)
     if args.cpu_baseline == "on":

@@ -137,6 +137,46 @@ int dv_verify_init(const dv_config *cfg, const dv_weights *w, void *stream, dv_h
 int dv_verify_step(dv_handle *h, const int32_t *tokens, const int32_t *tree_parents,
                    int32_t n_tree, dv_kv *kv, float *out_logits, dv_accept *out_accept);
 
+/* Stochastic verification at temperature T > 0: the same forward pass as
+ * dv_verify_step, then the speculative sampling rule instead of greedy
+ * matching (Section 3.1 names speculative sampling as the acceptance rule;
+ * Section 5 credits it with keeping the target's output distribution).  Reading: the
+ * children of node u are independent draws from the draft distribution
+ * draft_probs[u]; with p = softmax(logits[u] / T), starting at the root the
+ * children of the current node are tried in index order; child c (token t)
+ * is accepted when u_accept[c] * q[u][t] < p[t] and becomes the current
+ * node; a rejected child replaces p by max(p - q[u], 0), renormalised; when
+ * no child is accepted the bonus token is drawn from the current p by
+ * inverse CDF (smallest id whose running mass exceeds u_bonus[current]
+ * times the total).  All arithmetic is fp32.
+ *   draft_probs: device [n_tree][vocab] fp32, 16-byte aligned, row u = the
+ *       draft distribution at node u (rows of nodes without children are not
+ *       read; entries must be >= 0, rows need not be normalised exactly);
+ *   temperature: finite, > 0;
+ *   u_accept, u_bonus: HOST arrays of n_tree floats in [0, 1) (the random
+ *       numbers the rule draws; u_accept[0] is not used);
+ *   out_logits: as dv_verify_step (16-byte aligned); when NULL the logits
+ *       go to a workspace of the handle;
+ *   other arguments as dv_verify_step.  out_accept->path is the accepted
+ *   chain, bonus_token the drawn token, argmax[] is left 0.  The step is
+ *   pending for dv_kv_commit like a greedy one.
+ * Errors: DV_EINVAL (as dv_verify_step, plus temperature, draft_probs,
+ * uniforms), DV_ECAPACITY, DV_EHIP. */
+int dv_verify_step_sampled(dv_handle *h, const int32_t *tokens, const int32_t *tree_parents,
+                           int32_t n_tree, dv_kv *kv, const float *draft_probs, float temperature,
+                           const float *u_accept, const float *u_bonus, float *out_logits,
+                           dv_accept *out_accept);
+
+/* The sampling rule of dv_verify_step_sampled alone, on caller logits:
+ * logits is device [n_tree][vocab] fp32, 16-byte aligned (row i = the
+ * logits after node i).
+ * Does not touch any cache and leaves no pending step (base_len is set to
+ * -1).  Synchronises the handle's stream.  Errors: DV_EINVAL, DV_EHIP. */
+int dv_accept_sampled(dv_handle *h, const float *logits, const int32_t *tokens,
+                      const int32_t *tree_parents, int32_t n_tree, const float *draft_probs,
+                      float temperature, const float *u_accept, const float *u_bonus,
+                      dv_accept *out_accept);
+
 /* Commit the accepted path of the pending step: for k < accept_len the
  * entries of node path[k] move to slot len + k (all layers, heads, K and V;
  * all sources are read before any destination is written), then

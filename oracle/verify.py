@@ -285,7 +285,7 @@ def sample_inverse_cdf(p: np.ndarray, u: float) -> int:
     return int(np.searchsorted(c, u * c[-1], side="right"))
 
 
-def accept_sampled(logits, tokens, parents, q, temperature, u_accept, u_bonus):
+def accept_sampled(logits, tokens, parents, q, temperature, u_accept, u_bonus, trace=None):
     """Stochastic tree verification (temperature T > 0): recursive rejection
     sampling over each accepted node's children, the speculative sampling rule
     the paper applies (Section 3.1) and credits with preserving the target's
@@ -299,7 +299,12 @@ def accept_sampled(logits, tokens, parents, q, temperature, u_accept, u_bonus):
     replaces p by the residual max(p - q[u], 0), renormalised.  When a child
     is accepted it becomes the current node; when none is, the bonus token is
     drawn from the current p by inverse CDF with u_bonus[current].
-    Returns (accept_len, path root->last, bonus)."""
+    Returns (accept_len, path root->last, bonus).
+
+    ``trace``, when a list, receives every decision the walk takes, for tests
+    that need the margin of a decision: ("accept", child, u*q[t], p[t], mass)
+    per tried child and ("bonus", p, u, mass) at the end, where mass is the
+    product of the residual totals since p was last a softmax."""
     info = tree_info(parents)
     tokens = np.asarray(tokens)
     m = len(tokens)
@@ -308,9 +313,11 @@ def accept_sampled(logits, tokens, parents, q, temperature, u_accept, u_bonus):
     while True:
         p = softmax_t(logits[cur], temperature)
         qu = np.asarray(q[cur], dtype=np.float64)
-        moved = False
+        moved, mass = False, 1.0
         for c in children[cur]:
             t = int(tokens[c])
+            if trace is not None:
+                trace.append(("accept", c, float(u_accept[c]) * qu[t], p[t], mass))
             if float(u_accept[c]) * qu[t] < p[t]:
                 path.append(c)
                 cur = c
@@ -320,7 +327,10 @@ def accept_sampled(logits, tokens, parents, q, temperature, u_accept, u_bonus):
             s = r.sum()
             if s > 0:
                 p = r / s
+                mass *= s
         if not moved:
+            if trace is not None:
+                trace.append(("bonus", p, float(u_bonus[cur]), mass))
             return len(path), np.array(path), sample_inverse_cdf(p, float(u_bonus[cur]))
 
 

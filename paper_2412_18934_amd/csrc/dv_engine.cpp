@@ -62,6 +62,8 @@ struct dv_handle {
     uint16_t *pk_lm = nullptr;
     StepDesc *h_sd = nullptr;  // the step's tree (kernels get it by value)
     DevAccept *d_acc = nullptr, *h_acc = nullptr;
+    float *logits_ws = nullptr;  // [max_tree][vocab] logits of a sampled step without out_logits
+    float *p_ws = nullptr;       // [2][vocab] current / residual distribution of the sampling walk
     GemmPlan p_qkv, p_o, p_gu, p_down, p_lm;
     int n_cu = 256;
 
@@ -207,8 +209,11 @@ int check_tree(dv_handle *h, const int32_t *parents, int n, int base, int32_t *p
 }
 
 // Enqueue the forward pass over the tree described by h->h_sd (already
-// filled) and, when with_head, the lm_head, argmax and acceptance kernels.
-int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_head)
+// filled) and, when with_head, the lm_head, argmax and acceptance kernels
+// (the greedy rule, or the sampling rule when smp is given; out_logits must
+// then be non-null, and smp's logits are set to it).
+int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_head,
+                    SampleArgs *smp = nullptr)
 {
     const dv_config &c = h->cfg;
     StepDesc *sd = h->h_sd;
@@ -348,6 +353,14 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
     if ((rc = gemm(h->p_lm, EPI_LOGITS, h->lm_head, nullptr, nullptr, h->pk_lm, c.vocab, d, h->u, h->u_s,
                    out_logits, nullptr)))
         return rc;
+    if (smp) {
+        smp->logits = out_logits;
+        prof_begin(h, DV_K_OTHER);
+        hipError_t e = launch_accept_sampled(*smp, s);
+        prof_end(h);
+        if (e != hipSuccess) return hip_fail(h, e, "sampled accept launch");
+        return DV_OK;
+    }
     AcceptArgs ac{};
     ac.arg_val = h->arg_val;
     ac.arg_idx = h->arg_idx;
@@ -379,6 +392,39 @@ void fill_desc(StepDesc *sd, const int32_t *tokens, const int32_t *parents, int 
         sd->depth[i] = depth[i];
         sd->anc[i] = anc[i];
     }
+}
+
+// Validate the sampling inputs of a step over an n-node tree and fill the
+// walk's arguments (logits are set by the caller).
+int prepare_sampled(dv_handle *h, const int32_t *tokens, const int32_t *parents, int n,
+                    const float *draft_probs, float temperature, const float *u_accept,
+                    const float *u_bonus, SampleArgs *sa)
+{
+    if (!draft_probs || !u_accept || !u_bonus) return set_err(h, DV_EINVAL, "null draft distribution or uniforms");
+    if (reinterpret_cast<uintptr_t>(draft_probs) % 16)
+        return set_err(h, DV_EINVAL, "draft_probs must be 16-byte aligned");
+    if (!(temperature > 0.f) || !std::isfinite(temperature) || !std::isfinite(1.f / temperature))
+        return set_err(h, DV_EINVAL, "temperature must be finite and > 0 (got %g)", (double)temperature);
+    for (int i = 0; i < n; ++i) {
+        if (!(u_bonus[i] >= 0.f && u_bonus[i] < 1.f))
+            return set_err(h, DV_EINVAL, "u_bonus[%d] = %g outside [0, 1)", i, (double)u_bonus[i]);
+        if (i > 0 && !(u_accept[i] >= 0.f && u_accept[i] < 1.f))
+            return set_err(h, DV_EINVAL, "u_accept[%d] = %g outside [0, 1)", i, (double)u_accept[i]);
+    }
+    std::memset(sa, 0, sizeof *sa);
+    sa->q = draft_probs;
+    sa->p = h->p_ws;
+    sa->V = h->cfg.vocab;
+    sa->M = n;
+    sa->inv_t = 1.f / temperature;
+    for (int i = 0; i < n; ++i) {
+        sa->tokens[i] = tokens[i];
+        sa->parents[i] = parents[i];
+        sa->u_accept[i] = i > 0 ? u_accept[i] : 0.f;
+        sa->u_bonus[i] = u_bonus[i];
+    }
+    sa->acc = h->d_acc;
+    return DV_OK;
 }
 
 int check_kv(dv_handle *h, const dv_kv *kv)
@@ -520,7 +566,9 @@ int dv_verify_init(const dv_config *cfg, const dv_weights *w, void *stream, dv_h
               dalloc((void **)&h->arg_idx, (size_t)h->p_lm.n_groups * rows * 4) &&
               dalloc((void **)&h->rope_cos, (size_t)c.max_ctx * (hd / 2) * 4) &&
               dalloc((void **)&h->rope_sin, (size_t)c.max_ctx * (hd / 2) * 4) &&
-              dalloc((void **)&h->d_acc, sizeof(DevAccept));
+              dalloc((void **)&h->d_acc, sizeof(DevAccept)) &&
+              dalloc((void **)&h->logits_ws, (size_t)c.max_tree * c.vocab * 4) &&
+              dalloc((void **)&h->p_ws, (size_t)2 * c.vocab * 4);
     h->h_sd = new StepDesc();
     ok = ok && hipHostMalloc((void **)&h->h_acc, sizeof(DevAccept), hipHostMallocDefault) == hipSuccess;
     if (!ok) {
@@ -591,8 +639,9 @@ int dv_verify_init(const dv_config *cfg, const dv_weights *w, void *stream, dv_h
     return DV_OK;
 }
 
-int dv_verify_step(dv_handle *h, const int32_t *tokens, const int32_t *tree_parents, int32_t n_tree,
-                   dv_kv *kv, float *out_logits, dv_accept *out_accept)
+static int verify_step_impl(dv_handle *h, const int32_t *tokens, const int32_t *tree_parents, int32_t n_tree,
+                            dv_kv *kv, float *out_logits, dv_accept *out_accept, const float *draft_probs,
+                            float temperature, const float *u_accept, const float *u_bonus, bool sampled)
 {
     if (!h) return set_err(nullptr, DV_EINVAL, "null handle");
     if (h->poisoned) return DV_EHIP;
@@ -610,9 +659,18 @@ int dv_verify_step(dv_handle *h, const int32_t *tokens, const int32_t *tree_pare
     if ((long)kv->len + n_tree > kv->capacity || (long)kv->len + n_tree > h->cfg.max_ctx)
         return set_err(h, DV_ECAPACITY, "len %d + n_tree %d exceeds capacity %d / max_ctx %d",
                        kv->len, n_tree, kv->capacity, h->cfg.max_ctx);
+    SampleArgs sa;
+    if (sampled) {
+        if ((rc = prepare_sampled(h, tokens, tree_parents, n_tree, draft_probs, temperature, u_accept, u_bonus,
+                                  &sa)))
+            return rc;
+        if (out_logits && reinterpret_cast<uintptr_t>(out_logits) % 16)
+            return set_err(h, DV_EINVAL, "out_logits must be 16-byte aligned");
+        if (!out_logits) out_logits = h->logits_ws;
+    }
 
     fill_desc(h->h_sd, tokens, tree_parents, n_tree, kv->len, pos, depth, anc);
-    if ((rc = enqueue_forward(h, kv, out_logits, true))) return rc;
+    if ((rc = enqueue_forward(h, kv, out_logits, true, sampled ? &sa : nullptr))) return rc;
     HIPCHK(h, hipMemcpyAsync(h->h_acc, h->d_acc, sizeof(DevAccept), hipMemcpyDeviceToHost, h->stream));
     HIPCHK(h, hipStreamSynchronize(h->stream));
     prof_collect(h);
@@ -624,7 +682,8 @@ int dv_verify_step(dv_handle *h, const int32_t *tokens, const int32_t *tree_pare
     out_accept->n_tree = n_tree;
     out_accept->base_len = kv->len;
     for (int i = 0; i < a.accept_len && i < DV_MAX_TREE; ++i) out_accept->path[i] = a.path[i];
-    for (int i = 0; i < n_tree; ++i) out_accept->argmax[i] = a.argmax[i];
+    if (!sampled)
+        for (int i = 0; i < n_tree; ++i) out_accept->argmax[i] = a.argmax[i];
 
     h->pending = true;
     h->pend_n = n_tree;
@@ -632,6 +691,59 @@ int dv_verify_step(dv_handle *h, const int32_t *tokens, const int32_t *tree_pare
     h->pend_k = kv->k;
     h->pend_v = kv->v;
     std::memcpy(h->pend_parents, tree_parents, n_tree * sizeof(int32_t));
+    return DV_OK;
+}
+
+int dv_verify_step(dv_handle *h, const int32_t *tokens, const int32_t *tree_parents, int32_t n_tree,
+                   dv_kv *kv, float *out_logits, dv_accept *out_accept)
+{
+    return verify_step_impl(h, tokens, tree_parents, n_tree, kv, out_logits, out_accept, nullptr, 0.f, nullptr,
+                            nullptr, false);
+}
+
+int dv_verify_step_sampled(dv_handle *h, const int32_t *tokens, const int32_t *tree_parents, int32_t n_tree,
+                           dv_kv *kv, const float *draft_probs, float temperature, const float *u_accept,
+                           const float *u_bonus, float *out_logits, dv_accept *out_accept)
+{
+    return verify_step_impl(h, tokens, tree_parents, n_tree, kv, out_logits, out_accept, draft_probs,
+                            temperature, u_accept, u_bonus, true);
+}
+
+int dv_accept_sampled(dv_handle *h, const float *logits, const int32_t *tokens, const int32_t *tree_parents,
+                      int32_t n_tree, const float *draft_probs, float temperature, const float *u_accept,
+                      const float *u_bonus, dv_accept *out_accept)
+{
+    if (!h) return set_err(nullptr, DV_EINVAL, "null handle");
+    if (h->poisoned) return DV_EHIP;
+    if (!logits || !tokens || !tree_parents || !out_accept) return set_err(h, DV_EINVAL, "null argument");
+    if (reinterpret_cast<uintptr_t>(logits) % 16) return set_err(h, DV_EINVAL, "logits must be 16-byte aligned");
+    if (n_tree < 1 || n_tree > h->cfg.max_tree)
+        return set_err(h, DV_EINVAL, "n_tree %d outside [1, %d]", n_tree, h->cfg.max_tree);
+    for (int i = 0; i < n_tree; ++i)
+        if (tokens[i] < 0 || tokens[i] >= h->cfg.vocab)
+            return set_err(h, DV_EINVAL, "token id %d at node %d outside [0, %d)", tokens[i], i, h->cfg.vocab);
+    int32_t pos[DV_MAX_TREE], depth[DV_MAX_TREE];
+    uint64_t anc[DV_MAX_TREE];
+    int rc = check_tree(h, tree_parents, n_tree, 0, pos, depth, anc);
+    if (rc) return rc;
+    SampleArgs sa;
+    if ((rc = prepare_sampled(h, tokens, tree_parents, n_tree, draft_probs, temperature, u_accept, u_bonus, &sa)))
+        return rc;
+    sa.logits = logits;
+    prof_begin(h, DV_K_OTHER);
+    hipError_t e = launch_accept_sampled(sa, h->stream);
+    prof_end(h);
+    if (e != hipSuccess) return hip_fail(h, e, "sampled accept launch");
+    HIPCHK(h, hipMemcpyAsync(h->h_acc, h->d_acc, sizeof(DevAccept), hipMemcpyDeviceToHost, h->stream));
+    HIPCHK(h, hipStreamSynchronize(h->stream));
+    prof_collect(h);
+    const DevAccept &a = *h->h_acc;
+    std::memset(out_accept, 0, sizeof *out_accept);
+    out_accept->accept_len = a.accept_len;
+    out_accept->bonus_token = a.bonus;
+    out_accept->n_tree = n_tree;
+    out_accept->base_len = -1;
+    for (int i = 0; i < a.accept_len && i < DV_MAX_TREE; ++i) out_accept->path[i] = a.path[i];
     return DV_OK;
 }
 
@@ -718,7 +830,7 @@ void dv_verify_free(dv_handle *h)
                     (void *)h->u_s, (void *)h->attn_s, (void *)h->h_s, (void *)h->ssq,
                     (void *)h->part_o, (void *)h->part_m, (void *)h->part_l, (void *)h->attn_cnt, (void *)h->part_gemm, (void *)h->cnt,
                     (void *)h->arg_val, (void *)h->arg_idx, (void *)h->rope_cos,
-                    (void *)h->rope_sin, (void *)h->d_acc})
+                    (void *)h->rope_sin, (void *)h->d_acc, (void *)h->logits_ws, (void *)h->p_ws})
         if (p) (void)hipFree(p);
     for (auto &w : h->layers)
         for (void *p : {(void *)w.pk_qkv, (void *)w.pk_o, (void *)w.pk_gu, (void *)w.pk_down})

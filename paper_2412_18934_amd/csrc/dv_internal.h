@@ -150,6 +150,19 @@ struct AcceptArgs {
     DevAccept *acc;
 };
 
+// Sampled acceptance (one workgroup): the tree walk of the speculative
+// sampling rule over full-vocabulary rows of logits and draft probabilities.
+struct SampleArgs {
+    const float *logits;       // [M][V]
+    const float *q;            // [M][V] draft distributions
+    float *p;                  // [V] workspace: the current (residual) distribution
+    int32_t V, M;
+    float inv_t;               // 1 / temperature
+    int32_t tokens[DV_TREE_MAX], parents[DV_TREE_MAX];
+    float u_accept[DV_TREE_MAX], u_bonus[DV_TREE_MAX];
+    DevAccept *acc;
+};
+
 struct CommitArgs {
     void *kc, *vc;             // whole cache [L][H][cap][hd]
     int32_t LH, cap, hd, P, n;
@@ -170,4 +183,5 @@ hipError_t launch_embed_norm(const NormArgs &a, int Mpad, int weight_bf16, hipSt
 hipError_t launch_attention(const AttnArgs &a, int kv_bf16, hipStream_t s);
 hipError_t launch_attn_merge(const AttnArgs &a, int Mpad, hipStream_t s);
 hipError_t launch_accept(const AcceptArgs &a, hipStream_t s);
+hipError_t launch_accept_sampled(const SampleArgs &a, hipStream_t s);
 hipError_t launch_kv_commit(const CommitArgs &a, int kv_bf16, hipStream_t s);

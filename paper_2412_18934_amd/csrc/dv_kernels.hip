@@ -11,6 +11,7 @@
 //                      LOGITS -> 1/rms, logits + per-group argmax
 //   k_attn / merge   tree-masked attention over the cache, split over keys
 //   k_accept         vocab-wide argmax reduce + greedy acceptance walk
+//   k_accept_sampled speculative sampling walk over full logits rows (T > 0)
 //   k_kv_commit      in-place compaction of the accepted path
 //
 // Weights are bf16 or fp32, activations and accumulation fp32.  Every
@@ -1265,6 +1266,167 @@ __global__ __launch_bounds__(1024) void k_accept(AcceptArgs a)
 }
 
 // ---------------------------------------------------------------------------
+// Sampled acceptance (temperature > 0), one workgroup of 1024 threads walking
+// the tree.  Thread i owns the vocabulary chunk [i ch, i ch + ch), ch a
+// multiple of 4; every total is the chunk summed in id order followed by a
+// fixed butterfly / wave-order combine, so a run is deterministic.  The
+// current distribution is kept unnormalised (P and its total S) in one of two
+// workspace rows, so a rejected child forms its residual without a division:
+// child token t is accepted iff u q(t) S < P(t); the residual is
+// R = max(P - q S, 0), adopted only when its total is positive.  The bonus is
+// the first id whose running mass exceeds u_bonus times the total.
+
+constexpr int SAMPLE_THREADS = 1024;
+
+// Block-wide reduction of one value per thread (OP: 0 sum, 1 max, 2 min),
+// identical in every thread: a butterfly within each wave, then the wave
+// results in wave order.
+template <int OP, typename T>
+__device__ __forceinline__ T red_op(T a, T b)
+{
+    return OP == 0 ? a + b : (OP == 1 ? (a > b ? a : b) : (a < b ? a : b));
+}
+
+template <int OP, typename T>
+__device__ __forceinline__ T block_reduce(T v, T *red)
+{
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v = red_op<OP>(v, __shfl_xor(v, off));
+    __syncthreads();  // red[] is free again
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+    __syncthreads();
+    T r = red[0];
+#pragma unroll
+    for (int w = 1; w < SAMPLE_THREADS / 64; ++w) r = red_op<OP>(r, red[w]);
+    return r;
+}
+
+__global__ __launch_bounds__(SAMPLE_THREADS) void k_accept_sampled(SampleArgs a)
+{
+    __shared__ float red[SAMPLE_THREADS / 64];
+    __shared__ int ired[SAMPLE_THREADS / 64];
+    __shared__ float scan_w[SAMPLE_THREADS / 64];
+    __shared__ int32_t par_s[DV_TREE_MAX], tok_s[DV_TREE_MAX], path_s[DV_TREE_MAX];
+    __shared__ float ua_s[DV_TREE_MAX], ub_s[DV_TREE_MAX];
+    const int tid = threadIdx.x, V = a.V, M = a.M;
+    if (tid < M) {
+        par_s[tid] = a.parents[tid];
+        tok_s[tid] = a.tokens[tid];
+        ua_s[tid] = a.u_accept[tid];
+        ub_s[tid] = a.u_bonus[tid];
+    }
+    if (tid == 0) path_s[0] = 0;
+    const int ch = ((V + 4 * SAMPLE_THREADS - 1) / (4 * SAMPLE_THREADS)) * 4;
+    const int v0 = min(tid * ch, V), v1 = min(v0 + ch, V);
+    const float k2 = a.inv_t * 1.4426950408889634f;  // exp(x / T) = 2^(x log2(e) / T)
+    float *P = a.p, *Pn = a.p + V;
+    float S = 0.f;
+    int cur = 0, n = 1;
+
+    // P <- exp((z - max z) / T) of the logits row at node `node`, S <- its total
+    auto load_dist = [&](int node) {
+        const float4 *z = reinterpret_cast<const float4 *>(a.logits + (size_t)node * V);
+        float mx = -INFINITY;
+        for (int v = v0; v < v1; v += 4) {
+            const float4 t = z[v >> 2];
+            mx = fmaxf(mx, fmaxf(fmaxf(t.x, t.y), fmaxf(t.z, t.w)));
+        }
+        mx = block_reduce<1>(mx, red);
+        float sum = 0.f;
+        for (int v = v0; v < v1; v += 4) {
+            const float4 t = z[v >> 2];
+            float4 e;
+            e.x = exp2f((t.x - mx) * k2);
+            e.y = exp2f((t.y - mx) * k2);
+            e.z = exp2f((t.z - mx) * k2);
+            e.w = exp2f((t.w - mx) * k2);
+            reinterpret_cast<float4 *>(P)[v >> 2] = e;
+            sum += e.x + e.y + e.z + e.w;
+        }
+        S = block_reduce<0>(sum, red);  // its barriers also publish P
+    };
+
+    load_dist(0);
+    int c = 1;
+    while (true) {
+        while (c < M && par_s[c] != cur) ++c;
+        if (c >= M) break;  // no child of cur left: stop here
+        const float *qu = a.q + (size_t)cur * V;
+        const int t = tok_s[c];
+        if (ua_s[c] * qu[t] * S < P[t]) {
+            if (tid == 0) path_s[n] = c;
+            ++n;
+            cur = c;
+            load_dist(cur);
+            c = cur + 1;
+            continue;
+        }
+        // rejected: residual of the current distribution
+        float sum = 0.f;
+        for (int v = v0; v < v1; v += 4) {
+            const float4 pv = reinterpret_cast<const float4 *>(P)[v >> 2];
+            const float4 qv = reinterpret_cast<const float4 *>(qu)[v >> 2];
+            float4 r;
+            r.x = fmaxf(pv.x - qv.x * S, 0.f);
+            r.y = fmaxf(pv.y - qv.y * S, 0.f);
+            r.z = fmaxf(pv.z - qv.z * S, 0.f);
+            r.w = fmaxf(pv.w - qv.w * S, 0.f);
+            reinterpret_cast<float4 *>(Pn)[v >> 2] = r;
+            sum += r.x + r.y + r.z + r.w;
+        }
+        const float S2 = block_reduce<0>(sum, red);
+        if (S2 > 0.f) {
+            float *tmp = P;
+            P = Pn;
+            Pn = tmp;
+            S = S2;
+        }
+        ++c;
+    }
+
+    // bonus: inclusive scan of the chunk totals in thread order
+    float own = 0.f;
+    for (int v = v0; v < v1; v += 4) {
+        const float4 pv = reinterpret_cast<const float4 *>(P)[v >> 2];
+        own += pv.x + pv.y + pv.z + pv.w;
+    }
+    const int lane = tid & 63, wv = tid >> 6;
+    float inc = own;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const float o = __shfl_up(inc, off);
+        if (lane >= off) inc += o;
+    }
+    if (lane == 63) scan_w[wv] = inc;
+    __syncthreads();
+    float wbase = 0.f, total = 0.f;
+    for (int w = 0; w < SAMPLE_THREADS / 64; ++w) {
+        if (w < wv) wbase += scan_w[w];
+        total += scan_w[w];
+    }
+    const float target = ub_s[cur] * total;
+    const float excl = __shfl_up(inc, 1);
+    float run = wbase + (lane ? excl : 0.f);
+    int cand = 0x7fffffff, last_pos = -1;
+    for (int v = v0; v < v1; ++v) {
+        const float pv = P[v];
+        if (pv > 0.f) {
+            last_pos = v;
+            run += pv;
+            if (run > target) { cand = v; break; }
+        }
+    }
+    cand = block_reduce<2>(cand, ired);
+    if (cand == 0x7fffffff)  // rounding left the target beyond the last prefix
+        cand = block_reduce<1>(last_pos, ired);
+    if (tid == 0) {
+        for (int k = 0; k < n; ++k) a.acc->path[k] = path_s[k];
+        a.acc->accept_len = n;
+        a.acc->bonus = cand;
+    }
+}
+
+// ---------------------------------------------------------------------------
 // KV commit: slot P+k <- slot P+path[k] for k < n, for every (layer, head)
 // of K (blockIdx.y = 0, rows [cap][hd]) and V (1, columns of [hd][cap]).  A
 // destination can be the source of another k, so every entry is read into
@@ -1422,6 +1584,13 @@ hipError_t launch_attn_merge(const AttnArgs &a, int Mpad, hipStream_t s)
 hipError_t launch_accept(const AcceptArgs &a, hipStream_t s)
 {
     hipLaunchKernelGGL(k_accept, dim3(1), dim3(1024), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_accept_sampled(const SampleArgs &a, hipStream_t s)
+{
+    if (a.M < 1 || a.M > DV_TREE_MAX || a.V < 4 || a.V % 4) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_accept_sampled, dim3(1), dim3(SAMPLE_THREADS), 0, s, a);
     return hipGetLastError();
 }
 

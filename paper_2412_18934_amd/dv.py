@@ -20,8 +20,9 @@ DV_MAX_TREE = 64
 DV_K_GEMM, DV_K_ATTN, DV_K_NORM, DV_K_OTHER = 0, 1, 2, 3
 
 # every symbol include/dv.h declares
-EXPORTS = ("dv_verify_init", "dv_verify_step", "dv_kv_commit", "dv_prefill", "dv_verify_free",
-           "dv_last_error", "dv_tree_prepare", "dv_profile_enable", "dv_profile_read")
+EXPORTS = ("dv_verify_init", "dv_verify_step", "dv_verify_step_sampled", "dv_accept_sampled",
+           "dv_kv_commit", "dv_prefill", "dv_verify_free", "dv_last_error", "dv_tree_prepare",
+           "dv_profile_enable", "dv_profile_read")
 
 
 class DvError(RuntimeError):
@@ -85,6 +86,13 @@ def lib():
         L.dv_verify_step.argtypes = [vp, i32p, i32p, i32, ctypes.POINTER(dv_kv), vp,
                                      ctypes.POINTER(dv_accept)]
         L.dv_verify_step.restype = ctypes.c_int
+        f32p = ctypes.POINTER(ctypes.c_float)
+        L.dv_verify_step_sampled.argtypes = [vp, i32p, i32p, i32, ctypes.POINTER(dv_kv), vp, ctypes.c_float,
+                                             f32p, f32p, vp, ctypes.POINTER(dv_accept)]
+        L.dv_verify_step_sampled.restype = ctypes.c_int
+        L.dv_accept_sampled.argtypes = [vp, vp, i32p, i32p, i32, vp, ctypes.c_float, f32p, f32p,
+                                        ctypes.POINTER(dv_accept)]
+        L.dv_accept_sampled.restype = ctypes.c_int
         L.dv_kv_commit.argtypes = [vp, ctypes.POINTER(dv_kv), ctypes.POINTER(dv_accept)]
         L.dv_kv_commit.restype = ctypes.c_int
         L.dv_prefill.argtypes = [vp, i32p, i32, ctypes.POINTER(dv_kv), i32p]
@@ -135,6 +143,44 @@ def dv_verify_step(h, tokens, tree_parents, kv: dv_kv, out_logits: int = 0) -> d
     acc = dv_accept()
     rc = lib().dv_verify_step(h, _ptr(t), _ptr(p), len(t), ctypes.byref(kv),
                               ctypes.c_void_p(out_logits or None), ctypes.byref(acc))
+    _check(rc, h)
+    return acc
+
+
+def _f32(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.float32))
+
+
+def _fptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_float))
+
+
+def dv_verify_step_sampled(h, tokens, tree_parents, kv: dv_kv, draft_probs: int, temperature: float,
+                           u_accept, u_bonus, out_logits: int = 0) -> dv_accept:
+    """draft_probs / out_logits: device addresses; u_accept / u_bonus: host arrays."""
+    t, p = _i32(tokens), _i32(tree_parents)
+    ua, ub = _f32(u_accept), _f32(u_bonus)
+    if len(ua) < len(t) or len(ub) < len(t):
+        raise ValueError("u_accept and u_bonus need one entry per tree node")
+    acc = dv_accept()
+    rc = lib().dv_verify_step_sampled(h, _ptr(t), _ptr(p), len(t), ctypes.byref(kv),
+                                      ctypes.c_void_p(draft_probs or None), float(temperature), _fptr(ua),
+                                      _fptr(ub), ctypes.c_void_p(out_logits or None), ctypes.byref(acc))
+    _check(rc, h)
+    return acc
+
+
+def dv_accept_sampled(h, logits: int, tokens, tree_parents, draft_probs: int, temperature: float,
+                      u_accept, u_bonus) -> dv_accept:
+    """logits / draft_probs: device addresses; u_accept / u_bonus: host arrays."""
+    t, p = _i32(tokens), _i32(tree_parents)
+    ua, ub = _f32(u_accept), _f32(u_bonus)
+    if len(ua) < len(t) or len(ub) < len(t):
+        raise ValueError("u_accept and u_bonus need one entry per tree node")
+    acc = dv_accept()
+    rc = lib().dv_accept_sampled(h, ctypes.c_void_p(logits or None), _ptr(t), _ptr(p), len(t),
+                                 ctypes.c_void_p(draft_probs or None), float(temperature), _fptr(ua), _fptr(ub),
+                                 ctypes.byref(acc))
     _check(rc, h)
     return acc
 

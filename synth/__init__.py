@@ -175,6 +175,7 @@ def shrink(model: ModelCfg, **kw) -> ModelCfg:
 # tensor ids inside one seed
 
 T_EMBED, T_LMHEAD, T_PROMPT, T_TREE_PARENT, T_TREE_TOKEN = 1, 2, 3, 4, 5
+T_UNIFORM, T_DRAFT = 6, 7
 LAYER_NAMES = ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down")
 
 
@@ -264,6 +265,27 @@ def random_tree(seed: int, n: int, depth: int, vocab: int, chain: bool = False,
         parents[i] = p
         dep[i] = dep[p] + 1
     return toks, parents
+
+
+def uniform01(seed: int, tensor: int, n: int, start: int = 0) -> np.ndarray:
+    """``n`` float32 uniforms in [0, 1): the top 24 bits of the stream, so
+    every value is exact in float32 and strictly below 1."""
+    return (u64(seed, tensor, n, start) >> np.uint64(40)).astype(np.float32) * np.float32(2.0 ** -24)
+
+
+def sampling_uniforms(seed: int, n: int, stream: int = 0):
+    """The random numbers of one sampled acceptance over an n-node tree:
+    (u_accept float32[n], u_bonus float32[n])."""
+    u = uniform01(seed, T_UNIFORM + 16 * stream, 2 * n)
+    return u[:n].copy(), u[n:].copy()
+
+
+def draft_rows(seed: int, m: int, vocab: int, sharp: float = 8.0, stream: int = 0) -> np.ndarray:
+    """m draft distributions over the vocabulary, float32 [m][vocab]: uniforms
+    raised to ``sharp`` (a few ids carry most of the mass), each row divided
+    by its float64 total."""
+    w = uniform01(seed, T_DRAFT + 16 * stream, m * vocab).astype(np.float64).reshape(m, vocab) ** sharp
+    return (w / w.sum(axis=1, keepdims=True)).astype(np.float32)
 
 
 def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:

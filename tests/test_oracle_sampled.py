@@ -1,7 +1,7 @@
 """Pins of the oracle's stochastic (temperature > 0) acceptance.
 
-The paper fixes no formula for its "speculative sampling algorithm" (Section
-3.1) beyond what it credits it with (Section 5, "Verifying Draft Tokens"): the
+The paper fixes no formula for its speculative sampling rule (Section 3.1)
+beyond what it credits it with (Section 5, on verifying draft tokens): the
 accepted tokens follow the target model's own distribution.  That property is
 the pin: with drafts drawn from q, the tokens emitted by ``accept_sampled``
 must be distributed exactly as target sampling would emit them (chi-square over
