@@ -1301,6 +1301,20 @@ __device__ __forceinline__ T block_reduce(T v, T *red)
     return r;
 }
 
+// Up to SAMPLE_BATCH float4 of a thread's chunk, all loads issued before any
+// is used (entries past v1 read as `fill`).
+constexpr int SAMPLE_BATCH = 8;
+
+__device__ __forceinline__ void load_batch(const float *base, int v, int v1, float fill,
+                                           float4 (&t)[SAMPLE_BATCH])
+{
+#pragma unroll
+    for (int j = 0; j < SAMPLE_BATCH; ++j) {
+        const int vv = v + 4 * j;
+        t[j] = vv < v1 ? reinterpret_cast<const float4 *>(base)[vv >> 2] : make_float4(fill, fill, fill, fill);
+    }
+}
+
 __global__ __launch_bounds__(SAMPLE_THREADS) void k_accept_sampled(SampleArgs a)
 {
     __shared__ float red[SAMPLE_THREADS / 64];
@@ -1323,25 +1337,38 @@ __global__ __launch_bounds__(SAMPLE_THREADS) void k_accept_sampled(SampleArgs a)
     float S = 0.f;
     int cur = 0, n = 1;
 
-    // P <- exp((z - max z) / T) of the logits row at node `node`, S <- its total
+    // P <- exp((z - max z) / T) of the logits row at node `node`, S <- its
+    // total.  The first batch of the chunk (the whole chunk up to a
+    // 32768-id vocabulary) stays in registers between the two passes.
     auto load_dist = [&](int node) {
-        const float4 *z = reinterpret_cast<const float4 *>(a.logits + (size_t)node * V);
+        const float *z = a.logits + (size_t)node * V;
+        float4 t0[SAMPLE_BATCH], t[SAMPLE_BATCH];
+        load_batch(z, v0, v1, -INFINITY, t0);
         float mx = -INFINITY;
-        for (int v = v0; v < v1; v += 4) {
-            const float4 t = z[v >> 2];
-            mx = fmaxf(mx, fmaxf(fmaxf(t.x, t.y), fmaxf(t.z, t.w)));
+#pragma unroll
+        for (int j = 0; j < SAMPLE_BATCH; ++j) mx = fmaxf(mx, fmaxf(fmaxf(t0[j].x, t0[j].y), fmaxf(t0[j].z, t0[j].w)));
+        for (int v = v0 + 4 * SAMPLE_BATCH; v < v1; v += 4 * SAMPLE_BATCH) {
+            load_batch(z, v, v1, -INFINITY, t);
+#pragma unroll
+            for (int j = 0; j < SAMPLE_BATCH; ++j) mx = fmaxf(mx, fmaxf(fmaxf(t[j].x, t[j].y), fmaxf(t[j].z, t[j].w)));
         }
         mx = block_reduce<1>(mx, red);
         float sum = 0.f;
-        for (int v = v0; v < v1; v += 4) {
-            const float4 t = z[v >> 2];
-            float4 e;
-            e.x = exp2f((t.x - mx) * k2);
-            e.y = exp2f((t.y - mx) * k2);
-            e.z = exp2f((t.z - mx) * k2);
-            e.w = exp2f((t.w - mx) * k2);
-            reinterpret_cast<float4 *>(P)[v >> 2] = e;
-            sum += e.x + e.y + e.z + e.w;
+        for (int v = v0; v < v1; v += 4 * SAMPLE_BATCH) {
+            if (v != v0) load_batch(z, v, v1, -INFINITY, t);
+#pragma unroll
+            for (int j = 0; j < SAMPLE_BATCH; ++j) {
+                const float4 x = v == v0 ? t0[j] : t[j];
+                if (v + 4 * j < v1) {
+                    float4 e;
+                    e.x = exp2f((x.x - mx) * k2);
+                    e.y = exp2f((x.y - mx) * k2);
+                    e.z = exp2f((x.z - mx) * k2);
+                    e.w = exp2f((x.w - mx) * k2);
+                    reinterpret_cast<float4 *>(P)[(v >> 2) + j] = e;
+                    sum += e.x + e.y + e.z + e.w;
+                }
+            }
         }
         S = block_reduce<0>(sum, red);  // its barriers also publish P
     };
@@ -1363,16 +1390,22 @@ __global__ __launch_bounds__(SAMPLE_THREADS) void k_accept_sampled(SampleArgs a)
         }
         // rejected: residual of the current distribution
         float sum = 0.f;
-        for (int v = v0; v < v1; v += 4) {
-            const float4 pv = reinterpret_cast<const float4 *>(P)[v >> 2];
-            const float4 qv = reinterpret_cast<const float4 *>(qu)[v >> 2];
-            float4 r;
-            r.x = fmaxf(pv.x - qv.x * S, 0.f);
-            r.y = fmaxf(pv.y - qv.y * S, 0.f);
-            r.z = fmaxf(pv.z - qv.z * S, 0.f);
-            r.w = fmaxf(pv.w - qv.w * S, 0.f);
-            reinterpret_cast<float4 *>(Pn)[v >> 2] = r;
-            sum += r.x + r.y + r.z + r.w;
+        for (int v = v0; v < v1; v += 4 * SAMPLE_BATCH) {
+            float4 pv[SAMPLE_BATCH], qv[SAMPLE_BATCH];
+            load_batch(P, v, v1, 0.f, pv);
+            load_batch(qu, v, v1, 0.f, qv);
+#pragma unroll
+            for (int j = 0; j < SAMPLE_BATCH; ++j) {
+                if (v + 4 * j < v1) {
+                    float4 r;
+                    r.x = fmaxf(pv[j].x - qv[j].x * S, 0.f);
+                    r.y = fmaxf(pv[j].y - qv[j].y * S, 0.f);
+                    r.z = fmaxf(pv[j].z - qv[j].z * S, 0.f);
+                    r.w = fmaxf(pv[j].w - qv[j].w * S, 0.f);
+                    reinterpret_cast<float4 *>(Pn)[(v >> 2) + j] = r;
+                    sum += r.x + r.y + r.z + r.w;
+                }
+            }
         }
         const float S2 = block_reduce<0>(sum, red);
         if (S2 > 0.f) {
@@ -1384,11 +1417,14 @@ __global__ __launch_bounds__(SAMPLE_THREADS) void k_accept_sampled(SampleArgs a)
         ++c;
     }
 
-    // bonus: inclusive scan of the chunk totals in thread order
+    // bonus: inclusive scan of the chunk totals in thread order, then each
+    // thread walks its own chunk from its exclusive prefix
     float own = 0.f;
-    for (int v = v0; v < v1; v += 4) {
-        const float4 pv = reinterpret_cast<const float4 *>(P)[v >> 2];
-        own += pv.x + pv.y + pv.z + pv.w;
+    for (int v = v0; v < v1; v += 4 * SAMPLE_BATCH) {
+        float4 pv[SAMPLE_BATCH];
+        load_batch(P, v, v1, 0.f, pv);
+#pragma unroll
+        for (int j = 0; j < SAMPLE_BATCH; ++j) own += pv[j].x + pv[j].y + pv[j].z + pv[j].w;
     }
     const int lane = tid & 63, wv = tid >> 6;
     float inc = own;
@@ -1408,12 +1444,20 @@ __global__ __launch_bounds__(SAMPLE_THREADS) void k_accept_sampled(SampleArgs a)
     const float excl = __shfl_up(inc, 1);
     float run = wbase + (lane ? excl : 0.f);
     int cand = 0x7fffffff, last_pos = -1;
-    for (int v = v0; v < v1; ++v) {
-        const float pv = P[v];
-        if (pv > 0.f) {
-            last_pos = v;
-            run += pv;
-            if (run > target) { cand = v; break; }
+    for (int v = v0; v < v1 && cand == 0x7fffffff; v += 4 * SAMPLE_BATCH) {
+        float4 pv[SAMPLE_BATCH];
+        load_batch(P, v, v1, 0.f, pv);
+#pragma unroll
+        for (int j = 0; j < SAMPLE_BATCH; ++j) {
+            const float e[4] = {pv[j].x, pv[j].y, pv[j].z, pv[j].w};
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                if (cand == 0x7fffffff && e[k] > 0.f) {
+                    last_pos = v + 4 * j + k;
+                    run += e[k];
+                    if (run > target) cand = last_pos;
+                }
+            }
         }
     }
     cand = block_reduce<2>(cand, ired);

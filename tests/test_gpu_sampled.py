@@ -134,11 +134,13 @@ def test_accept_sampled_matches_oracle(head_case, m, temperature):
     assert differ <= 1, (exact, differ)
 
 
-def test_accept_sampled_ragged_chunks():
-    # vocab 8224: threads own 12 ids each, the last busy thread 4, the rest none
-    case = GpuCase(small_cfg(n_layers=1, n_heads=1, head_dim=64, vocab=8224), seed=6, capacity=64)
+@pytest.mark.parametrize("V", [8224, 40992])
+def test_accept_sampled_ragged_chunks(V):
+    # 8224: threads own 12 ids each, the last busy thread 4, the rest none;
+    # 40992: 44 ids each (a second load batch), the last busy thread 28
+    case = GpuCase(small_cfg(n_layers=1, n_heads=1, head_dim=64, vocab=V), seed=6, capacity=64)
     try:
-        V, exact = 8224, 0
+        exact = 0
         for seed in range(20):
             m = 1 + seed * 3
             rng = np.random.default_rng(seed)
