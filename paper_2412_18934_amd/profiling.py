@@ -58,10 +58,11 @@ def summarize_stats(stats_csv, trace_csv, out_path, command):
             gemm_n += n
     lines += ["", "Projection kernels (k_proj, k_gemm_valu): %d launches, average %.2f us."
               % (gemm_n, gemm_ns / max(gemm_n, 1) / 1e3)]
-    # one full step from the trace: the span between two k_accept dispatches
+    # one full greedy step from the trace: the span between two k_accept
+    # dispatches (the sampled leg that follows ends in k_accept_sampled)
     trace = list(csv.DictReader(open(trace_csv)))
     trace.sort(key=lambda r: int(r["Start_Timestamp"]))
-    acc = [i for i, r in enumerate(trace) if _short(r["Kernel_Name"]).startswith("k_accept")]
+    acc = [i for i, r in enumerate(trace) if _short(r["Kernel_Name"]) == "k_accept"]
     if len(acc) >= 2:
         step = trace[acc[-2] + 1: acc[-1] + 1]
         span = (int(step[-1]["End_Timestamp"]) - int(step[0]["Start_Timestamp"])) / 1e3
