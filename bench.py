@@ -29,19 +29,32 @@ HBM_PEAK_GBS = 8000.0
 # rocprofv3 FETCH_SIZE/WRITE_SIZE summary of the default workload (bytes per dispatch)
 HBM_WORKLOAD = "llama13b-bf16-m16-ctx1024"
 HBM_PROFILE = "verify_step_llama13b_m16_ctx1024_hbm_bytes.txt"
+I8_WORKLOAD = "llama13b-i8-m16-ctx1024"
 
 
 def log(msg):
     print("[bench] " + msg, file=sys.stderr, flush=True)
 
 
-def gemm_bytes(mc, m, esz):
-    """Algorithmic bytes of the projection kernels in one step: weights once,
-    activations in once (split bf16 hi + lo: 4 bytes per value), outputs out
-    once; the residual projections also read and write their rows of the
-    fp32 residual stream and write the next RMSNorm's input."""
+def weight_bytes(mc):
+    """Bytes per projection weight, and per output row (int8: its fp32 scale)."""
+    return {"bf16": (2, 0), "f32": (4, 0), "i8": (1, 4)}[mc.weight_dtype]
+
+
+def kv_bytes(mc):
+    return 4 if mc.kv_dtype == "f32" else 2
+
+
+def gemm_bytes(mc, m):
+    """Algorithmic bytes of the projection kernels in one step: weights once
+    (int8: plus one fp32 scale per row), activations in once (split bf16 hi +
+    lo: 4 bytes per value), outputs out once; the residual projections also
+    read and write their rows of the fp32 residual stream and write the next
+    RMSNorm's input."""
     d, f, v, L = mc.d_model, mc.d_ffn, mc.vocab, mc.n_layers
-    w = esz * (L * (4 * d * d + 3 * d * f) + v * d)
+    wsz, rsz = weight_bytes(mc)
+    esz = kv_bytes(mc)
+    w = wsz * (L * (4 * d * d + 3 * d * f) + v * d) + rsz * (L * (4 * d + 2 * f + d) + v)
     per_layer = 4 * m * (d + d + 2 * d * esz / 4      # QKV: in, q out, k/v cache write
                          + d + 2 * d + d              # O: in, residual read+write, next input
                          + d + f                      # gate/up: in, h out
@@ -50,12 +63,71 @@ def gemm_bytes(mc, m, esz):
     return w + L * per_layer + head, 4 * L + 1
 
 
-def step_bytes(mc, m, p, esz):
+def step_bytes(mc, m, p):
     """Algorithmic HBM bytes of a whole step (no logits written)."""
     d, L, H, hd = mc.d_model, mc.n_layers, mc.n_heads, mc.head_dim
-    g, _ = gemm_bytes(mc, m, esz)
+    g, _ = gemm_bytes(mc, m)
+    esz = kv_bytes(mc)
     kv_read = L * 2 * H * (p + m) * hd * esz
     return g + kv_read + m * d * esz
+
+
+def int8_leg(args):
+    """The weight-only int8 variant of the 13B workload (same context, tree and
+    seeds): K timed steps, then the projection launches timed by HIP events."""
+    import torch
+    from paper_2412_18934_amd import device as D
+    from paper_2412_18934_amd import dv
+    wl = synth.WORKLOADS[I8_WORKLOAD]
+    mc, sd = wl.model, wl.seeds
+    m, p = wl.n_tree, wl.context
+    t0 = time.perf_counter()
+    W = D.DeviceWeights(mc.n_layers, lambda l: synth.layer_weights(mc, sd["weights"], l),
+                        synth.embed(mc, sd["weights"]), synth.lm_head(mc, sd["weights"]),
+                        synth.final_norm(mc), lm_head_scale=synth.lm_head_scale(mc, sd["weights"]))
+    cap = p + 64
+    kv = D.DeviceKV(mc.n_layers, mc.n_heads, mc.head_dim, cap, mc.weight_dtype)
+    for l in range(mc.n_layers):
+        k, v = synth.kv_layer(mc, sd["kv"], l, p)
+        kv.set_layer(l, k, v)
+    kv.c.len = p
+    toks, par = synth.random_tree(sd["tree"], m, wl.depth, mc.vocab, chain=wl.chain)
+    log("int8 inputs resident (%.1f GB weights) after %.1f s" % (W.nbytes() / 1e9, time.perf_counter() - t0))
+    cfg = D.make_config(mc.n_layers, mc.d_model, mc.n_heads, mc.head_dim, mc.d_ffn, mc.vocab,
+                        mc.rms_eps, mc.rope_base, mc.weight_dtype, cap, 64)
+    h = dv.dv_verify_init(cfg, W.c, torch.cuda.current_stream().cuda_stream)
+    try:
+        for _ in range(args.warmup):
+            dv.dv_verify_step(h, toks, par, kv.c, 0)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        for _ in range(args.steps):
+            acc = dv.dv_verify_step(h, toks, par, kv.c, 0)
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t1) / args.steps * 1e3
+        dv.dv_profile_enable(h, 1 << dv.DV_K_GEMM)
+        dv.dv_profile_read(h, dv.DV_K_GEMM, reset=True)
+        for _ in range(args.steps):
+            dv.dv_verify_step(h, toks, par, kv.c, 0)
+        dv.dv_profile_enable(h, 0)
+        gemm_ms, gemm_n = dv.dv_profile_read(h, dv.DV_K_GEMM, reset=True)
+    finally:
+        dv.dv_verify_free(h)
+    gbytes, _ = gemm_bytes(mc, m)
+    sbytes = step_bytes(mc, m, p)
+    per_launch = gbytes / (gemm_n / args.steps)
+    proj_gbs = per_launch / (gemm_ms / gemm_n * 1e-3) / 1e9
+    step_gbs = sbytes / (ms * 1e-3) / 1e9
+    log("int8 step: %.3f ms (%.0f GB/s algorithmic)" % (ms, step_gbs))
+    del W, kv
+    torch.cuda.empty_cache()
+    return {"workload": wl.name, "weights": "int8 per-row scales; bf16 KV; fp32 activations",
+            "ms_per_step": round(ms, 4), "value": round(m / (ms * 1e-3), 2), "unit": "draft tokens/s",
+            "accept_len": acc.accept_len,
+            "step_hbm": {"bytes": int(sbytes), "achieved_gbs": round(step_gbs, 1),
+                         "frac": round(step_gbs / HBM_PEAK_GBS, 4)},
+            "proj": {"bytes_per_launch": int(per_launch), "avg_launch_us": round(gemm_ms / gemm_n * 1e3, 2),
+                     "achieved_gbs": round(proj_gbs, 1), "frac": round(proj_gbs / HBM_PEAK_GBS, 4)}}
 
 
 def cpu_baseline(wl, toks, par):
@@ -78,7 +150,8 @@ def cpu_baseline(wl, toks, par):
     del raw_kv
     om = ov.OracleModel(mc, lambda l: layers[l],
                         lambda ids: synth.embed_rows(mc, sd["weights"], ids),
-                        synth.lm_head(mc, sd["weights"]), synth.final_norm(mc))
+                        synth.lm_head(mc, sd["weights"]), synth.final_norm(mc),
+                        lm_head_scale=synth.lm_head_scale(mc, sd["weights"]))
     log("cpu oracle inputs ready in %.1f s" % (time.perf_counter() - t0))
     t0 = time.perf_counter()
     ov.verify_step(om, kv_o, toks, par)
@@ -105,6 +178,8 @@ def main():
                     help="HIP events around the projection kernels inside the timed region")
     ap.add_argument("--sampled", choices=["on", "off"], default="on",
                     help="also time the temperature-1 step (speculative sampling acceptance)")
+    ap.add_argument("--int8", choices=["on", "off"], default="on",
+                    help="also time the weight-only int8 variant of the 13B workload")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run one 256 MiB device-to-device copy before warm-up (a known-size "
                          "reference dispatch for HBM byte counters)")
@@ -121,7 +196,6 @@ def main():
         wl = synth.WORKLOADS[args.workload]
     mc, sd = wl.model, wl.seeds
     m, p = wl.n_tree, wl.context
-    esz = 2 if mc.weight_dtype == "bf16" else 4
 
     import torch
     from paper_2412_18934_amd import device as D
@@ -140,7 +214,8 @@ def main():
         return synth.layer_weights(mc, sd["weights"], l)
 
     W = D.DeviceWeights(mc.n_layers, layer_fn, synth.embed(mc, sd["weights"]),
-                        synth.lm_head(mc, sd["weights"]), synth.final_norm(mc))
+                        synth.lm_head(mc, sd["weights"]), synth.final_norm(mc),
+                        lm_head_scale=synth.lm_head_scale(mc, sd["weights"]))
     cap = p + 64
     kv = D.DeviceKV(mc.n_layers, mc.n_heads, mc.head_dim, cap, mc.weight_dtype)
     for l in range(mc.n_layers):
@@ -175,9 +250,55 @@ def main():
     ms = elapsed / args.steps * 1e3
     log("timed %d steps: %.3f ms/step" % (args.steps, ms))
 
+    # latency distribution: each call ends with the accept struct on the host,
+    # so the host clock around one call is that step's latency
+    lat = []
+    for _ in range(args.steps):
+        t1 = time.perf_counter()
+        dv.dv_verify_step(h, toks, par, kv.c, 0)
+        lat.append((time.perf_counter() - t1) * 1e3)
+    lat_ms = {"p10": round(float(np.percentile(lat, 10)), 4), "p50": round(float(np.median(lat)), 4),
+              "p90": round(float(np.percentile(lat, 90)), 4)}
+
+    # commit latency: a step, then the commit of a 5-node root path (the
+    # deepest node's ancestors, clipped), after which the cache length is set
+    # back so every repetition sees the same context
+    depth = np.ones(m, dtype=np.int64)
+    for i in range(1, m):
+        depth[i] = depth[par[i]] + 1
+    node = int(np.argmax(depth))
+    chain = [node]
+    while par[chain[-1]] >= 0:
+        chain.append(int(par[chain[-1]]))
+    chain = chain[::-1][:5]
+    commit_ms = []
+    for _ in range(min(args.steps, 10)):
+        a = dv.dv_verify_step(h, toks, par, kv.c, 0)
+        a.accept_len = len(chain)
+        for k, nd in enumerate(chain):
+            a.path[k] = nd
+        t1 = time.perf_counter()
+        dv.dv_kv_commit(h, kv.c, a)
+        torch.cuda.synchronize()
+        commit_ms.append((time.perf_counter() - t1) * 1e3)
+        kv.c.len = p
+
+    # streaming probe: one 1 GiB device copy (2 GiB moved), best of 3
+    src = torch.empty(256 << 20, dtype=torch.float32, device="cuda:0").fill_(1.0)
+    dst = torch.empty_like(src)
+    best = float("inf")
+    for _ in range(4):
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        best = min(best, time.perf_counter() - t1)
+    probe_gbs = 2 * src.nbytes / best / 1e9
+    del src, dst
+
     # roofline pass: the same steps again with every projection launch timed
     # by HIP events recorded by its own dispatch on the library's stream
-    gbytes, glaunch = gemm_bytes(mc, m, esz)
+    gbytes, glaunch = gemm_bytes(mc, m)
     roof = None
     if args.roofline_events == "inline":
         dv.dv_profile_enable(h, 1 << dv.DV_K_GEMM)
@@ -231,7 +352,7 @@ def main():
                    "accept_kernel_us": round(acc_ms / max(acc_n, 1) * 1e3, 2)}
         log("sampled step: %.3f ms, accept kernel %.1f us" % (ms_s, sampled["accept_kernel_us"]))
         del q, logits
-    sbytes = step_bytes(mc, m, p, esz)
+    sbytes = step_bytes(mc, m, p)
     step_gbs = sbytes / (ms * 1e-3) / 1e9
 
     result = {
@@ -246,15 +367,20 @@ def main():
                    "layers": mc.n_layers, "d_model": mc.d_model, "d_ffn": mc.d_ffn,
                    "vocab": mc.vocab},
         "step_hbm": {"bytes": int(sbytes), "achieved_gbs": round(step_gbs, 1),
-                     "frac": round(step_gbs / HBM_PEAK_GBS, 4)},
+                     "frac": round(step_gbs / HBM_PEAK_GBS, 4),
+                     "copy_probe_gbs": round(probe_gbs, 1), "frac_of_probe": round(step_gbs / probe_gbs, 4)},
+        "latency_ms": lat_ms,
+        "commit_ms": {"path_len": len(chain), "p50": round(float(np.median(commit_ms)), 4)},
         "roofline": roof,
         "accept_len": acc.accept_len,
         "sampled": sampled,
     }
     dv.dv_verify_free(h)
+    del W, kv
+    torch.cuda.empty_cache()
+    if args.int8 == "on" and wl.name == HBM_WORKLOAD:
+        result["int8"] = int8_leg(args)
     if args.cpu_baseline == "on":
-        del W, kv
-        torch.cuda.empty_cache()
         result["cpu_baseline"] = cpu_baseline(wl, toks, par)
     print(json.dumps(result), flush=True)
 

@@ -54,13 +54,19 @@ extern "C" {
 
 #define DV_F32 0
 #define DV_BF16 1
+/* Weight-only int8 (the int8 setting the paper runs its target in on the
+ * laptop, Section 4): every projection matrix (wq, wk, wv, wo, w_gate, w_up,
+ * w_down, lm_head) is int8 [out][in] with one fp32 scale per output row,
+ * W[r][c] = scale[r] * q[r][c]; the embedding, the norm gains and the KV
+ * cache are bf16.  Activations and accumulation stay fp32 as for DV_BF16. */
+#define DV_I8 2
 
 #define DV_MAX_TREE 64
 
-/* Model shape.  weight_dtype is also the KV-cache dtype.  Shape limits:
- * head_dim in {64, 128} with n_heads * head_dim == d_model; d_model and
- * vocab multiples of 32; d_ffn a multiple of 16; 1 <= max_tree <= 64;
- * for DV_BF16, d_model and d_ffn multiples of 32. */
+/* Model shape.  weight_dtype is also the KV-cache dtype (bf16 for DV_I8).
+ * Shape limits: head_dim in {64, 128} with n_heads * head_dim == d_model;
+ * d_model and vocab multiples of 32; d_ffn a multiple of 16;
+ * 1 <= max_tree <= 64; for DV_I8, d_model and d_ffn multiples of 64. */
 typedef struct dv_config {
     int32_t n_layers;
     int32_t d_model;
@@ -70,14 +76,16 @@ typedef struct dv_config {
     int32_t vocab;
     float rms_eps;
     float rope_base;
-    int32_t weight_dtype; /* DV_F32 or DV_BF16                               */
+    int32_t weight_dtype; /* DV_F32, DV_BF16 or DV_I8                        */
     int32_t max_ctx;      /* largest len + n_tree any step may reach          */
     int32_t max_tree;     /* largest n_tree (and prefill chunk), <= 64        */
 } dv_config;
 
-/* Device pointers to weights, all of weight_dtype.  The per-layer fields are
- * HOST arrays of n_layers device pointers; they are copied at init, the
- * weights themselves are not copied and must outlive the handle. */
+/* Device pointers to weights, all of weight_dtype (for DV_I8: projection
+ * matrices int8, embed and norm gains bf16, plus the per-row scales).  The
+ * per-layer fields are HOST arrays of n_layers device pointers; they are
+ * copied at init, the weights themselves are not copied and must outlive the
+ * handle.  The *_scale fields are read only for DV_I8 (NULL otherwise). */
 typedef struct dv_weights {
     const void *embed;       /* [vocab][d_model]                 */
     const void *final_norm;  /* [d_model]                        */
@@ -91,6 +99,14 @@ typedef struct dv_weights {
     const void *const *w_gate;    /* [d_ffn][d_model]            */
     const void *const *w_up;      /* [d_ffn][d_model]            */
     const void *const *w_down;    /* [d_model][d_ffn]            */
+    const float *lm_head_scale;   /* [vocab]            (DV_I8)  */
+    const float *const *wq_scale; /* [d_model] per layer (DV_I8) */
+    const float *const *wk_scale; /* [d_model]                   */
+    const float *const *wv_scale; /* [d_model]                   */
+    const float *const *wo_scale; /* [d_model]                   */
+    const float *const *w_gate_scale; /* [d_ffn]                 */
+    const float *const *w_up_scale;   /* [d_ffn]                 */
+    const float *const *w_down_scale; /* [d_model]               */
 } dv_weights;
 
 /* KV cache: device buffers of weight_dtype, per layer and head

@@ -18,5 +18,5 @@ distribution it must reproduce (Monte Carlo) and its greedy limit.
 from .verify import (  # noqa: F401
     OracleModel, TreeInfo, tree_info, round_cache, bf16_to_f64, rmsnorm, rope,
     attention_node, forward_tree, argmax_lowest, greedy_accept, verify_step, commit,
-    prefill, greedy_decode, softmax_t, sample_inverse_cdf, accept_sampled,
+    prefill, greedy_decode, softmax_t, sample_inverse_cdf, accept_sampled, dequantize_rows,
 )

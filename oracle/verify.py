@@ -36,7 +36,9 @@ def bf16_to_f64(bits: np.ndarray) -> np.ndarray:
     return (np.asarray(bits, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
 
 
-def _to_float(raw: np.ndarray, dtype) -> np.ndarray:
+def _to_float(raw, dtype) -> np.ndarray:
+    if isinstance(raw, tuple):          # (int8 codes, row scales)
+        return dequantize_rows(raw[0], raw[1], dtype)
     if raw.dtype == np.uint16:
         return bf16_to_f64(raw).astype(dtype, copy=False)
     return np.asarray(raw).astype(dtype, copy=False)
@@ -75,23 +77,33 @@ def round_cache(x: np.ndarray, kv_dtype: str) -> np.ndarray:
 # model container
 
 
+def dequantize_rows(q: np.ndarray, scale: np.ndarray, dtype=np.float64) -> np.ndarray:
+    """Weight-only int8 (the int8 target of Section 4): W[r][c] = scale[r] *
+    q[r][c], one scale per output row.  Exact in float64."""
+    return np.asarray(q).astype(dtype) * np.asarray(scale).astype(dtype)[:, None]
+
+
 class OracleModel:
-    """Weights as raw arrays (bf16 bits or fp32), matrices ``[out][in]``.
+    """Weights as raw arrays (bf16 bits, fp32, or int8 codes with per-row
+    scales), matrices ``[out][in]``.
 
     ``layer_fn(l)`` returns a dict with wq, wk, wv, wo, w_gate, w_up, w_down,
-    attn_norm, ffn_norm; it is called once per layer per forward pass so large
-    models never hold more than one layer in float64.
+    attn_norm, ffn_norm (and, for int8 matrices, ``<name>_scale``); it is
+    called once per layer per forward pass so large models never hold more
+    than one layer in float64.  ``lm_head_scale`` marks an int8 lm_head.
     """
 
-    def __init__(self, cfg, layer_fn, embed_rows_fn, lm_head, final_norm):
+    def __init__(self, cfg, layer_fn, embed_rows_fn, lm_head, final_norm, lm_head_scale=None):
         self.cfg = cfg
         self.layer_fn = layer_fn
         self.embed_rows_fn = embed_rows_fn
-        self.lm_head = lm_head
+        self.lm_head = lm_head if lm_head_scale is None else (lm_head, lm_head_scale)
         self.final_norm = final_norm
 
     def layer(self, l: int, dtype) -> dict:
-        return {k: _to_float(v, dtype) for k, v in self.layer_fn(l).items()}
+        raw = self.layer_fn(l)
+        return {k: (dequantize_rows(v, raw[k + "_scale"], dtype) if k + "_scale" in raw else _to_float(v, dtype))
+                for k, v in raw.items() if not k.endswith("_scale")}
 
     def embed(self, ids, dtype) -> np.ndarray:
         return _to_float(self.embed_rows_fn(np.asarray(ids)), dtype)

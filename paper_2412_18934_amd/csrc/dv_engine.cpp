@@ -20,7 +20,10 @@ thread_local std::string g_init_error;
 
 struct LayerW {
     const void *attn_norm, *wq, *wk, *wv, *wo, *ffn_norm, *w_gate, *w_up, *w_down;
+    const float *sq = nullptr, *sk = nullptr, *sv = nullptr, *so = nullptr, *sg = nullptr, *su = nullptr,
+                *sd = nullptr;  // int8: row scales as passed in
     uint16_t *pk_qkv = nullptr, *pk_o = nullptr, *pk_gu = nullptr, *pk_down = nullptr;
+    float *ps_qkv = nullptr, *ps_o = nullptr, *ps_gu = nullptr, *ps_down = nullptr;  // int8: packed-order scales
 };
 
 struct GemmPlan {
@@ -41,7 +44,8 @@ struct ProfEv {
 struct dv_handle {
     dv_config cfg{};
     hipStream_t stream = nullptr;
-    int bf16 = 0;
+    int bf16 = 0;          // 16-bit embedding, gains and KV cache; MFMA projections
+    int wkind = W_F32;     // projection weights: W_F32, W_BF16 or W_I8
     size_t esz = 4;
     const void *embed = nullptr, *final_norm = nullptr, *lm_head = nullptr;
     std::vector<LayerW> layers;
@@ -60,6 +64,8 @@ struct dv_handle {
     int32_t *arg_idx = nullptr;
     float *rope_cos = nullptr, *rope_sin = nullptr;
     uint16_t *pk_lm = nullptr;
+    const float *lm_scale = nullptr;
+    float *ps_lm = nullptr;
     StepDesc *h_sd = nullptr;  // the step's tree (kernels get it by value)
     DevAccept *d_acc = nullptr, *h_acc = nullptr;
     float *logits_ws = nullptr;  // [max_tree][vocab] logits of a sampled step without out_logits
@@ -144,9 +150,9 @@ int gemm_units(const GemmPlan &p) { return p.n_groups * p.ks; }
 
 // Grid of a launch: every unit its own workgroup, capped at what the CUs hold
 // at once (the workgroups then loop over the units).
-int gemm_grid(const GemmPlan &p, int epi, int bf16, int mt, int n_cu)
+int gemm_grid(const GemmPlan &p, int epi, int wkind, int mt, int n_cu)
 {
-    const int cap = std::max(1, gemm_blocks_per_cu(epi, bf16, p.mfma, mt, p.rb) * n_cu);
+    const int cap = std::max(1, gemm_blocks_per_cu(epi, wkind, p.mfma, mt, p.rb) * n_cu);
     return std::min(gemm_units(p), cap);
 }
 
@@ -278,10 +284,11 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
     aa.out_split = h->p_o.mfma ? h->attn_s : nullptr;
 
     auto gemm = [&](const GemmPlan &p, int epi, const void *w0, const void *w1, const void *w2,
-                    const uint16_t *packed, int N, int K, const float *x, const uint16_t *xs,
+                    const uint16_t *packed, const float *scale, int N, int K, const float *x, const uint16_t *xs,
                     float *out, const void *gain) -> int {
         GemmArgs a = g;
         a.packed = packed;
+        a.scale = scale;
         a.xs = xs;
         a.w0 = w0;
         a.w1 = w1;
@@ -296,9 +303,9 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
         a.x = x;
         a.out = out;
         a.gain = gain;
-        const int grid = gemm_grid(p, epi, h->bf16, Mpad / 16, h->n_cu);
+        const int grid = gemm_grid(p, epi, h->wkind, Mpad / 16, h->n_cu);
         ProfEv *ev = prof_pair(h, DV_K_GEMM);
-        hipError_t e = launch_gemm(a, grid, epi, h->bf16, p.mfma, s, ev ? ev->a : nullptr, ev ? ev->b : nullptr);
+        hipError_t e = launch_gemm(a, grid, epi, h->wkind, p.mfma, s, ev ? ev->a : nullptr, ev ? ev->b : nullptr);
         if (e != hipSuccess) return hip_fail(h, e, "gemm launch");
         // the next projection normalises with this one's sums of squares
         if (epi == EPI_RESID) g.n_ssq_in = p.n_groups;
@@ -326,7 +333,7 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
         const LayerW &w = h->layers[l];
         g.kc = (char *)kv->k + l * layer_kv;
         g.vc = (char *)kv->v + l * layer_kv;
-        if ((rc = gemm(h->p_qkv, EPI_QKV, w.wq, w.wk, w.wv, w.pk_qkv, d, d, h->u, h->u_s, h->q, nullptr)))
+        if ((rc = gemm(h->p_qkv, EPI_QKV, w.wq, w.wk, w.wv, w.pk_qkv, w.ps_qkv, d, d, h->u, h->u_s, h->q, nullptr)))
             return rc;
         aa.kc = g.kc;
         aa.vc = g.vc;
@@ -336,21 +343,21 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
         if (e == hipSuccess && n_split > 1 && !h->bf16) e = launch_attn_merge(aa, Mpad, s);
         prof_end(h);
         if (e != hipSuccess) return hip_fail(h, e, "attention launch");
-        if ((rc = gemm(h->p_o, EPI_RESID, w.wo, nullptr, nullptr, w.pk_o, d, d, h->attn, h->attn_s, nullptr,
+        if ((rc = gemm(h->p_o, EPI_RESID, w.wo, nullptr, nullptr, w.pk_o, w.ps_o, d, d, h->attn, h->attn_s, nullptr,
                        w.ffn_norm)))
             return rc;
-        if ((rc = gemm(h->p_gu, EPI_SWIGLU, w.w_gate, w.w_up, nullptr, w.pk_gu, F, d, h->u, h->u_s, h->hbuf,
+        if ((rc = gemm(h->p_gu, EPI_SWIGLU, w.w_gate, w.w_up, nullptr, w.pk_gu, w.ps_gu, F, d, h->u, h->u_s, h->hbuf,
                        nullptr)))
             return rc;
         const void *next_gain = l + 1 < c.n_layers ? h->layers[l + 1].attn_norm : h->final_norm;
-        if ((rc = gemm(h->p_down, EPI_RESID, w.w_down, nullptr, nullptr, w.pk_down, d, F, h->hbuf, h->h_s,
+        if ((rc = gemm(h->p_down, EPI_RESID, w.w_down, nullptr, nullptr, w.pk_down, w.ps_down, d, F, h->hbuf, h->h_s,
                        nullptr, next_gain)))
             return rc;
     }
     if (!with_head) return DV_OK;
     g.arg_val = h->arg_val;
     g.arg_idx = h->arg_idx;
-    if ((rc = gemm(h->p_lm, EPI_LOGITS, h->lm_head, nullptr, nullptr, h->pk_lm, c.vocab, d, h->u, h->u_s,
+    if ((rc = gemm(h->p_lm, EPI_LOGITS, h->lm_head, nullptr, nullptr, h->pk_lm, h->ps_lm, c.vocab, d, h->u, h->u_s,
                    out_logits, nullptr)))
         return rc;
     if (smp) {
@@ -471,8 +478,10 @@ int dv_verify_init(const dv_config *cfg, const dv_weights *w, void *stream, dv_h
     if (c.d_model > 8192) return set_err(nullptr, DV_EINVAL, "d_model above 8192");
     if (c.d_model % 32 || c.vocab % 32 || c.d_ffn % 16)
         return set_err(nullptr, DV_EINVAL, "d_model and vocab must be multiples of 32, d_ffn of 16");
-    if (c.weight_dtype != DV_F32 && c.weight_dtype != DV_BF16)
-        return set_err(nullptr, DV_EINVAL, "weight_dtype must be DV_F32 or DV_BF16");
+    if (c.weight_dtype != DV_F32 && c.weight_dtype != DV_BF16 && c.weight_dtype != DV_I8)
+        return set_err(nullptr, DV_EINVAL, "weight_dtype must be DV_F32, DV_BF16 or DV_I8");
+    if (c.weight_dtype == DV_I8 && (c.d_model % 64 || c.d_ffn % 64))
+        return set_err(nullptr, DV_EINVAL, "DV_I8 needs d_model and d_ffn multiples of 64");
     if (c.max_tree < 1 || c.max_tree > DV_MAX_TREE)
         return set_err(nullptr, DV_EINVAL, "max_tree must be in [1, 64]");
     if (c.max_ctx < c.max_tree) return set_err(nullptr, DV_EINVAL, "max_ctx < max_tree");
@@ -485,6 +494,15 @@ int dv_verify_init(const dv_config *cfg, const dv_weights *w, void *stream, dv_h
         if (!w->attn_norm[l] || !w->wq[l] || !w->wk[l] || !w->wv[l] || !w->wo[l] ||
             !w->ffn_norm[l] || !w->w_gate[l] || !w->w_up[l] || !w->w_down[l])
             return set_err(nullptr, DV_EINVAL, "null weight pointer in layer %d", l);
+    if (c.weight_dtype == DV_I8) {
+        if (!w->lm_head_scale || !w->wq_scale || !w->wk_scale || !w->wv_scale || !w->wo_scale ||
+            !w->w_gate_scale || !w->w_up_scale || !w->w_down_scale)
+            return set_err(nullptr, DV_EINVAL, "null row-scale table (DV_I8)");
+        for (int l = 0; l < c.n_layers; ++l)
+            if (!w->wq_scale[l] || !w->wk_scale[l] || !w->wv_scale[l] || !w->wo_scale[l] ||
+                !w->w_gate_scale[l] || !w->w_up_scale[l] || !w->w_down_scale[l])
+                return set_err(nullptr, DV_EINVAL, "null row-scale pointer in layer %d", l);
+    }
 
     // weights may have been written by work still queued on another stream
     if (hipDeviceSynchronize() != hipSuccess)
@@ -492,11 +510,13 @@ int dv_verify_init(const dv_config *cfg, const dv_weights *w, void *stream, dv_h
     dv_handle *h = new dv_handle;
     h->cfg = c;
     h->stream = (hipStream_t)stream;
-    h->bf16 = c.weight_dtype == DV_BF16;
+    h->bf16 = c.weight_dtype == DV_BF16 || c.weight_dtype == DV_I8;
+    h->wkind = c.weight_dtype == DV_I8 ? W_I8 : (c.weight_dtype == DV_BF16 ? W_BF16 : W_F32);
     h->esz = h->bf16 ? 2 : 4;
     h->embed = w->embed;
     h->final_norm = w->final_norm;
     h->lm_head = w->lm_head;
+    if (h->wkind == W_I8) h->lm_scale = w->lm_head_scale;
     h->layers.resize(c.n_layers);
     for (int l = 0; l < c.n_layers; ++l)
     {
@@ -510,6 +530,15 @@ int dv_verify_init(const dv_config *cfg, const dv_weights *w, void *stream, dv_h
         lw.w_gate = w->w_gate[l];
         lw.w_up = w->w_up[l];
         lw.w_down = w->w_down[l];
+        if (h->wkind == W_I8) {
+            lw.sq = w->wq_scale[l];
+            lw.sk = w->wk_scale[l];
+            lw.sv = w->wv_scale[l];
+            lw.so = w->wo_scale[l];
+            lw.sg = w->w_gate_scale[l];
+            lw.su = w->w_up_scale[l];
+            lw.sd = w->w_down_scale[l];
+        }
     }
 
     const int d = c.d_model, F = c.d_ffn, H = c.n_heads, hd = c.head_dim, V = c.vocab;
@@ -598,32 +627,45 @@ int dv_verify_init(const dv_config *cfg, const dv_weights *w, void *stream, dv_h
     // MFMA path: keep the projection matrices in tile order (one extra copy of
     // the projection weights in HBM, written once here)
     if (mf) {
+        // int8: the weights keep one byte each and the row scales follow the
+        // packed row order
         auto pack = [&](const GemmPlan &p, int epi, const void *w0, const void *w1, const void *w2,
-                        int N, int K, uint16_t **dst) -> bool {
+                        const float *s0, const float *s1, const float *s2, int N, int K, uint16_t **dst,
+                        float **sdst) -> bool {
             if (!p.mfma) return true;
             const size_t elems = (size_t)p.n_tiles * DV_GEMM_TILE * K;
-            if (hipMalloc((void **)dst, elems * 2) != hipSuccess) return false;
+            if (hipMalloc((void **)dst, elems * (h->wkind == W_I8 ? 1 : 2)) != hipSuccess) return false;
             GemmArgs a{};
             a.w0 = w0;
             a.w1 = w1;
             a.w2 = w2;
+            a.s0 = s0;
+            a.s1 = s1;
+            a.s2 = s2;
             a.N = N;
             a.K = K;
             a.n_tiles = p.n_tiles;
             a.rb = p.rb;
             a.n_groups = p.n_groups;
             a.hd = hd;
-            return launch_pack(a, epi, *dst, nullptr) == hipSuccess;
+            if (launch_pack(a, epi, h->wkind, *dst, nullptr) != hipSuccess) return false;
+            if (h->wkind != W_I8) return true;
+            if (hipMalloc((void **)sdst, (size_t)p.n_tiles * DV_GEMM_TILE * sizeof(float)) != hipSuccess)
+                return false;
+            return launch_pack_scales(a, epi, *sdst, nullptr) == hipSuccess;
         };
         bool okp = true;
         for (int l = 0; l < c.n_layers && okp; ++l) {
             LayerW &w = h->layers[l];
-            okp = pack(h->p_qkv, EPI_QKV, w.wq, w.wk, w.wv, d, d, &w.pk_qkv) &&
-                  pack(h->p_o, EPI_RESID, w.wo, nullptr, nullptr, d, d, &w.pk_o) &&
-                  pack(h->p_gu, EPI_SWIGLU, w.w_gate, w.w_up, nullptr, F, d, &w.pk_gu) &&
-                  pack(h->p_down, EPI_RESID, w.w_down, nullptr, nullptr, d, F, &w.pk_down);
+            okp = pack(h->p_qkv, EPI_QKV, w.wq, w.wk, w.wv, w.sq, w.sk, w.sv, d, d, &w.pk_qkv, &w.ps_qkv) &&
+                  pack(h->p_o, EPI_RESID, w.wo, nullptr, nullptr, w.so, nullptr, nullptr, d, d, &w.pk_o, &w.ps_o) &&
+                  pack(h->p_gu, EPI_SWIGLU, w.w_gate, w.w_up, nullptr, w.sg, w.su, nullptr, F, d, &w.pk_gu,
+                       &w.ps_gu) &&
+                  pack(h->p_down, EPI_RESID, w.w_down, nullptr, nullptr, w.sd, nullptr, nullptr, d, F, &w.pk_down,
+                       &w.ps_down);
         }
-        okp = okp && pack(h->p_lm, EPI_LOGITS, h->lm_head, nullptr, nullptr, V, d, &h->pk_lm);
+        okp = okp && pack(h->p_lm, EPI_LOGITS, h->lm_head, nullptr, nullptr, h->lm_scale, nullptr, nullptr, V, d,
+                          &h->pk_lm, &h->ps_lm);
         if (!okp) {
             std::string msg = std::string("packed weight allocation failed: ") +
                               hipGetErrorString(hipGetLastError());
@@ -833,9 +875,11 @@ void dv_verify_free(dv_handle *h)
                     (void *)h->rope_sin, (void *)h->d_acc, (void *)h->logits_ws, (void *)h->p_ws})
         if (p) (void)hipFree(p);
     for (auto &w : h->layers)
-        for (void *p : {(void *)w.pk_qkv, (void *)w.pk_o, (void *)w.pk_gu, (void *)w.pk_down})
+        for (void *p : {(void *)w.pk_qkv, (void *)w.pk_o, (void *)w.pk_gu, (void *)w.pk_down, (void *)w.ps_qkv,
+                        (void *)w.ps_o, (void *)w.ps_gu, (void *)w.ps_down})
             if (p) (void)hipFree(p);
     if (h->pk_lm) (void)hipFree(h->pk_lm);
+    if (h->ps_lm) (void)hipFree(h->ps_lm);
     delete h->h_sd;
     if (h->h_acc) (void)hipHostFree(h->h_acc);
     for (auto &e : h->ev_live) { (void)hipEventDestroy(e.a); (void)hipEventDestroy(e.b); }

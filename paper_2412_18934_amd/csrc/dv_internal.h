@@ -62,9 +62,18 @@ enum GemmEpi { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LOGITS = 3 };
 //           segments q | k | v one after another;
 //   SWIGLU: gate rows [16t, 16t+16) | the same up rows;
 //   else:   rows [32t, 32t+16) | [32t+16, 32t+32).
+// int8 weights use the same groups and blocks over pairs of k-steps: the 1 KB
+// block of (k-step pair p, g, b) -- 16 rows x 64 columns, lane l holding row
+// l%16, columns 64 p + 8 (l/16) .. +8 in bytes 0-7 and 64 p + 32 + 8 (l/16)
+// .. +8 in bytes 8-15 -- starts at byte ((p G + g) rb + b) 1024; the row
+// scales follow the packed row order (block gb = g rb + b, row r at gb 16 + r).
+enum WeightKind { W_F32 = 0, W_BF16 = 1, W_I8 = 2 };
+
 struct GemmArgs {
     const void *w0, *w1, *w2;  // QKV: wq, wk, wv; SWIGLU: w_gate, w_up; else w0
     const uint16_t *packed;    // MFMA path: the weights in block order (above)
+    const float *s0, *s1, *s2; // int8: per-row scales of w0, w1, w2 (packing only)
+    const float *scale;        // int8: the row scales in packed row order
     int32_t N;                 // rows of one matrix (d_model, d_ffn or vocab)
     int32_t K;                 // reduction length (row length of the matrices)
     int32_t n_tiles;           // 32-row tiles (QKV counts the three matrices)
@@ -171,13 +180,14 @@ struct CommitArgs {
 
 // launchers (dv_kernels.hip); each returns the launch status
 // copy a projection's bf16 rows into MFMA block order (init time)
-hipError_t launch_pack(const GemmArgs &a, int epi, uint16_t *dst, hipStream_t s);
+hipError_t launch_pack(const GemmArgs &a, int epi, int wkind, void *dst, hipStream_t s);
+hipError_t launch_pack_scales(const GemmArgs &a, int epi, float *dst, hipStream_t s);
 // the MFMA workgroup shape used for row groups of rb blocks
 GemmShape gemm_shape(int rb);
 // workgroups one CU can hold for a GEMM variant (cached)
-int gemm_blocks_per_cu(int epi, int weight_bf16, int use_mfma, int mt, int rb);
+int gemm_blocks_per_cu(int epi, int wkind, int use_mfma, int mt, int rb);
 // ev_start/ev_stop (optional, both or neither): timestamps of this launch
-hipError_t launch_gemm(const GemmArgs &a, int grid, int epi, int weight_bf16, int use_mfma,
+hipError_t launch_gemm(const GemmArgs &a, int grid, int epi, int wkind, int use_mfma,
                        hipStream_t s, hipEvent_t ev_start, hipEvent_t ev_stop);
 hipError_t launch_embed_norm(const NormArgs &a, int Mpad, int weight_bf16, hipStream_t s);
 hipError_t launch_attention(const AttnArgs &a, int kv_bf16, hipStream_t s);

@@ -113,6 +113,7 @@ __device__ __forceinline__ void store_split4(uint16_t *xs, int m, int k, int MT,
 struct RowMap {
     const void *ptr[2];
     int32_t row0[2];
+    int32_t mat[2];  // which of w0, w1, w2 each half reads
 };
 
 __device__ __forceinline__ RowMap row_map(const GemmArgs &a, int epi, int t)
@@ -125,14 +126,18 @@ __device__ __forceinline__ RowMap row_map(const GemmArgs &a, int epi, int t)
         const int h = tt / per_head, j0 = (tt - h * per_head) * 16;
         const void *w = seg == 0 ? a.w0 : (seg == 1 ? a.w1 : a.w2);
         m.ptr[0] = m.ptr[1] = w;
+        m.mat[0] = m.mat[1] = seg;
         m.row0[0] = h * a.hd + j0;
         m.row0[1] = h * a.hd + a.hd / 2 + j0;
     } else if (epi == EPI_SWIGLU) {
         m.ptr[0] = a.w0;
         m.ptr[1] = a.w1;
+        m.mat[0] = 0;
+        m.mat[1] = 1;
         m.row0[0] = m.row0[1] = t * 16;
     } else {
         m.ptr[0] = m.ptr[1] = a.w0;
+        m.mat[0] = m.mat[1] = 0;
         m.row0[0] = t * DV_GEMM_TILE;
         m.row0[1] = t * DV_GEMM_TILE + 16;
     }
@@ -386,13 +391,56 @@ __global__ __launch_bounds__(64) void k_pack_blocks(GemmArgs a, int epi, uint16_
     }
 }
 
-template <int MT, int EPI, typename KV, int NW, int U, int RB>
+// int8 weights: lane l of block (pair p, g, b) takes 8 bytes of k-step 2p and
+// 8 bytes of k-step 2p + 1 of its row, so one 16-byte load feeds two MFMA
+// k-steps.
+__global__ __launch_bounds__(64) void k_pack_blocks_i8(GemmArgs a, int epi, uint8_t *dst)
+{
+    const int gb = blockIdx.x, lane = threadIdx.x;
+    const int rb = a.rb, G = a.n_groups, S2 = a.K / 64;
+    const int g = gb / rb, b = gb - g * rb;
+    const RowMap rm = row_map(a, epi, gb >> 1);
+    const int h = gb & 1;
+    const int8_t *src = reinterpret_cast<const int8_t *>(rm.ptr[h]) + (size_t)(rm.row0[h] + (lane & 15)) * a.K +
+                        (lane >> 4) * 8;
+    for (int p = blockIdx.y; p < S2; p += gridDim.y) {
+        const uint2 lo = *reinterpret_cast<const uint2 *>(src + 64 * p);
+        const uint2 hi = *reinterpret_cast<const uint2 *>(src + 64 * p + 32);
+        *reinterpret_cast<uint4 *>(dst + (((size_t)p * G + g) * rb + b) * 1024 + lane * 16) =
+            make_uint4(lo.x, lo.y, hi.x, hi.y);
+    }
+}
+
+// Row scales in packed row order: block gb, row r -> dst[16 gb + r].
+__global__ __launch_bounds__(16) void k_pack_scales(GemmArgs a, int epi, float *dst)
+{
+    const int gb = blockIdx.x, r = threadIdx.x;
+    const RowMap rm = row_map(a, epi, gb >> 1);
+    const int h = gb & 1;
+    const float *sc = rm.mat[h] == 0 ? a.s0 : (rm.mat[h] == 1 ? a.s1 : a.s2);
+    dst[gb * 16 + r] = sc[rm.row0[h] + r];
+}
+
+// Four int8 values -> four bf16 (exact: |q| <= 128 needs 8 significant bits),
+// two per dword, low byte first.
+__device__ __forceinline__ uint2 i8x4_to_bf16(uint32_t d)
+{
+    const uint32_t f0 = __float_as_uint((float)(int8_t)(d & 0xff));
+    const uint32_t f1 = __float_as_uint((float)(int8_t)((d >> 8) & 0xff));
+    const uint32_t f2 = __float_as_uint((float)(int8_t)((d >> 16) & 0xff));
+    const uint32_t f3 = __float_as_uint((float)(int8_t)(d >> 24));
+    return make_uint2(__builtin_amdgcn_perm(f1, f0, 0x07060302u), __builtin_amdgcn_perm(f3, f2, 0x07060302u));
+}
+
+template <int MT, int EPI, typename KV, int NW, int U, int RB, bool Q8 = false>
 __global__ __launch_bounds__(64 * NW) void k_proj(GemmArgs a)
 {
     constexpr int ROWS = RB * 16, LD = ROWS + 1, NE = RB * MT * 64;
     static_assert(64 * NW >= 4 * 16 * MT, "input_rinv needs 4 threads per token");
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, tid = threadIdx.x;
-    const int S = a.K / 32, G = a.n_groups, KS = a.ks;
+    // a step is one k-step of 32 (bf16 weights) or a pair of them (int8)
+    constexpr int XP = Q8 ? 4 : 2;
+    const int S = a.K / (Q8 ? 64 : 32), G = a.n_groups, KS = a.ks;
     __shared__ f32x4 red[NW][NE / 64][64];
     __shared__ float Y[16 * MT * LD];
     __shared__ float rinv[DV_TREE_MAX];
@@ -425,35 +473,47 @@ __global__ __launch_bounds__(64 * NW) void k_proj(GemmArgs a)
         auto wp = [&](int i, int b) -> const u32x4 * {
             return Wb + (((size_t)(s0 + NW * i) * G + g) * RB + b) * 64 + lane;
         };
-        auto xp = [&](int i, int mt, int q) -> const u32x4 * {
-            return Xb + (((size_t)(s0 + NW * i) * MT + mt) * 2 + q) * 64 + lane;
+        // activation block of step i, half hf (int8: k-step 2 step + hf), part q
+        auto xp = [&](int i, int hf, int mt, int q) -> const u32x4 * {
+            const size_t k32 = Q8 ? 2 * (size_t)(s0 + NW * i) + hf : (size_t)(s0 + NW * i);
+            return Xb + ((k32 * MT + mt) * 2 + q) * 64 + lane;
         };
         f32x4 acc[RB][MT];
 #pragma unroll
         for (int b = 0; b < RB; ++b)
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) acc[b][mt] = (f32x4){0.f, 0.f, 0.f, 0.f};
+        f32x4 rs[Q8 ? RB : 1];  // int8: this lane's four row scales per block
         if (n > 0) {
-            u32x4 wb[U][RB], xb[U][MT][2];
+            u32x4 wb[U][RB], xb[U][MT][XP];
             auto fetch = [&](int j, int i) {
 #pragma unroll
                 for (int b = 0; b < RB; ++b) wb[j][b] = load_weights(wp(i, b));
 #pragma unroll
-                for (int mt = 0; mt < MT; ++mt) {
-                    xb[j][mt][0] = *xp(i, mt, 0);
-                    xb[j][mt][1] = *xp(i, mt, 1);
-                }
+                for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                    for (int q = 0; q < XP; ++q) xb[j][mt][q] = *xp(i, q >> 1, mt, q & 1);
             };
             auto mfma = [&](int j) {
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt) {
-                    const bf16x8 hi = __builtin_bit_cast(bf16x8, xb[j][mt][0]);
-                    const bf16x8 lo = __builtin_bit_cast(bf16x8, xb[j][mt][1]);
 #pragma unroll
-                    for (int b = 0; b < RB; ++b) {
-                        const bf16x8 w = __builtin_bit_cast(bf16x8, wb[j][b]);
-                        acc[b][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, hi, acc[b][mt], 0, 0, 0);
-                        acc[b][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, lo, acc[b][mt], 0, 0, 0);
+                    for (int hf = 0; hf < XP / 2; ++hf) {
+                        const bf16x8 hi = __builtin_bit_cast(bf16x8, xb[j][mt][2 * hf]);
+                        const bf16x8 lo = __builtin_bit_cast(bf16x8, xb[j][mt][2 * hf + 1]);
+#pragma unroll
+                        for (int b = 0; b < RB; ++b) {
+                            bf16x8 w;
+                            if (Q8) {
+                                const uint2 c0 = i8x4_to_bf16(wb[j][b][2 * hf]);
+                                const uint2 c1 = i8x4_to_bf16(wb[j][b][2 * hf + 1]);
+                                w = __builtin_bit_cast(bf16x8, (u32x4){c0.x, c0.y, c1.x, c1.y});
+                            } else {
+                                w = __builtin_bit_cast(bf16x8, wb[j][b]);
+                            }
+                            acc[b][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, hi, acc[b][mt], 0, 0, 0);
+                            acc[b][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, lo, acc[b][mt], 0, 0, 0);
+                        }
                     }
                 }
             };
@@ -461,6 +521,11 @@ __global__ __launch_bounds__(64 * NW) void k_proj(GemmArgs a)
             // last step and are dropped)
 #pragma unroll
             for (int j = 0; j < U; ++j) fetch(j, min(j, n - 1));
+            if (Q8) {
+#pragma unroll
+                for (int b = 0; b < RB; ++b)
+                    rs[b] = *reinterpret_cast<const f32x4 *>(a.scale + (g * RB + b) * 16 + 4 * (lane >> 4));
+            }
             stage(g);
             if (EPI != EPI_RESID && !have_rinv) {
                 // the first unit's loads are in flight; the norm scalars of
@@ -479,6 +544,13 @@ __global__ __launch_bounds__(64 * NW) void k_proj(GemmArgs a)
 #pragma unroll
             for (int j = 0; j < U; ++j)
                 if (i + j < n) mfma(j);
+            if (Q8) {
+                // W = scale[row] q: scale this wave's sums row by row
+#pragma unroll
+                for (int b = 0; b < RB; ++b)
+#pragma unroll
+                    for (int mt = 0; mt < MT; ++mt) acc[b][mt] *= rs[b];
+            }
         } else {
             stage(g);
             if (EPI != EPI_RESID && !have_rinv) {
@@ -1503,55 +1575,58 @@ __global__ __launch_bounds__(256) void k_kv_commit(CommitArgs a)
 GemmShape gemm_shape(int rb) { return rb == 4 ? GemmShape{4, 2} : GemmShape{4, 4}; }
 
 // more token tiles hold more accumulators and operands: fewer steps in flight
-template <int EPI, typename KV, int RB>
+template <int EPI, typename KV, int RB, bool Q8>
 static const void *proj_kernel_mt(int mt)
 {
     constexpr int U1 = RB == 4 ? 2 : 4;
     switch (mt) {
-    case 1: return (const void *)k_proj<1, EPI, KV, 4, U1, RB>;
-    case 2: return (const void *)k_proj<2, EPI, KV, 4, 2, RB>;
-    case 3: return (const void *)k_proj<3, EPI, KV, 4, 1, RB>;
-    case 4: return (const void *)k_proj<4, EPI, KV, 4, 1, RB>;
+    case 1: return (const void *)k_proj<1, EPI, KV, 4, U1, RB, Q8>;
+    case 2: return (const void *)k_proj<2, EPI, KV, 4, 2, RB, Q8>;
+    case 3: return (const void *)k_proj<3, EPI, KV, 4, 1, RB, Q8>;
+    case 4: return (const void *)k_proj<4, EPI, KV, 4, 1, RB, Q8>;
     default: return nullptr;
     }
 }
 
 template <int EPI>
-static const void *gemm_kernel(int weight_bf16, int use_mfma, int mt, int rb)
+static const void *gemm_kernel(int wkind, int use_mfma, int mt, int rb)
 {
-    if (weight_bf16 && use_mfma) {
-        if (rb == 4) return proj_kernel_mt<EPI, uint16_t, 4>(mt);
-        if (rb == 2) return proj_kernel_mt<EPI, uint16_t, 2>(mt);
+    if (wkind != W_F32 && use_mfma) {
+        const bool q8 = wkind == W_I8;
+        if (rb == 4) return q8 ? proj_kernel_mt<EPI, uint16_t, 4, true>(mt) : proj_kernel_mt<EPI, uint16_t, 4, false>(mt);
+        if (rb == 2) return q8 ? proj_kernel_mt<EPI, uint16_t, 2, true>(mt) : proj_kernel_mt<EPI, uint16_t, 2, false>(mt);
         return nullptr;
     }
-    if (weight_bf16) return (const void *)k_gemm_valu<uint16_t, EPI, uint16_t>;
-    return (const void *)k_gemm_valu<float, EPI, float>;
+    if (wkind == W_BF16) return (const void *)k_gemm_valu<uint16_t, EPI, uint16_t>;
+    if (wkind == W_F32) return (const void *)k_gemm_valu<float, EPI, float>;
+    return nullptr;  // int8 weights have no VALU kernel
 }
 
-static const void *gemm_kernel_any(int epi, int weight_bf16, int use_mfma, int mt, int rb)
+static const void *gemm_kernel_any(int epi, int wkind, int use_mfma, int mt, int rb)
 {
     switch (epi) {
-    case EPI_QKV: return gemm_kernel<EPI_QKV>(weight_bf16, use_mfma, mt, rb);
-    case EPI_RESID: return gemm_kernel<EPI_RESID>(weight_bf16, use_mfma, mt, rb);
-    case EPI_SWIGLU: return gemm_kernel<EPI_SWIGLU>(weight_bf16, use_mfma, mt, rb);
-    case EPI_LOGITS: return gemm_kernel<EPI_LOGITS>(weight_bf16, use_mfma, mt, rb);
+    case EPI_QKV: return gemm_kernel<EPI_QKV>(wkind, use_mfma, mt, rb);
+    case EPI_RESID: return gemm_kernel<EPI_RESID>(wkind, use_mfma, mt, rb);
+    case EPI_SWIGLU: return gemm_kernel<EPI_SWIGLU>(wkind, use_mfma, mt, rb);
+    case EPI_LOGITS: return gemm_kernel<EPI_LOGITS>(wkind, use_mfma, mt, rb);
     }
     return nullptr;
 }
 
-static int gemm_threads(int weight_bf16, int use_mfma, int rb)
+static int gemm_threads(int wkind, int use_mfma, int rb)
 {
-    return (weight_bf16 && use_mfma) ? 64 * gemm_shape(rb).nw : 256;
+    return (wkind != W_F32 && use_mfma) ? 64 * gemm_shape(rb).nw : 256;
 }
 
-int gemm_blocks_per_cu(int epi, int weight_bf16, int use_mfma, int mt, int rb)
+int gemm_blocks_per_cu(int epi, int wkind, int use_mfma, int mt, int rb)
 {
-    static int cache[4][2][2][5][2];
-    int &c = cache[epi & 3][weight_bf16 ? 1 : 0][use_mfma ? 1 : 0][(mt >= 1 && mt <= 4) ? mt : 0][rb == 4];
+    static int cache[4][3][2][5][2];
+    if (wkind < 0 || wkind > 2) return 1;
+    int &c = cache[epi & 3][wkind][use_mfma ? 1 : 0][(mt >= 1 && mt <= 4) ? mt : 0][rb == 4];
     if (c == 0) {
-        const void *k = gemm_kernel_any(epi, weight_bf16, use_mfma, mt, rb);
+        const void *k = gemm_kernel_any(epi, wkind, use_mfma, mt, rb);
         int n = 0;
-        if (!k || hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k, gemm_threads(weight_bf16, use_mfma, rb), 0) !=
+        if (!k || hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k, gemm_threads(wkind, use_mfma, rb), 0) !=
                       hipSuccess || n < 1)
             n = 1;
         c = n;
@@ -1559,23 +1634,40 @@ int gemm_blocks_per_cu(int epi, int weight_bf16, int use_mfma, int mt, int rb)
     return c;
 }
 
-hipError_t launch_gemm(const GemmArgs &a, int grid, int epi, int weight_bf16, int use_mfma, hipStream_t s,
+hipError_t launch_gemm(const GemmArgs &a, int grid, int epi, int wkind, int use_mfma, hipStream_t s,
                        hipEvent_t ev_start, hipEvent_t ev_stop)
 {
-    const void *k = gemm_kernel_any(epi, weight_bf16, use_mfma, a.Mpad / 16, a.rb);
+    const void *k = gemm_kernel_any(epi, wkind, use_mfma, a.Mpad / 16, a.rb);
     if (!k || grid < 1) return hipErrorInvalidValue;
+    if (wkind == W_I8 && (!a.scale || a.K % 64)) return hipErrorInvalidValue;
     GemmArgs arg = a;
     void *params[] = {&arg};
-    const dim3 block(gemm_threads(weight_bf16, use_mfma, a.rb));
+    const dim3 block(gemm_threads(wkind, use_mfma, a.rb));
     // with events: timestamps taken by the dispatch itself (no extra packets)
     if (ev_start && ev_stop) return hipExtLaunchKernel(k, dim3(grid), block, params, 0, s, ev_start, ev_stop, 0);
     return hipLaunchKernel(k, dim3(grid), block, params, 0, s);
 }
 
-hipError_t launch_pack(const GemmArgs &a, int epi, uint16_t *dst, hipStream_t s)
+hipError_t launch_pack(const GemmArgs &a, int epi, int wkind, void *dst, hipStream_t s)
 {
     if (a.rb != 2 && a.rb != 4) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_pack_blocks, dim3(a.n_groups * a.rb, std::min(a.K / 32, 64)), dim3(64), 0, s, a, epi, dst);
+    if (wkind == W_I8) {
+        if (a.K % 64) return hipErrorInvalidValue;
+        hipLaunchKernelGGL(k_pack_blocks_i8, dim3(a.n_groups * a.rb, std::min(a.K / 64, 64)), dim3(64), 0, s, a, epi,
+                           static_cast<uint8_t *>(dst));
+    } else if (wkind == W_BF16) {
+        hipLaunchKernelGGL(k_pack_blocks, dim3(a.n_groups * a.rb, std::min(a.K / 32, 64)), dim3(64), 0, s, a, epi,
+                           static_cast<uint16_t *>(dst));
+    } else {
+        return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_pack_scales(const GemmArgs &a, int epi, float *dst, hipStream_t s)
+{
+    if (a.rb != 2 && a.rb != 4) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_pack_scales, dim3(a.n_groups * a.rb), dim3(16), 0, s, a, epi, dst);
     return hipGetLastError();
 }
 

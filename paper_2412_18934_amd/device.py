@@ -14,50 +14,63 @@ import torch
 from . import dv
 
 LAYER_KEYS = ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up", "w_down")
+MATRIX_KEYS = ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down")
 
 
 def to_device(a: np.ndarray, device) -> torch.Tensor:
-    """Copy a host array (uint16 bf16 bits or float32) to a device tensor."""
+    """Copy a host array (uint16 bf16 bits, float32 or int8) to a device tensor."""
     a = np.ascontiguousarray(a)
     if a.dtype == np.uint16:
         return torch.from_numpy(a.view(np.int16)).to(device).view(torch.bfloat16)
-    if a.dtype == np.float32:
+    if a.dtype in (np.float32, np.int8):
         return torch.from_numpy(a).to(device)
     raise TypeError("unsupported host dtype %s" % a.dtype)
 
 
 def make_config(n_layers, d_model, n_heads, head_dim, d_ffn, vocab, rms_eps, rope_base,
                 weight_dtype, max_ctx, max_tree) -> dv.dv_config:
+    wd = {"bf16": dv.DV_BF16, "f32": dv.DV_F32, "i8": dv.DV_I8}[weight_dtype]
     return dv.dv_config(n_layers, d_model, n_heads, head_dim, d_ffn, vocab, rms_eps, rope_base,
-                        dv.DV_BF16 if weight_dtype == "bf16" else dv.DV_F32, max_ctx, max_tree)
+                        wd, max_ctx, max_tree)
 
 
 class DeviceWeights:
     """Uploads weights and builds the dv_weights pointer tables.
 
-    layer_fn(l) -> dict with the LAYER_KEYS arrays of layer l."""
+    layer_fn(l) -> dict with the LAYER_KEYS arrays of layer l (int8 weights:
+    also ``<matrix>_scale``, float32 per row; lm_head_scale for the head)."""
 
-    def __init__(self, n_layers, layer_fn, embed, lm_head, final_norm, device="cuda:0"):
+    def __init__(self, n_layers, layer_fn, embed, lm_head, final_norm, device="cuda:0", lm_head_scale=None):
         self.device = torch.device(device)
         self.embed = to_device(embed, self.device)
         self.lm_head = to_device(lm_head, self.device)
         self.final_norm = to_device(final_norm, self.device)
+        self.lm_head_scale = None if lm_head_scale is None else to_device(lm_head_scale, self.device)
         self.layers = []
         for l in range(n_layers):
             src = layer_fn(l)
-            self.layers.append({k: to_device(src[k], self.device) for k in LAYER_KEYS})
+            keys = LAYER_KEYS + tuple(k + "_scale" for k in MATRIX_KEYS if k + "_scale" in src)
+            self.layers.append({k: to_device(src[k], self.device) for k in keys})
             del src
+        self.quantized = "wq_scale" in self.layers[0] if self.layers else False
         self._tables = {}
-        for k in LAYER_KEYS:
+        keys = LAYER_KEYS + (tuple(k + "_scale" for k in MATRIX_KEYS) if self.quantized else ())
+        for k in keys:
             arr = (ctypes.c_void_p * n_layers)(*[t[k].data_ptr() for t in self.layers])
             self._tables[k] = arr
         pp = ctypes.POINTER(ctypes.c_void_p)
+        scale_tables = [ctypes.cast(self._tables[k + "_scale"], pp) if self.quantized else None
+                        for k in MATRIX_KEYS]
         self.c = dv.dv_weights(
             self.embed.data_ptr(), self.final_norm.data_ptr(), self.lm_head.data_ptr(),
-            *[ctypes.cast(self._tables[k], pp) for k in LAYER_KEYS])
+            *[ctypes.cast(self._tables[k], pp) for k in LAYER_KEYS],
+            self.lm_head_scale.data_ptr() if self.lm_head_scale is not None else None,
+            *scale_tables)
 
     def nbytes(self) -> int:
         n = self.embed.nbytes + self.lm_head.nbytes + self.final_norm.nbytes
+        if self.lm_head_scale is not None:
+            n += self.lm_head_scale.nbytes
         return n + sum(t.nbytes for lay in self.layers for t in lay.values())
 
 
@@ -67,7 +80,7 @@ class DeviceKV:
 
     def __init__(self, n_layers, n_heads, head_dim, capacity, weight_dtype, device="cuda:0",
                  fill=None):
-        dt = torch.bfloat16 if weight_dtype == "bf16" else torch.float32
+        dt = torch.float32 if weight_dtype == "f32" else torch.bfloat16  # int8 models keep a bf16 cache
         kshape = (n_layers, n_heads, capacity, head_dim)
         vshape = (n_layers, n_heads, head_dim, capacity)
         if fill is None:

@@ -15,7 +15,7 @@ import numpy as np
 _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdv.so")
 
 DV_OK, DV_EINVAL, DV_ECAPACITY, DV_ESTATE, DV_EHIP, DV_ENOMEM = 0, -1, -2, -3, -4, -5
-DV_F32, DV_BF16 = 0, 1
+DV_F32, DV_BF16, DV_I8 = 0, 1, 2
 DV_MAX_TREE = 64
 DV_K_GEMM, DV_K_ATTN, DV_K_NORM, DV_K_OTHER = 0, 1, 2, 3
 
@@ -47,7 +47,9 @@ class dv_weights(ctypes.Structure):
     _fields_ = [("embed", ctypes.c_void_p), ("final_norm", ctypes.c_void_p),
                 ("lm_head", ctypes.c_void_p), ("attn_norm", _PP), ("wq", _PP), ("wk", _PP),
                 ("wv", _PP), ("wo", _PP), ("ffn_norm", _PP), ("w_gate", _PP), ("w_up", _PP),
-                ("w_down", _PP)]
+                ("w_down", _PP), ("lm_head_scale", ctypes.c_void_p), ("wq_scale", _PP),
+                ("wk_scale", _PP), ("wv_scale", _PP), ("wo_scale", _PP), ("w_gate_scale", _PP),
+                ("w_up_scale", _PP), ("w_down_scale", _PP)]
 
 
 class dv_kv(ctypes.Structure):

@@ -48,6 +48,7 @@ def _L():
         lib.dvs_key.restype = u64
         lib.dvs_normal_bf16.argtypes = [u64, u64, u64, u64, ctypes.c_double, p]
         lib.dvs_normal_f32.argtypes = [u64, u64, u64, u64, ctypes.c_double, p]
+        lib.dvs_normal_i8.argtypes = [u64, u64, u64, u64, ctypes.c_double, p]
         lib.dvs_u64.argtypes = [u64, u64, u64, u64, p]
         lib.dvs_uniform_int.argtypes = [u64, u64, u64, u64, ctypes.c_uint32, p]
         _lib = lib
@@ -58,8 +59,12 @@ def _L():
 # raw streams
 
 def normal(seed: int, tensor: int, n: int, sigma: float, dtype: str, start: int = 0) -> np.ndarray:
-    """``n`` draws of N(0, sigma^2) stored as ``dtype`` ('bf16' -> uint16 bits, 'f32')."""
-    if dtype == "bf16":
+    """``n`` draws of N(0, sigma^2) stored as ``dtype`` ('bf16' -> uint16 bits, 'f32',
+    'i8' -> int8 codes rint(sigma z) clipped to [-127, 127])."""
+    if dtype == "i8":
+        out = np.empty(n, dtype=np.int8)
+        _L().dvs_normal_i8(seed, tensor, start, n, sigma, out.ctypes.data)
+    elif dtype == "bf16":
         out = np.empty(n, dtype=np.uint16)
         _L().dvs_normal_bf16(seed, tensor, start, n, sigma, out.ctypes.data)
     elif dtype == "f32":
@@ -111,12 +116,17 @@ class ModelCfg:
     vocab: int
     rms_eps: float = 1e-6
     rope_base: float = 10000.0
-    weight_dtype: str = "bf16"   # 'bf16' or 'f32'; the KV cache uses the same dtype
+    weight_dtype: str = "bf16"   # 'bf16', 'f32' or 'i8'; the KV cache uses the same dtype (bf16 for 'i8')
     init_std: float = 0.02
 
     @property
     def kv_dtype(self) -> str:
-        return self.weight_dtype
+        return "bf16" if self.weight_dtype == "i8" else self.weight_dtype
+
+    @property
+    def dense_dtype(self) -> str:
+        """dtype of the embedding and the norm gains"""
+        return "bf16" if self.weight_dtype == "i8" else self.weight_dtype
 
     def layer_params(self) -> int:
         d, f = self.d_model, self.d_ffn
@@ -147,6 +157,7 @@ LLAMA7B = ModelCfg(n_layers=32, d_model=4096, n_heads=32, head_dim=128, d_ffn=11
                    vocab=32000)
 LLAMA13B = ModelCfg(n_layers=40, d_model=5120, n_heads=40, head_dim=128, d_ffn=13824,
                     vocab=32000)
+LLAMA13B_I8 = replace(LLAMA13B, weight_dtype="i8")
 
 WORKLOADS = {
     "tiny-f32-chain4": Workload("tiny-f32-chain4", TINY, context=64, n_tree=4, depth=4,
@@ -158,6 +169,10 @@ WORKLOADS = {
                                           weight_seed=301),
     "llama13b-bf16-ctx8192": Workload("llama13b-bf16-ctx8192", LLAMA13B, context=8192,
                                       n_tree=16, depth=6, seed_base=500, weight_seed=301),
+    # weight-only int8 variant of the 13B workload (same context, tree and seeds)
+    "llama13b-i8-m16-ctx1024": Workload("llama13b-i8-m16-ctx1024", LLAMA13B_I8,
+                                        context=1024, n_tree=16, depth=6, seed_base=300,
+                                        weight_seed=301),
 }
 SWEEP_M = (1, 2, 4, 8, 16, 32, 64)
 
@@ -176,6 +191,7 @@ def shrink(model: ModelCfg, **kw) -> ModelCfg:
 
 T_EMBED, T_LMHEAD, T_PROMPT, T_TREE_PARENT, T_TREE_TOKEN = 1, 2, 3, 4, 5
 T_UNIFORM, T_DRAFT = 6, 7
+T_SCALE_OFFSET = 1 << 40   # row scales of the matrix with tensor id t use id t + T_SCALE_OFFSET
 LAYER_NAMES = ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down")
 
 
@@ -193,36 +209,65 @@ def _ones(n: int, dtype: str) -> np.ndarray:
     return np.ones(n, dtype=np.float32)
 
 
+I8_CODE_SIGMA = 127.0 / 4.0   # int8 codes: the clip sits at 4 standard deviations
+
+
+def row_scales(cfg: ModelCfg, seed: int, tensor: int, rows: int) -> np.ndarray:
+    """Per-row scales of an int8 matrix: init_std / I8_CODE_SIGMA, varied by
+    up to +-25% per row (uniform), float32."""
+    u = uniform01(seed, tensor, rows).astype(np.float64)
+    return (cfg.init_std / I8_CODE_SIGMA * (0.75 + 0.5 * u)).astype(np.float32)
+
+
+def _matrix(cfg: ModelCfg, seed: int, tensor: int, rows: int, cols: int, out: dict, key: str):
+    if cfg.weight_dtype == "i8":
+        out[key] = normal(seed, tensor, rows * cols, I8_CODE_SIGMA, "i8").reshape(rows, cols)
+        out[key + "_scale"] = row_scales(cfg, seed, tensor + T_SCALE_OFFSET, rows)
+    else:
+        out[key] = normal(seed, tensor, rows * cols, cfg.init_std, cfg.weight_dtype).reshape(rows, cols)
+
+
 def layer_weights(cfg: ModelCfg, seed: int, l: int) -> dict:
-    """Weights of layer ``l``: matrices ``[out][in]``, norm gains = 1."""
-    d, f, dt, s = cfg.d_model, cfg.d_ffn, cfg.weight_dtype, cfg.init_std
+    """Weights of layer ``l``: matrices ``[out][in]``, norm gains = 1.  For
+    'i8' each matrix comes with ``<name>_scale`` (float32 per row)."""
+    d, f = cfg.d_model, cfg.d_ffn
     shapes = dict(wq=(d, d), wk=(d, d), wv=(d, d), wo=(d, d),
                   w_gate=(f, d), w_up=(f, d), w_down=(d, f))
-    out = {k: normal(seed, _t_layer(l, k), a * b, s, dt).reshape(a, b)
-           for k, (a, b) in shapes.items()}
-    out["attn_norm"] = _ones(d, dt)
-    out["ffn_norm"] = _ones(d, dt)
+    out = {}
+    for k, (a, b) in shapes.items():
+        _matrix(cfg, seed, _t_layer(l, k), a, b, out, k)
+    out["attn_norm"] = _ones(d, cfg.dense_dtype)
+    out["ffn_norm"] = _ones(d, cfg.dense_dtype)
     return out
 
 
 def embed(cfg: ModelCfg, seed: int) -> np.ndarray:
     return normal(seed, T_EMBED, cfg.vocab * cfg.d_model, cfg.init_std,
-                  cfg.weight_dtype).reshape(cfg.vocab, cfg.d_model)
+                  cfg.dense_dtype).reshape(cfg.vocab, cfg.d_model)
 
 
 def embed_rows(cfg: ModelCfg, seed: int, ids) -> np.ndarray:
-    rows = [normal(seed, T_EMBED, cfg.d_model, cfg.init_std, cfg.weight_dtype,
+    rows = [normal(seed, T_EMBED, cfg.d_model, cfg.init_std, cfg.dense_dtype,
                    start=int(t) * cfg.d_model) for t in ids]
     return np.stack(rows)
 
 
 def lm_head(cfg: ModelCfg, seed: int) -> np.ndarray:
-    return normal(seed, T_LMHEAD, cfg.vocab * cfg.d_model, cfg.init_std,
-                  cfg.weight_dtype).reshape(cfg.vocab, cfg.d_model)
+    """The lm_head matrix (for 'i8' the int8 codes; see lm_head_scale)."""
+    out = {}
+    _matrix(cfg, seed, T_LMHEAD, cfg.vocab, cfg.d_model, out, "w")
+    return out["w"]
+
+
+def lm_head_scale(cfg: ModelCfg, seed: int):
+    """Row scales of an 'i8' lm_head (None otherwise)."""
+    if cfg.weight_dtype != "i8":
+        return None
+    return row_scales(cfg, seed, T_LMHEAD + T_SCALE_OFFSET, cfg.vocab)
 
 
 def final_norm(cfg: ModelCfg) -> np.ndarray:
-    return _ones(cfg.d_model, cfg.weight_dtype)
+    return _ones(cfg.d_model, cfg.dense_dtype)
 
 
 def kv_sigma(cfg: ModelCfg) -> float:

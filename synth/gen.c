@@ -90,6 +90,19 @@ void dvs_normal_f32(uint64_t seed, uint64_t tensor, uint64_t start, uint64_t n,
     NORMAL_LOOP(out[i - start] = v)
 }
 
+/* out[e] = int8(clamp(rint(sigma * N_{start+e}), -127, 127)), e < n: integer
+ * codes with a Gaussian profile (sigma = 127/4 puts the clip at 4 standard
+ * deviations). */
+void dvs_normal_i8(uint64_t seed, uint64_t tensor, uint64_t start, uint64_t n,
+                   double sigma, int8_t *out)
+{
+    NORMAL_LOOP({
+        float r = rintf(v);
+        r = r > 127.f ? 127.f : (r < -127.f ? -127.f : r);
+        out[i - start] = (int8_t)r;
+    })
+}
+
 /* Raw 64-bit draws (for small host-side choices such as tree shapes). */
 void dvs_u64(uint64_t seed, uint64_t tensor, uint64_t start, uint64_t n, uint64_t *out)
 {

@@ -21,11 +21,12 @@ class Weights:
         self.layers = [synth.layer_weights(cfg, seed, l) for l in range(cfg.n_layers)]
         self.embed = synth.embed(cfg, seed)
         self.lm_head = synth.lm_head(cfg, seed)
+        self.lm_head_scale = synth.lm_head_scale(cfg, seed)
         self.final_norm = synth.final_norm(cfg)
 
     def oracle(self):
         return OracleModel(self.cfg, lambda l: self.layers[l], lambda ids: self.embed[ids],
-                           self.lm_head, self.final_norm)
+                           self.lm_head, self.final_norm, lm_head_scale=self.lm_head_scale)
 
 
 def all_parent_arrays(m):
@@ -49,7 +50,7 @@ class GpuCase:
         self.w = weights or Weights(cfg, seed)
         self.capacity = capacity
         self.dev = D.DeviceWeights(cfg.n_layers, lambda l: self.w.layers[l], self.w.embed,
-                                   self.w.lm_head, self.w.final_norm)
+                                   self.w.lm_head, self.w.final_norm, lm_head_scale=self.w.lm_head_scale)
         self.ccfg = D.make_config(cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.head_dim, cfg.d_ffn,
                                   cfg.vocab, cfg.rms_eps, cfg.rope_base, cfg.weight_dtype,
                                   max_ctx or capacity, max_tree)

@@ -95,6 +95,35 @@ def test_init_rejects_null_weight_pointer():
     assert e.value.code == dv.DV_EINVAL and "layer 1" in str(e.value)
 
 
+def _header_fields(name):
+    src = open(os.path.join(ROOT, "include", "dv.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    body = re.search(r"typedef struct %s \{(.*?)\} %s;" % (name, name), src, flags=re.S).group(1)
+    return re.findall(r"(\w+)\s*(?:\[[^\]]*\])?\s*;", body)
+
+
+@pytest.mark.parametrize("name", ["dv_config", "dv_weights", "dv_kv", "dv_accept"])
+def test_binding_structs_follow_the_header(name):
+    assert [f[0] for f in getattr(dv, name)._fields_] == _header_fields(name)
+
+
+def test_int8_config_needs_64_multiples_and_scales():
+    w, tab = _fake_weights()
+    with pytest.raises(dv.DvError) as e:   # d_ffn 688 is not a multiple of 64
+        dv.dv_verify_init(_good_cfg(weight_dtype=dv.DV_I8), w)
+    assert e.value.code == dv.DV_EINVAL and "64" in str(e.value)
+    with pytest.raises(dv.DvError) as e:   # no scale tables
+        dv.dv_verify_init(_good_cfg(weight_dtype=dv.DV_I8, d_ffn=704), w)
+    assert e.value.code == dv.DV_EINVAL and "scale" in str(e.value)
+    pp = ctypes.cast(tab, ctypes.POINTER(ctypes.c_void_p))
+    w.lm_head_scale = 0x1000
+    for f in ("wq_scale", "wk_scale", "wv_scale", "wo_scale", "w_gate_scale", "w_up_scale"):
+        setattr(w, f, pp)
+    with pytest.raises(dv.DvError) as e:   # w_down_scale still missing
+        dv.dv_verify_init(_good_cfg(weight_dtype=dv.DV_I8, d_ffn=704), w)
+    assert e.value.code == dv.DV_EINVAL and "scale" in str(e.value)
+
+
 def test_calls_on_null_handle_fail_cleanly():
     L = dv.lib()
     kv = dv.dv_kv(0, 0, 0, 0)
@@ -106,4 +135,9 @@ def test_calls_on_null_handle_fail_cleanly():
     assert L.dv_kv_commit(None, ctypes.byref(kv), ctypes.byref(acc)) == dv.DV_EINVAL
     assert L.dv_prefill(None, dv._ptr(t), 1, ctypes.byref(kv), None) == dv.DV_EINVAL
     assert L.dv_profile_enable(None, 1) == dv.DV_EINVAL
+    u = np.zeros(1, np.float32)
+    assert L.dv_verify_step_sampled(None, dv._ptr(t), dv._ptr(p), 1, ctypes.byref(kv), None, 1.0,
+                                    dv._fptr(u), dv._fptr(u), None, ctypes.byref(acc)) == dv.DV_EINVAL
+    assert L.dv_accept_sampled(None, None, dv._ptr(t), dv._ptr(p), 1, None, 1.0, dv._fptr(u), dv._fptr(u),
+                               ctypes.byref(acc)) == dv.DV_EINVAL
     L.dv_verify_free(None)

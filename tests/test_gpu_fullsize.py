@@ -30,7 +30,8 @@ def _say(msg):
 
 
 class _Model:
-    """One set of full-size weights on the GPU and on the host (bf16 bits)."""
+    """One set of full-size weights on the GPU and on the host (bf16 bits, or
+    int8 codes with row scales)."""
 
     def __init__(self, mc, seed):
         t0 = time.time()
@@ -38,10 +39,12 @@ class _Model:
         self.layers = [synth.layer_weights(mc, seed, l) for l in range(mc.n_layers)]
         self.embed = synth.embed(mc, seed)
         self.lm = synth.lm_head(mc, seed)
+        self.lm_s = synth.lm_head_scale(mc, seed)
         self.fn = synth.final_norm(mc)
-        self.dev = D.DeviceWeights(mc.n_layers, lambda l: self.layers[l], self.embed, self.lm, self.fn)
+        self.dev = D.DeviceWeights(mc.n_layers, lambda l: self.layers[l], self.embed, self.lm, self.fn,
+                                   lm_head_scale=self.lm_s)
         self.om = ov.OracleModel(mc, lambda l: self.layers[l], lambda ids: self.embed[ids],
-                                 self.lm, self.fn)
+                                 self.lm, self.fn, lm_head_scale=self.lm_s)
         _say("weights ready in %.0f s" % (time.time() - t0))
 
     def run(self, wl, m=None):
@@ -100,6 +103,15 @@ def test_llama13b_sweep_extremes(llama13b, m):
 
 def test_llama13b_ctx8192(llama13b):
     llama13b.run(synth.WORKLOADS["llama13b-bf16-ctx8192"])
+
+
+def test_llama13b_int8_m16_ctx1024():
+    """The weight-only int8 13B workload bench.py times beside the headline."""
+    wl = synth.WORKLOADS["llama13b-i8-m16-ctx1024"]
+    model = _Model(wl.model, wl.seeds["weights"])
+    model.run(wl)
+    del model
+    torch.cuda.empty_cache()
 
 
 def test_llama7b_m8_ctx512():
