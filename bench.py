@@ -30,6 +30,7 @@ HBM_PEAK_GBS = 8000.0
 HBM_WORKLOAD = "llama13b-bf16-m16-ctx1024"
 HBM_PROFILE = "verify_step_llama13b_m16_ctx1024_hbm_bytes.txt"
 I8_WORKLOAD = "llama13b-i8-m16-ctx1024"
+MFMA_BF16_PEAK_TFLOPS = 2500.0
 
 
 def log(msg):
@@ -130,6 +131,46 @@ def int8_leg(args):
                      "achieved_gbs": round(proj_gbs, 1), "frac": round(proj_gbs / HBM_PEAK_GBS, 4)}}
 
 
+def prefill_leg(args, h, mc, cap, seed):
+    """Large-M prefill of a 1024-token prompt on the 13B weights already
+    resident: prompt tokens/s, and the projection GEMMs' achieved rate
+    (algorithmic 2 M N K flops; the GEMMs execute twice that, hi and lo rows)."""
+    import torch
+    from paper_2412_18934_amd import device as D
+    from paper_2412_18934_amd import dv
+    n = 1024
+    prompt = synth.prompt(seed, n, mc.vocab)
+    kv = D.DeviceKV(mc.n_layers, mc.n_heads, mc.head_dim, cap, mc.weight_dtype)
+    reps = max(2, min(args.steps, 5))
+    dv.dv_prefill(h, prompt, kv.c)     # warm-up (workspace, GEMM plans)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        kv.c.len = 0
+        nxt = dv.dv_prefill(h, prompt, kv.c)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) / reps * 1e3
+    dv.dv_profile_enable(h, 1 << dv.DV_K_GEMM)
+    dv.dv_profile_read(h, dv.DV_K_GEMM, reset=True)
+    kv.c.len = 0
+    dv.dv_prefill(h, prompt, kv.c)
+    dv.dv_profile_enable(h, 0)
+    gemm_ms, gemm_n = dv.dv_profile_read(h, dv.DV_K_GEMM, reset=True)
+    d, f, L = mc.d_model, mc.d_ffn, mc.n_layers
+    gemm_flops = 2.0 * n * L * (4 * d * d + 3 * d * f) + 2.0 * d * mc.vocab
+    attn_flops = 4.0 * L * d * n * (n + 1) / 2
+    tflops = gemm_flops / (gemm_ms * 1e-3) / 1e12
+    log("prefill %d tokens: %.2f ms (%.0f tok/s), GEMMs %.2f ms = %.0f TFLOP/s"
+        % (n, ms, n / (ms * 1e-3), gemm_ms, tflops))
+    del kv
+    return {"prompt_tokens": n, "ms": round(ms, 3), "value": round(n / (ms * 1e-3), 1), "unit": "prompt tokens/s",
+            "next_token": int(nxt),
+            "gemm": {"launches": int(gemm_n), "ms": round(gemm_ms, 3), "algorithmic_tflops": round(tflops, 1),
+                     "executed_tflops": round(2 * tflops, 1), "peak_tflops": MFMA_BF16_PEAK_TFLOPS,
+                     "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4)},
+            "total_flops": gemm_flops + attn_flops}
+
+
 def cpu_baseline(wl, toks, par):
     """The oracle as it stands (float64 numpy), timed on the host for one
     whole step of the workload (all layers, same tree and context).  Weight
@@ -178,6 +219,8 @@ def main():
                     help="HIP events around the projection kernels inside the timed region")
     ap.add_argument("--sampled", choices=["on", "off"], default="on",
                     help="also time the temperature-1 step (speculative sampling acceptance)")
+    ap.add_argument("--prefill", choices=["on", "off"], default="on",
+                    help="also time a 1024-token prefill of the 13B model (large-M path)")
     ap.add_argument("--int8", choices=["on", "off"], default="on",
                     help="also time the weight-only int8 variant of the 13B workload")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -375,6 +418,8 @@ def main():
         "accept_len": acc.accept_len,
         "sampled": sampled,
     }
+    if args.prefill == "on" and wl.name == HBM_WORKLOAD:
+        result["prefill"] = prefill_leg(args, h, mc, cap, sd["prompt"])
     dv.dv_verify_free(h)
     del W, kv
     torch.cuda.empty_cache()

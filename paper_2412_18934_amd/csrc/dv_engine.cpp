@@ -69,6 +69,12 @@ struct dv_handle {
     StepDesc *h_sd = nullptr;  // the step's tree (kernels get it by value)
     DevAccept *d_acc = nullptr, *h_acc = nullptr;
     float *logits_ws = nullptr;  // [max_tree][vocab] logits of a sampled step without out_logits
+    // large-M prefill (allocated at its first use, sized for pf_cap tokens)
+    BlasCtx *blas = nullptr;
+    int pf_cap = 0;
+    int32_t *pf_tok = nullptr;
+    float *pf_x = nullptr, *pf_q = nullptr, *pf_D0 = nullptr, *pf_D1 = nullptr, *pf_D2 = nullptr;
+    uint16_t *pf_xs = nullptr;
     float *p_ws = nullptr;       // [2][vocab] current / residual distribution of the sampling walk
     GemmPlan p_qkv, p_o, p_gu, p_down, p_lm;
     int n_cu = 256;
@@ -431,6 +437,116 @@ int prepare_sampled(dv_handle *h, const int32_t *tokens, const int32_t *parents,
         sa->u_bonus[i] = u_bonus[i];
     }
     sa->acc = h->d_acc;
+    return DV_OK;
+}
+
+// Large-M prefill: chunks of up to DV_PF_CHUNK tokens, each one causal pass
+// through all layers (plain GEMMs for the projections, the fused kernels of
+// dv_kernels.hip for everything between them).  bf16 weights only.
+constexpr int DV_PF_CHUNK = 1024;
+
+int pf_reserve(dv_handle *h, int tokens)
+{
+    if (h->pf_cap >= tokens) return DV_OK;
+    const dv_config &c = h->cfg;
+    for (void *p : {(void *)h->pf_tok, (void *)h->pf_x, (void *)h->pf_q, (void *)h->pf_D0, (void *)h->pf_D1,
+                    (void *)h->pf_D2, (void *)h->pf_xs})
+        if (p) (void)hipFree(p);
+    h->pf_tok = nullptr;
+    h->pf_x = h->pf_q = h->pf_D0 = h->pf_D1 = h->pf_D2 = nullptr;
+    h->pf_xs = nullptr;
+    h->pf_cap = 0;
+    const size_t Mc = tokens, wide = std::max(c.d_model, c.d_ffn);
+    bool ok = hipMalloc((void **)&h->pf_tok, Mc * 4) == hipSuccess &&
+              hipMalloc((void **)&h->pf_x, Mc * c.d_model * 4) == hipSuccess &&
+              hipMalloc((void **)&h->pf_q, Mc * c.d_model * 4) == hipSuccess &&
+              hipMalloc((void **)&h->pf_D0, 2 * Mc * wide * 4) == hipSuccess &&
+              hipMalloc((void **)&h->pf_D1, 2 * Mc * wide * 4) == hipSuccess &&
+              hipMalloc((void **)&h->pf_D2, std::max(2 * Mc * c.d_model, (size_t)2 * c.vocab) * 4) == hipSuccess &&
+              hipMalloc((void **)&h->pf_xs, 2 * Mc * wide * 2) == hipSuccess;
+    if (!h->blas) h->blas = blas_create();
+    if (!ok || !h->blas) return set_err(h, DV_ENOMEM, "prefill workspace for %d tokens: allocation failed", tokens);
+    h->pf_cap = tokens;
+    return DV_OK;
+}
+
+int prefill_large(dv_handle *h, const int32_t *tokens, int n, dv_kv *kv, int32_t *out_next_token)
+{
+    const dv_config &c = h->cfg;
+    const int d = c.d_model, F = c.d_ffn, H = c.n_heads, hd = c.head_dim, V = c.vocab;
+    hipStream_t s = h->stream;
+    int rc = pf_reserve(h, std::min(n, DV_PF_CHUNK));
+    if (rc) return rc;
+    auto gemm = [&](const void *w, int m, int rows, int k, const uint16_t *B, int ldb, float *D) -> int {
+        prof_begin(h, DV_K_GEMM);
+        const int r = blas_gemm_tn(h->blas, m, rows, k, static_cast<const uint16_t *>(w), B, ldb, D, s);
+        prof_end(h);
+        return r ? set_err(h, DV_EHIP, "hipBLASLt GEMM %dx%dx%d failed", m, rows, k) : DV_OK;
+    };
+    auto ck = [&](hipError_t e, const char *what) -> int { return e == hipSuccess ? DV_OK : hip_fail(h, e, what); };
+    const size_t layer_kv = (size_t)H * kv->capacity * hd;
+    int done = 0;
+    while (done < n) {
+        const int M = std::min(DV_PF_CHUNK, n - done), P0 = kv->len;
+        HIPCHK(h, hipMemcpyAsync(h->pf_tok, tokens + done, (size_t)M * 4, hipMemcpyHostToDevice, s));
+        prof_begin(h, DV_K_NORM);
+        rc = ck(launch_pf_norm(h->pf_tok, h->embed, nullptr, M, d, h->pf_x, h->layers[0].attn_norm, c.rms_eps,
+                               h->pf_xs, s), "prefill embedding norm");
+        prof_end(h);
+        if (rc) return rc;
+        for (int l = 0; l < c.n_layers; ++l) {
+            const LayerW &w = h->layers[l];
+            uint16_t *kc = static_cast<uint16_t *>(kv->k) + (size_t)l * layer_kv;
+            uint16_t *vc = static_cast<uint16_t *>(kv->v) + (size_t)l * layer_kv;
+            if ((rc = gemm(w.wq, d, 2 * M, d, h->pf_xs, d, h->pf_D0)) || (rc = gemm(w.wk, d, 2 * M, d, h->pf_xs, d, h->pf_D1)) ||
+                (rc = gemm(w.wv, d, 2 * M, d, h->pf_xs, d, h->pf_D2)))
+                return rc;
+            prof_begin(h, DV_K_OTHER);
+            rc = ck(launch_pf_qkv(h->pf_D0, h->pf_D1, h->pf_D2, M, P0, H, hd, kv->capacity, h->rope_cos, h->rope_sin,
+                                  h->pf_q, kc, vc, s), "prefill rotary/KV write");
+            prof_end(h);
+            if (rc) return rc;
+            prof_begin(h, DV_K_ATTN);
+            rc = ck(launch_attn_causal(h->pf_q, kc, vc, M, P0, H, hd, kv->capacity, h->pf_xs, s), "causal attention");
+            prof_end(h);
+            if (rc) return rc;
+            if ((rc = gemm(w.wo, d, 2 * M, d, h->pf_xs, d, h->pf_D0))) return rc;
+            prof_begin(h, DV_K_NORM);
+            rc = ck(launch_pf_norm(nullptr, nullptr, h->pf_D0, M, d, h->pf_x, w.ffn_norm, c.rms_eps, h->pf_xs, s),
+                    "prefill residual norm");
+            prof_end(h);
+            if (rc) return rc;
+            if ((rc = gemm(w.w_gate, F, 2 * M, d, h->pf_xs, d, h->pf_D0)) ||
+                (rc = gemm(w.w_up, F, 2 * M, d, h->pf_xs, d, h->pf_D1)))
+                return rc;
+            prof_begin(h, DV_K_OTHER);
+            rc = ck(launch_pf_swiglu(h->pf_D0, h->pf_D1, M, F, h->pf_xs, s), "prefill swiglu");
+            prof_end(h);
+            if (rc) return rc;
+            if ((rc = gemm(w.w_down, d, 2 * M, F, h->pf_xs, F, h->pf_D0))) return rc;
+            const void *next_gain = l + 1 < c.n_layers ? h->layers[l + 1].attn_norm : h->final_norm;
+            prof_begin(h, DV_K_NORM);
+            rc = ck(launch_pf_norm(nullptr, nullptr, h->pf_D0, M, d, h->pf_x, next_gain, c.rms_eps, h->pf_xs, s),
+                    "prefill residual norm");
+            prof_end(h);
+            if (rc) return rc;
+        }
+        const bool last = done + M == n;
+        if (last) {
+            // logits of the chunk's last token only: its hi and lo rows are M rows apart
+            if ((rc = gemm(h->lm_head, V, 2, d, h->pf_xs + (size_t)(M - 1) * d, M * d, h->pf_D2))) return rc;
+            prof_begin(h, DV_K_OTHER);
+            rc = ck(launch_pf_argmax(h->pf_D2, V, h->d_acc, s), "prefill argmax");
+            prof_end(h);
+            if (rc) return rc;
+            HIPCHK(h, hipMemcpyAsync(h->h_acc, h->d_acc, sizeof(DevAccept), hipMemcpyDeviceToHost, s));
+        }
+        HIPCHK(h, hipStreamSynchronize(s));  // also keeps the token upload alive until used
+        prof_collect(h);
+        kv->len += M;
+        done += M;
+        if (last && out_next_token) *out_next_token = h->h_acc->argmax[0];
+    }
     return DV_OK;
 }
 
@@ -841,6 +957,11 @@ int dv_prefill(dv_handle *h, const int32_t *tokens, int32_t n, dv_kv *kv, int32_
     if ((long)kv->len + n > kv->capacity || (long)kv->len + n > h->cfg.max_ctx)
         return set_err(h, DV_ECAPACITY, "prompt of %d does not fit (len %d, capacity %d, max_ctx %d)",
                        n, kv->len, kv->capacity, h->cfg.max_ctx);
+    if (h->wkind == W_BF16 && n > h->cfg.max_tree) {
+        rc = prefill_large(h, tokens, n, kv, out_next_token);
+        h->pending = false;
+        return rc;
+    }
     const int chunk = h->cfg.max_tree;
     int32_t parents[DV_MAX_TREE], pos[DV_MAX_TREE], depth[DV_MAX_TREE];
     uint64_t anc[DV_MAX_TREE];
@@ -880,6 +1001,10 @@ void dv_verify_free(dv_handle *h)
             if (p) (void)hipFree(p);
     if (h->pk_lm) (void)hipFree(h->pk_lm);
     if (h->ps_lm) (void)hipFree(h->ps_lm);
+    for (void *p : {(void *)h->pf_tok, (void *)h->pf_x, (void *)h->pf_q, (void *)h->pf_D0, (void *)h->pf_D1,
+                    (void *)h->pf_D2, (void *)h->pf_xs})
+        if (p) (void)hipFree(p);
+    blas_destroy(h->blas);
     delete h->h_sd;
     if (h->h_acc) (void)hipHostFree(h->h_acc);
     for (auto &e : h->ev_live) { (void)hipEventDestroy(e.a); (void)hipEventDestroy(e.b); }

@@ -194,4 +194,23 @@ hipError_t launch_attention(const AttnArgs &a, int kv_bf16, hipStream_t s);
 hipError_t launch_attn_merge(const AttnArgs &a, int Mpad, hipStream_t s);
 hipError_t launch_accept(const AcceptArgs &a, hipStream_t s);
 hipError_t launch_accept_sampled(const SampleArgs &a, hipStream_t s);
+
+// Large-M prefill (bf16 weights): activations as bf16 [2M][K] (hi rows, then
+// lo rows); GEMM results D [2M][N] fp32 (see dv_blas.cpp).
+hipError_t launch_pf_norm(const int32_t *tokens, const void *embed, const float *D, int M, int d, float *x,
+                          const void *gain, float eps, uint16_t *xs, hipStream_t s);
+hipError_t launch_pf_swiglu(const float *Dg, const float *Du, int M, int F, uint16_t *hs, hipStream_t s);
+hipError_t launch_pf_qkv(const float *Dq, const float *Dk, const float *Dv, int M, int P0, int H, int hd, int cap,
+                         const float *rc, const float *rs, float *q, void *kc, void *vc, hipStream_t s);
+hipError_t launch_attn_causal(const float *q, const void *kc, const void *vc, int M, int P0, int H, int hd, int cap,
+                              uint16_t *out, hipStream_t s);
+hipError_t launch_pf_argmax(const float *Dz, int V, DevAccept *acc, hipStream_t s);
+
+struct BlasCtx;
+BlasCtx *blas_create();
+void blas_destroy(BlasCtx *c);
+// D [n][m] fp32 = B [n][k] . A [m][k]^T, A and B bf16 row-major; B rows ldb
+// elements apart.  Returns 0 on success.
+int blas_gemm_tn(BlasCtx *c, int m, int n, int k, const uint16_t *A, const uint16_t *B, int ldb, float *D,
+                 hipStream_t s);
 hipError_t launch_kv_commit(const CommitArgs &a, int kv_bf16, hipStream_t s);

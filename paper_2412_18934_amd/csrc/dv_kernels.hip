@@ -1543,6 +1543,314 @@ __global__ __launch_bounds__(SAMPLE_THREADS) void k_accept_sampled(SampleArgs a)
 }
 
 // ---------------------------------------------------------------------------
+// Large-M prefill: a prompt chunk of M tokens in one causal pass.  The
+// projections there are plain GEMMs (hipBLASLt) whose activation operand is
+// bf16 [2M][K]: the hi parts (truncation) of the M tokens' rows, then their lo
+// parts (round-to-nearest-even of the remainder), so one GEMM yields D [2M][N]
+// fp32 and the fused kernels below add the two halves (hi first).
+
+// hi/lo of four consecutive values into rows i (hi) and M + i (lo)
+__device__ __forceinline__ void store_hilo4(uint16_t *xs, size_t hi_off, size_t lo_off, float4 v)
+{
+    const float f[4] = {v.x, v.y, v.z, v.w};
+    uint32_t hi[2], lo[2];
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+        uint32_t h2 = 0, l2 = 0;
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+            const float x = f[2 * p + q];
+            const float h = __uint_as_float(__float_as_uint(x) & 0xffff0000u);
+            h2 |= (__float_as_uint(x) >> 16) << (16 * q);
+            l2 |= (uint32_t)f2bf(x - h) << (16 * q);
+        }
+        hi[p] = h2;
+        lo[p] = l2;
+    }
+    *reinterpret_cast<uint2 *>(xs + hi_off) = make_uint2(hi[0], hi[1]);
+    *reinterpret_cast<uint2 *>(xs + lo_off) = make_uint2(lo[0], lo[1]);
+}
+
+constexpr int PF_THREADS = 256;
+
+__device__ __forceinline__ float pf_block_sum(float v, float *red)
+{
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+    __syncthreads();
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+    __syncthreads();
+    float r = 0.f;
+#pragma unroll
+    for (int w = 0; w < PF_THREADS / 64; ++w) r += red[w];
+    return r;
+}
+
+// One token per workgroup: x = (layer 0) the embedding row, or x + D[i] +
+// D[M + i] (a residual projection's two halves); then RMSNorm with gain g into
+// rows i / M + i of xs.  d % 4 == 0, d <= 4 * PF_THREADS * 8.
+__global__ __launch_bounds__(PF_THREADS) void k_pf_norm(const int32_t *tokens, const uint16_t *embed,
+                                                        const float *D, int M, int d, float *x,
+                                                        const uint16_t *gain, float eps, uint16_t *xs)
+{
+    __shared__ float red[PF_THREADS / 64];
+    const int i = blockIdx.x;
+    float4 v[8];
+    float ss = 0.f;
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+        const int k = 4 * (threadIdx.x + PF_THREADS * c);
+        v[c] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (k < d) {
+            if (embed) {
+                const uint2 e = *reinterpret_cast<const uint2 *>(embed + (size_t)tokens[i] * d + k);
+                v[c] = make_float4(__uint_as_float(e.x << 16), __uint_as_float(e.x & 0xffff0000u),
+                                   __uint_as_float(e.y << 16), __uint_as_float(e.y & 0xffff0000u));
+            } else {
+                const float4 a = *reinterpret_cast<const float4 *>(x + (size_t)i * d + k);
+                const float4 hi = *reinterpret_cast<const float4 *>(D + (size_t)i * d + k);
+                const float4 lo = *reinterpret_cast<const float4 *>(D + (size_t)(M + i) * d + k);
+                v[c] = make_float4(a.x + (hi.x + lo.x), a.y + (hi.y + lo.y), a.z + (hi.z + lo.z),
+                                   a.w + (hi.w + lo.w));
+            }
+            *reinterpret_cast<float4 *>(x + (size_t)i * d + k) = v[c];
+            ss += v[c].x * v[c].x + v[c].y * v[c].y + v[c].z * v[c].z + v[c].w * v[c].w;
+        }
+    }
+    const float rinv = 1.f / sqrtf(pf_block_sum(ss, red) / (float)d + eps);
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+        const int k = 4 * (threadIdx.x + PF_THREADS * c);
+        if (k < d) {
+            const float4 u = make_float4(v[c].x * rinv * bf2f(gain[k]), v[c].y * rinv * bf2f(gain[k + 1]),
+                                         v[c].z * rinv * bf2f(gain[k + 2]), v[c].w * rinv * bf2f(gain[k + 3]));
+            store_hilo4(xs, (size_t)i * d + k, (size_t)(M + i) * d + k, u);
+        }
+    }
+}
+
+// silu(gate) * up of the two GEMM results into the down projection's operand
+__global__ __launch_bounds__(PF_THREADS) void k_pf_swiglu(const float *Dg, const float *Du, int M, int F,
+                                                          uint16_t *hs)
+{
+    const size_t e = 4 * ((size_t)blockIdx.x * PF_THREADS + threadIdx.x);
+    if (e >= (size_t)M * F) return;
+    const size_t i = e / F, k = e - i * F;
+    const float4 gh = *reinterpret_cast<const float4 *>(Dg + e);
+    const float4 gl = *reinterpret_cast<const float4 *>(Dg + (size_t)M * F + e);
+    const float4 uh = *reinterpret_cast<const float4 *>(Du + e);
+    const float4 ul = *reinterpret_cast<const float4 *>(Du + (size_t)M * F + e);
+    const float4 h = make_float4(silu(gh.x + gl.x) * (uh.x + ul.x), silu(gh.y + gl.y) * (uh.y + ul.y),
+                                 silu(gh.z + gl.z) * (uh.z + ul.z), silu(gh.w + gl.w) * (uh.w + ul.w));
+    store_hilo4(hs, i * F + k, (size_t)(M + i) * F + k, h);
+}
+
+// Rotary embedding of q and k at positions P0 + i, q stored fp32 [M][d], k
+// and v rounded to bf16 into cache slots P0 + i.  Workgroup = (64 tokens, one
+// head); V goes through LDS so that each cache column is written contiguously.
+template <int HD>
+__global__ __launch_bounds__(PF_THREADS) void k_pf_qkv(const float *Dq, const float *Dk, const float *Dv, int M,
+                                                       int P0, int H, int cap, const float *rc, const float *rs,
+                                                       float *q, uint16_t *kc, uint16_t *vc)
+{
+    constexpr int HALF = HD / 2;
+    __shared__ float vt[HD][64 + 1];
+    const int i0 = blockIdx.x * 64, h = blockIdx.y, d = H * HD;
+    for (int e = threadIdx.x; e < 64 * HALF; e += PF_THREADS) {
+        const int t = e / HALF, j = e - t * HALF, i = i0 + t;
+        if (i >= M) continue;
+        const size_t c1 = (size_t)h * HD + j, c2 = c1 + HALF;
+        const size_t rh = (size_t)i * d, rl = (size_t)(M + i) * d;
+        const float c = rc[(size_t)(P0 + i) * HALF + j], s = rs[(size_t)(P0 + i) * HALF + j];
+        const float q1 = Dq[rh + c1] + Dq[rl + c1], q2 = Dq[rh + c2] + Dq[rl + c2];
+        q[rh + c1] = q1 * c - q2 * s;
+        q[rh + c2] = q2 * c + q1 * s;
+        const float k1 = Dk[rh + c1] + Dk[rl + c1], k2 = Dk[rh + c2] + Dk[rl + c2];
+        uint16_t *kr = kc + ((size_t)h * cap + P0 + i) * HD;
+        kr[j] = f2bf(k1 * c - k2 * s);
+        kr[j + HALF] = f2bf(k2 * c + k1 * s);
+        vt[j][t] = Dv[rh + c1] + Dv[rl + c1];
+        vt[j + HALF][t] = Dv[rh + c2] + Dv[rl + c2];
+    }
+    __syncthreads();
+    const int nt = min(64, M - i0);
+    for (int e = threadIdx.x; e < HD * 64; e += PF_THREADS) {
+        const int j = e / 64, t = e - j * 64;
+        if (t < nt) vc[((size_t)h * HD + j) * cap + P0 + i0 + t] = f2bf(vt[j][t]);
+    }
+}
+
+// Causal attention of the chunk's queries (positions P0 + i) over cache slots
+// [0, P0 + i].  Workgroup = 64 queries of one head, each wave 16 of them and
+// every key tile up to its last query, two tiles in flight; the scores and
+// the running softmax follow the tree-attention kernel (MFMA with q split in
+// hi + lo, exp2 in log2 units), the output goes to rows i / M + i of the O
+// projection's operand.
+template <int HD>
+__global__ __launch_bounds__(256) void k_attn_causal(const float *q, const uint16_t *kc_l, const uint16_t *vc_l,
+                                                     int M, int P0, int H, int cap, uint16_t *out)
+{
+    constexpr int NC = HD / 32, ND = HD / 16;
+    const int h = blockIdx.y, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int n = lane & 15, g = lane >> 4;
+    const int qb = blockIdx.x * 64 + wave * 16;  // first query of this wave
+    if (qb >= M) return;                         // no block-wide barriers below
+    const int D = H * HD;
+    const int kend = P0 + min(qb + 16, M);       // keys this wave may see
+    const int ntile = (kend + 31) / 32;
+    const float scale2 = 1.4426950408889634f / sqrtf((float)HD);
+    const uint16_t *kc = kc_l + (size_t)h * cap * HD;
+    const uint16_t *vc = vc_l + (size_t)h * HD * cap;
+    const int qi = min(qb + n, M - 1);          // this lane's query (B operand column)
+    const int lim = P0 + qb + n;                // last key it sees
+
+    bf16x8 qh[NC], ql[NC];
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+        const float *qp = q + (size_t)qi * D + h * HD + 32 * c + 8 * g;
+        split_hi_lo(*reinterpret_cast<const float4 *>(qp), *reinterpret_cast<const float4 *>(qp + 4), qh[c], ql[c]);
+    }
+    struct Tile {
+        u32x4 ka[NC], kb[NC], v[ND];
+    };
+    auto load = [&](int t, Tile &T) {
+        const int k0 = 32 * t;
+        const int ka = min(k0 + 8 * (n >> 2) + (n & 3), kend - 1);
+        const int kb = min(k0 + 8 * (n >> 2) + 4 + (n & 3), kend - 1);
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            T.ka[c] = *reinterpret_cast<const u32x4 *>(kc + (size_t)ka * HD + 32 * c + 8 * g);
+            T.kb[c] = *reinterpret_cast<const u32x4 *>(kc + (size_t)kb * HD + 32 * c + 8 * g);
+        }
+#pragma unroll
+        for (int dt = 0; dt < ND; ++dt)
+            T.v[dt] = *reinterpret_cast<const u32x4 *>(vc + (size_t)(dt * 16 + n) * cap + k0 + 8 * g);
+    };
+    float m_run = -INFINITY, l_run = 0.f;
+    f32x4 o[ND];
+#pragma unroll
+    for (int dt = 0; dt < ND; ++dt) o[dt] = (f32x4){0.f, 0.f, 0.f, 0.f};
+    auto process = [&](int t, Tile &cur) {
+        const int k0 = 32 * t;
+        f32x4 sa = (f32x4){0.f, 0.f, 0.f, 0.f}, sb = sa;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            const bf16x8 ka8 = __builtin_bit_cast(bf16x8, cur.ka[c]);
+            const bf16x8 kb8 = __builtin_bit_cast(bf16x8, cur.kb[c]);
+            sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka8, qh[c], sa, 0, 0, 0);
+            sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb8, qh[c], sb, 0, 0, 0);
+            sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka8, ql[c], sa, 0, 0, 0);
+            sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb8, ql[c], sb, 0, 0, 0);
+        }
+        // scores of query (lane n) for keys k0 + 8g + i
+        float sv[8], mt = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int key = k0 + 8 * g + i;
+            const float sc = (i < 4 ? sa[i] : sb[i - 4]) * scale2;
+            sv[i] = key <= lim ? sc : -INFINITY;
+            mt = fmaxf(mt, sv[i]);
+        }
+        mt = fmaxf(mt, __shfl_xor(mt, 16));
+        mt = fmaxf(mt, __shfl_xor(mt, 32));
+        const float mnew = fmaxf(m_run, mt);
+        const float alpha = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - mnew);
+        float ps = 0.f, pv[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            pv[i] = sv[i] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(sv[i] - mnew);
+            ps += pv[i];
+        }
+        ps += __shfl_xor(ps, 16);
+        ps += __shfl_xor(ps, 32);
+        l_run = l_run * alpha + ps;
+        m_run = mnew;
+        float al[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) al[j] = __shfl(alpha, 4 * g + j);
+        if (k0 + 32 > kend) {
+            // slots past the wave's last key hold nothing of this chunk yet
+#pragma unroll
+            for (int dt = 0; dt < ND; ++dt)
+#pragma unroll
+                for (int w = 0; w < 4; ++w) {
+                    const int key = k0 + 8 * g + 2 * w;
+                    uint32_t x = cur.v[dt][w];
+                    if (key >= kend) x &= 0xffff0000u;
+                    if (key + 1 >= kend) x &= 0x0000ffffu;
+                    cur.v[dt][w] = x;
+                }
+        }
+        bf16x8 ph, pl;
+        split_hi_lo(make_float4(pv[0], pv[1], pv[2], pv[3]), make_float4(pv[4], pv[5], pv[6], pv[7]), ph, pl);
+#pragma unroll
+        for (int dt = 0; dt < ND; ++dt) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) o[dt][j] *= al[j];
+            const bf16x8 v8 = __builtin_bit_cast(bf16x8, cur.v[dt]);
+            o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph, v8, o[dt], 0, 0, 0);
+            o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pl, v8, o[dt], 0, 0, 0);
+        }
+    };
+    Tile b0, b1;
+    load(0, b0);
+    for (int t = 0; t < ntile; t += 2) {
+        if (t + 1 < ntile) load(t + 1, b1);
+        process(t, b0);
+        if (t + 1 >= ntile) break;
+        if (t + 2 < ntile) load(t + 2, b0);
+        process(t + 1, b1);
+    }
+    // rows of o are queries qb + 4g + j; their sums l sit in lanes 4g + j
+    float lr[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) lr[j] = __shfl(l_run, 4 * g + j);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int i = qb + 4 * g + j;
+        if (i >= M) continue;
+#pragma unroll
+        for (int dt = 0; dt < ND; ++dt) {
+            const float r = o[dt][j] / lr[j];
+            const float hi = __uint_as_float(__float_as_uint(r) & 0xffff0000u);
+            const size_t col = (size_t)h * HD + dt * 16 + n;
+            out[(size_t)i * D + col] = (uint16_t)(__float_as_uint(r) >> 16);
+            out[(size_t)(M + i) * D + col] = f2bf(r - hi);
+        }
+    }
+}
+
+// argmax (lowest id on ties) of hi + lo rows D[0][v] + D[1][v]
+__global__ __launch_bounds__(1024) void k_pf_argmax(const float *Dz, int V, DevAccept *acc)
+{
+    __shared__ float bv[16];
+    __shared__ int bi[16];
+    float best = -INFINITY;
+    int idx = 0x7fffffff;
+    for (int v = threadIdx.x; v < V; v += 1024) {
+        const float z = Dz[v] + Dz[V + v];
+        if (z > best || (z == best && v < idx)) { best = z; idx = v; }
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        const float v2 = __shfl_xor(best, off);
+        const int i2 = __shfl_xor(idx, off);
+        arg_better(best, idx, v2, i2);
+    }
+    if ((threadIdx.x & 63) == 0) {
+        bv[threadIdx.x >> 6] = best;
+        bi[threadIdx.x >> 6] = idx;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        best = bv[0];
+        idx = bi[0];
+        for (int w = 1; w < 16; ++w) arg_better(best, idx, bv[w], bi[w]);
+        acc->argmax[0] = idx;
+    }
+}
+
+// ---------------------------------------------------------------------------
 // KV commit: slot P+k <- slot P+path[k] for k < n, for every (layer, head)
 // of K (blockIdx.y = 0, rows [cap][hd]) and V (1, columns of [hd][cap]).  A
 // destination can be the source of another k, so every entry is read into
@@ -1737,5 +2045,51 @@ hipError_t launch_kv_commit(const CommitArgs &a, int kv_bf16, hipStream_t s)
         hipLaunchKernelGGL(k_kv_commit<uint16_t>, dim3(a.LH, 2), dim3(256), 0, s, a);
     else
         hipLaunchKernelGGL(k_kv_commit<float>, dim3(a.LH, 2), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_pf_norm(const int32_t *tokens, const void *embed, const float *D, int M, int d, float *x,
+                          const void *gain, float eps, uint16_t *xs, hipStream_t s)
+{
+    if (d % 4 || d > 4 * PF_THREADS * 8 || M < 1) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_pf_norm, dim3(M), dim3(PF_THREADS), 0, s, tokens, static_cast<const uint16_t *>(embed), D,
+                       M, d, x, static_cast<const uint16_t *>(gain), eps, xs);
+    return hipGetLastError();
+}
+
+hipError_t launch_pf_swiglu(const float *Dg, const float *Du, int M, int F, uint16_t *hs, hipStream_t s)
+{
+    if (F % 4 || M < 1) return hipErrorInvalidValue;
+    const size_t n4 = (size_t)M * F / 4;
+    hipLaunchKernelGGL(k_pf_swiglu, dim3((unsigned)((n4 + PF_THREADS - 1) / PF_THREADS)), dim3(PF_THREADS), 0, s,
+                       Dg, Du, M, F, hs);
+    return hipGetLastError();
+}
+
+hipError_t launch_pf_qkv(const float *Dq, const float *Dk, const float *Dv, int M, int P0, int H, int hd, int cap,
+                         const float *rc, const float *rs, float *q, void *kc, void *vc, hipStream_t s)
+{
+    const dim3 grid((M + 63) / 64, H);
+    uint16_t *k16 = static_cast<uint16_t *>(kc), *v16 = static_cast<uint16_t *>(vc);
+    if (hd == 128) hipLaunchKernelGGL(k_pf_qkv<128>, grid, dim3(PF_THREADS), 0, s, Dq, Dk, Dv, M, P0, H, cap, rc, rs, q, k16, v16);
+    else if (hd == 64) hipLaunchKernelGGL(k_pf_qkv<64>, grid, dim3(PF_THREADS), 0, s, Dq, Dk, Dv, M, P0, H, cap, rc, rs, q, k16, v16);
+    else return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
+hipError_t launch_attn_causal(const float *q, const void *kc, const void *vc, int M, int P0, int H, int hd, int cap,
+                              uint16_t *out, hipStream_t s)
+{
+    const dim3 grid((M + 63) / 64, H);
+    const uint16_t *k16 = static_cast<const uint16_t *>(kc), *v16 = static_cast<const uint16_t *>(vc);
+    if (hd == 128) hipLaunchKernelGGL(k_attn_causal<128>, grid, dim3(256), 0, s, q, k16, v16, M, P0, H, cap, out);
+    else if (hd == 64) hipLaunchKernelGGL(k_attn_causal<64>, grid, dim3(256), 0, s, q, k16, v16, M, P0, H, cap, out);
+    else return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
+hipError_t launch_pf_argmax(const float *Dz, int V, DevAccept *acc, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_pf_argmax, dim3(1), dim3(1024), 0, s, Dz, V, acc);
     return hipGetLastError();
 }

@@ -105,6 +105,59 @@ def test_llama13b_ctx8192(llama13b):
     llama13b.run(synth.WORKLOADS["llama13b-bf16-ctx8192"])
 
 
+def test_llama13b_prefill_1024(llama13b):
+    """Large-M prefill of a 1024-token prompt at the 13B shape (the prompt
+    bench.py times): layer-0 keys and values of sampled tokens against the
+    oracle computed token by token, and the split property (600 + 424 tokens
+    in two calls write the cache one call writes) on the first, a middle and
+    the last layer."""
+    m = llama13b
+    mc = m.mc
+    n = 1024
+    cap = n + 64
+    prompt = synth.prompt(303, n, mc.vocab)
+    cfg = D.make_config(mc.n_layers, mc.d_model, mc.n_heads, mc.head_dim, mc.d_ffn, mc.vocab,
+                        mc.rms_eps, mc.rope_base, mc.weight_dtype, cap, 64)
+    h = dv.dv_verify_init(cfg, m.dev.c, torch.cuda.current_stream().cuda_stream)
+    try:
+        kv = D.DeviceKV(mc.n_layers, mc.n_heads, mc.head_dim, cap, mc.weight_dtype)
+        dv.dv_prefill(h, prompt, kv.c)
+        kv2 = D.DeviceKV(mc.n_layers, mc.n_heads, mc.head_dim, cap, mc.weight_dtype)
+        dv.dv_prefill(h, prompt[:600], kv2.c)
+        dv.dv_prefill(h, prompt[600:], kv2.c)
+        assert kv.c.len == kv2.c.len == n
+        w0 = m.om.layer(0, np.float64)
+        idx = np.array([0, 1, 17, 511, 600, 1023])
+        u = ov.rmsnorm(ov.bf16_to_f64(m.embed[prompt[idx]]), w0["attn_norm"], mc.rms_eps)
+        hh, hd = mc.n_heads, mc.head_dim
+        k_ref = ov.round_cache(ov.rope((u @ w0["wk"].T).reshape(len(idx), hh, hd), idx, mc.rope_base), "bf16")
+        v_ref = ov.round_cache((u @ w0["wv"].T).reshape(len(idx), hh, hd), "bf16")
+        k, v = kv.layer_host(0, n)
+        for got, want in ((k, k_ref), (v, v_ref)):
+            got = ov.bf16_to_f64(got[:, idx])                  # [H][len(idx)][hd]
+            want = np.transpose(want, (1, 0, 2))
+            rms = np.sqrt(np.mean(want ** 2))
+            np.testing.assert_allclose(got, want, rtol=2 ** -7, atol=1e-4 * rms)
+        # the two calls run other GEMM shapes (other summation orders), so
+        # entries near a bf16 rounding midpoint can round apart; the first
+        # layers keep the row bar, deep layers (where those one-step
+        # differences have passed through many attention layers) a
+        # statistical one: median and tail of |difference| / RMS
+        for l in (0, 1, 2, 20, mc.n_layers - 1):
+            a, b = kv.layer_host(l, n), kv2.layer_host(l, n)
+            for x, y in zip(a, b):
+                x, y = ov.bf16_to_f64(x), ov.bf16_to_f64(y)
+                rms = np.sqrt(np.mean(x ** 2))
+                if l <= 2:
+                    np.testing.assert_allclose(x, y, rtol=2 ** -6, atol=(1e-4 if l == 0 else 1e-2) * rms)
+                else:
+                    dif = np.abs(x - y) / rms
+                    assert np.median(dif) <= 1e-3 and dif.max() <= 5e-2, (l, np.median(dif), dif.max())
+        _say("prefill 1024 at 13B: sampled layer-0 rows and the split property hold")
+    finally:
+        dv.dv_verify_free(h)
+
+
 def test_llama13b_int8_m16_ctx1024():
     """The weight-only int8 13B workload bench.py times beside the headline."""
     wl = synth.WORKLOADS["llama13b-i8-m16-ctx1024"]
