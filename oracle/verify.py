@@ -203,12 +203,14 @@ def silu(z):
 # one forward pass over a tree
 
 
-def forward_tree(model: OracleModel, kv, tokens, parents, dtype=np.float64, kv_dtype=None):
+def forward_tree(model: OracleModel, kv, tokens, parents, dtype=np.float64, kv_dtype=None, x0=None):
     """Logits of every tree node after one pass of the decoder stack.
 
     kv: per layer (K, V) floats [H][P][hd] holding the committed cache.
+    x0: the stack's input rows [M][d] (default: the tokens' embeddings).
     Returns dict(logits [M][V], new_k, new_v: per layer [M][H][hd] rounded to
-    the cache dtype, tree: TreeInfo, pos)."""
+    the cache dtype, tree: TreeInfo, pos, hidden: the residual stream after
+    the last block [M][d])."""
     cfg = model.cfg
     kv_dtype = kv_dtype or cfg.kv_dtype
     info = tree_info(parents)
@@ -222,7 +224,7 @@ def forward_tree(model: OracleModel, kv, tokens, parents, dtype=np.float64, kv_d
     pos = p_ctx + info.depth - 1
     h, hd, d = cfg.n_heads, cfg.head_dim, cfg.d_model
 
-    x = model.embed(tokens, dtype)                           # [M][d]
+    x = model.embed(tokens, dtype) if x0 is None else np.asarray(x0, dtype=dtype)   # [M][d]
     new_k, new_v = [], []
     for l in range(cfg.n_layers):
         w = model.layer(l, dtype)
@@ -250,7 +252,7 @@ def forward_tree(model: OracleModel, kv, tokens, parents, dtype=np.float64, kv_d
         del w
     u = rmsnorm(x, _to_float(model.final_norm, dtype), cfg.rms_eps)
     logits = u @ _to_float(model.lm_head, dtype).T
-    return dict(logits=logits, new_k=new_k, new_v=new_v, tree=info, pos=pos)
+    return dict(logits=logits, new_k=new_k, new_v=new_v, tree=info, pos=pos, hidden=x)
 
 
 # ---------------------------------------------------------------------------
