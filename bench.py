@@ -171,6 +171,56 @@ def prefill_leg(args, h, mc, cap, seed):
             "total_flops": gemm_flops + attn_flops}
 
 
+def draft_leg(args, mc, sd, cap, n_blocks=1, depth=7, width=10, n_tree=16):
+    """Draft-tree construction at the 13B width (Section 4's server setting:
+    width 10, depth 7, 16 candidates) with a random-weight draft of n_blocks
+    blocks plus DGF, sharing the target's embedding and lm_head."""
+    import torch
+    from paper_2412_18934_amd import device as D
+    from paper_2412_18934_amd import dv
+    dcfg = synth.draft_cfg(mc, n_blocks)
+    dseed = sd["weights"] + 1000
+    Wd = D.DeviceWeights(dcfg.n_layers, lambda l: synth.layer_weights(dcfg, dseed, l),
+                         synth.embed(mc, sd["weights"]), synth.lm_head(mc, sd["weights"]), synth.final_norm(dcfg))
+    dg = {k: D.to_device(v, "cuda:0") for k, v in synth.dgf_weights(dcfg, dseed).items()}
+    dgf = dv.dv_dgf_weights(dg["w_hidden"].data_ptr(), dg["w_embed"].data_ptr(), dg["w_gate"].data_ptr())
+    cfg = D.make_config(dcfg.n_layers, dcfg.d_model, dcfg.n_heads, dcfg.head_dim, dcfg.d_ffn, dcfg.vocab,
+                        dcfg.rms_eps, dcfg.rope_base, dcfg.weight_dtype, cap, 64)
+    h = dv.dv_draft_init(cfg, Wd.c, dgf, torch.cuda.current_stream().cuda_stream)
+    kv = D.DeviceKV(dcfg.n_layers, dcfg.n_heads, dcfg.head_dim, cap, dcfg.weight_dtype)
+    p = cap - 64
+    for l in range(dcfg.n_layers):
+        k, v = synth.kv_layer(dcfg, sd["kv"] + 1000, l, p)
+        kv.set_layer(l, k, v)
+    kv.c.len = p
+    rf = torch.from_numpy(synth.features(sd["tree"], 1, dcfg.d_model)[0]).to("cuda:0")
+    root = int(synth.prompt(sd["tree"], 1, mc.vocab)[0])
+    try:
+        for _ in range(2):
+            tok, par, _ = dv.dv_draft_tree(h, root, rf.data_ptr(), kv.c, depth, width, n_tree)
+        reps = max(3, min(args.steps, 10))
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            tok, par, _ = dv.dv_draft_tree(h, root, rf.data_ptr(), kv.c, depth, width, n_tree)
+        ms = (time.perf_counter() - t0) / reps * 1e3
+    finally:
+        dv.dv_verify_free(h)
+    del Wd, dg, kv
+    torch.cuda.empty_cache()
+    log("draft tree (%d block(s), depth %d, width %d, %d nodes): %.3f ms" % (n_blocks, depth, width, len(tok), ms))
+    info = ov_tree_depth(par)
+    return {"blocks": n_blocks, "depth": depth, "width": width, "n_tree": n_tree, "nodes": int(len(tok)),
+            "tree_depth": info, "ms_per_tree": round(ms, 3), "ms_per_pass": round(ms / depth, 3)}
+
+
+def ov_tree_depth(par):
+    dep = [1] * len(par)
+    for i in range(1, len(par)):
+        dep[i] = dep[par[i]] + 1
+    return int(max(dep)) if dep else 0
+
+
 def cpu_baseline(wl, toks, par):
     """The oracle as it stands (float64 numpy), timed on the host for one
     whole step of the workload (all layers, same tree and context).  Weight
@@ -221,6 +271,8 @@ def main():
                     help="also time the temperature-1 step (speculative sampling acceptance)")
     ap.add_argument("--prefill", choices=["on", "off"], default="on",
                     help="also time a 1024-token prefill of the 13B model (large-M path)")
+    ap.add_argument("--draft", choices=["on", "off"], default="on",
+                    help="also time draft-tree construction (1-block DGF draft, width 10, depth 7, 16 nodes)")
     ap.add_argument("--int8", choices=["on", "off"], default="on",
                     help="also time the weight-only int8 variant of the 13B workload")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -420,6 +472,8 @@ def main():
     }
     if args.prefill == "on" and wl.name == HBM_WORKLOAD:
         result["prefill"] = prefill_leg(args, h, mc, cap, sd["prompt"])
+    if args.draft == "on" and wl.name == HBM_WORKLOAD:
+        result["draft"] = draft_leg(args, mc, sd, cap)
     dv.dv_verify_free(h)
     del W, kv
     torch.cuda.empty_cache()

@@ -193,6 +193,60 @@ int dv_accept_sampled(dv_handle *h, const float *logits, const int32_t *tokens,
                       float temperature, const float *u_accept, const float *u_bonus,
                       dv_accept *out_accept);
 
+/* ---- Draft side (Section 3.1 tree construction, Section 3.2 Dynamic Gated
+ * Fusion, Section 3.3 multiple blocks) ---------------------------------- */
+
+/* DGF weights, device bf16, row-major [out][in]:
+ *   w_hidden [d_model][d_model], w_embed [d_model][d_model],
+ *   w_gate [d_model][2 d_model] (applied to [h1 || h2]).
+ * Fusion: h1 = w_hidden f, h2 = w_embed e, g = sigmoid(w_gate [h1 || h2]),
+ * x0 = g h1 + (1 - g) h2 (no biases). */
+typedef struct dv_dgf_weights {
+    const void *w_hidden;
+    const void *w_embed;
+    const void *w_gate;
+} dv_dgf_weights;
+
+/* A draft handle: the draft's M blocks as a dv_config / dv_weights pair
+ * (n_layers = M, weight_dtype DV_BF16; embed and lm_head are normally the
+ * target's, final_norm the draft's own) plus the DGF weights.  Its KV cache
+ * (dv_kv of the same shape rules) holds the draft's committed context; tree
+ * nodes are written to slots [len, len + n) and never committed here.
+ * Errors: as dv_verify_init, DV_EINVAL for a non-bf16 config or null DGF
+ * weights. */
+int dv_draft_init(const dv_config *cfg, const dv_weights *w, const dv_dgf_weights *dgf, void *stream,
+                  dv_handle **out);
+
+/* One draft pass over an n_tree-node tree (tokens / tree_parents as for
+ * dv_verify_step): node i's input is DGF(feat_in[i], E[tokens[i]]), the
+ * stack runs with the tree mask and positions of the verify step, and
+ *   feat_out:   device [n_tree][d_model] fp32, the residual stream after the
+ *               last block (the feature node i's children take as input);
+ *   out_logits: device [n_tree][vocab] fp32 (after the final norm and
+ *               lm_head).
+ * feat_in: device [n_tree][d_model] fp32.  All device buffers 16-byte
+ * aligned.  Synchronises the stream.  Errors: DV_EINVAL, DV_ESTATE (not a
+ * draft handle), DV_ECAPACITY, DV_EHIP. */
+int dv_draft_forward(dv_handle *h, const int32_t *tokens, const int32_t *tree_parents, int32_t n_tree,
+                     dv_kv *kv, const float *feat_in, float *feat_out, float *out_logits);
+
+/* Draft-tree construction (Section 3.1): the score of a node is the product
+ * of the draft probabilities along its root path; for `depth` rounds the
+ * `width` best-scoring nodes of the newest layer are expanded by their
+ * `width` most probable tokens (lower id first on ties); then the root and
+ * the n_tree - 1 best other nodes (earlier-created first on ties) form the
+ * tree, in creation order.  Node 0 is root_token, fed root_feature (device
+ * [d_model] fp32: the hidden state handed over with the accepted tokens).
+ * Nodes that can no longer reach the final selection are dropped after every
+ * round, so every draft pass covers at most n_tree nodes.
+ * out_tokens / out_parents (host, n_tree entries) receive a tree ready for
+ * dv_verify_step (entries past the returned size are -1); out_scores (host,
+ * nullable) the scores.  Returns the tree size (>= 1), or a negative error:
+ * DV_EINVAL (width > 16, n_tree > max_tree, bad root), DV_ESTATE,
+ * DV_ECAPACITY (len + n_tree beyond the cache), DV_EHIP. */
+int dv_draft_tree(dv_handle *h, int32_t root_token, const float *root_feature, dv_kv *kv, int32_t depth,
+                  int32_t width, int32_t n_tree, int32_t *out_tokens, int32_t *out_parents, float *out_scores);
+
 /* Commit the accepted path of the pending step: for k < accept_len the
  * entries of node path[k] move to slot len + k (all layers, heads, K and V;
  * all sources are read before any destination is written), then

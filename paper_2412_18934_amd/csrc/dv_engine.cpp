@@ -75,6 +75,13 @@ struct dv_handle {
     int32_t *pf_tok = nullptr;
     float *pf_x = nullptr, *pf_q = nullptr, *pf_D0 = nullptr, *pf_D1 = nullptr, *pf_D2 = nullptr;
     uint16_t *pf_xs = nullptr;
+    // draft side
+    bool draft = false;
+    const void *dgf_h = nullptr, *dgf_e = nullptr, *dgf_g = nullptr;  // W_h, W_e [d][d], W_g [d][2d]
+    const float *x_in = nullptr;  // stack input rows for the next forward (null: embeddings)
+    float *feat_a = nullptr, *feat_b = nullptr;  // [DV_TREE_MAX + 1][d] draft features (row 64: the root's input)
+    int32_t *tk_tok = nullptr, *tk_tok_h = nullptr;
+    float *tk_p = nullptr, *tk_p_h = nullptr;
     float *p_ws = nullptr;       // [2][vocab] current / residual distribution of the sampling walk
     GemmPlan p_qkv, p_o, p_gu, p_down, p_lm;
     int n_cu = 256;
@@ -328,6 +335,7 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
         na.ssq = h->ssq;
         na.d = d;
         na.M = M;
+        na.x_in = h->x_in;
         std::memcpy(na.tokens, sd->tokens, sizeof na.tokens);
         prof_begin(h, DV_K_NORM);
         hipError_t e = launch_embed_norm(na, Mpad, h->bf16, s);
@@ -456,7 +464,9 @@ int pf_reserve(dv_handle *h, int tokens)
     h->pf_x = h->pf_q = h->pf_D0 = h->pf_D1 = h->pf_D2 = nullptr;
     h->pf_xs = nullptr;
     h->pf_cap = 0;
-    const size_t Mc = tokens, wide = std::max(c.d_model, c.d_ffn);
+    // wide: the widest operand row (d_ffn for the prefill, 2 d_model for the
+    // draft's gate input)
+    const size_t Mc = tokens, wide = std::max(2 * c.d_model, c.d_ffn);
     bool ok = hipMalloc((void **)&h->pf_tok, Mc * 4) == hipSuccess &&
               hipMalloc((void **)&h->pf_x, Mc * c.d_model * 4) == hipSuccess &&
               hipMalloc((void **)&h->pf_q, Mc * c.d_model * 4) == hipSuccess &&
@@ -547,6 +557,53 @@ int prefill_large(dv_handle *h, const int32_t *tokens, int n, dv_kv *kv, int32_t
         done += M;
         if (last && out_next_token) *out_next_token = h->h_acc->argmax[0];
     }
+    return DV_OK;
+}
+
+// Draft forward over an n-node tree (tree already checked, descriptor not
+// yet filled): DGF of (feat_in rows, token embeddings), the block stack with
+// those rows as input, logits of every node into out_logits, the residual
+// stream after the last block into feat_out.
+int draft_forward_impl(dv_handle *h, const int32_t *tokens, const int32_t *parents, int n, dv_kv *kv,
+                       const int32_t *pos, const int32_t *depth, const uint64_t *anc, const float *feat_in,
+                       float *feat_out, float *out_logits)
+{
+    const dv_config &c = h->cfg;
+    const int d = c.d_model;
+    hipStream_t s = h->stream;
+    int rc = pf_reserve(h, std::max(n, 1));
+    if (rc) return rc;
+    auto gemm = [&](const void *w, int m, int rows, int k, const uint16_t *B, float *D) -> int {
+        prof_begin(h, DV_K_GEMM);
+        const int r = blas_gemm_tn(h->blas, m, rows, k, static_cast<const uint16_t *>(w), B, k, D, s);
+        prof_end(h);
+        return r ? set_err(h, DV_EHIP, "hipBLASLt GEMM %dx%dx%d failed", m, rows, k) : DV_OK;
+    };
+    DgfTokens t{};
+    for (int i = 0; i < n; ++i) t.tok[i] = tokens[i];
+    // operands: pf_xs holds the feature hi/lo rows [2n][d] and then the
+    // [h1 || h2] rows [2n][2d]; the embedding rows go after the first
+    uint16_t *bf = h->pf_xs, *be = h->pf_xs + (size_t)2 * n * d;
+    prof_begin(h, DV_K_OTHER);
+    hipError_t e = launch_dgf_prep(feat_in, h->embed, t, n, d, bf, be, s);
+    prof_end(h);
+    if (e != hipSuccess) return hip_fail(h, e, "dgf prep");
+    if ((rc = gemm(h->dgf_h, d, 2 * n, d, bf, h->pf_D0)) || (rc = gemm(h->dgf_e, d, n, d, be, h->pf_D1))) return rc;
+    prof_begin(h, DV_K_OTHER);
+    e = launch_dgf_mid(h->pf_D0, h->pf_D1, n, d, h->pf_xs, s);
+    prof_end(h);
+    if (e != hipSuccess) return hip_fail(h, e, "dgf gate input");
+    if ((rc = gemm(h->dgf_g, d, 2 * n, 2 * d, h->pf_xs, h->pf_D2))) return rc;
+    prof_begin(h, DV_K_OTHER);
+    e = launch_dgf_out(h->pf_D2, h->pf_D0, h->pf_D1, n, d, h->pf_x, s);
+    prof_end(h);
+    if (e != hipSuccess) return hip_fail(h, e, "dgf output");
+    fill_desc(h->h_sd, tokens, parents, n, kv->len, pos, depth, anc);
+    h->x_in = h->pf_x;
+    rc = enqueue_forward(h, kv, out_logits, true);
+    h->x_in = nullptr;
+    if (rc) return rc;
+    HIPCHK(h, hipMemcpyAsync(feat_out, h->x, (size_t)n * d * sizeof(float), hipMemcpyDeviceToDevice, s));
     return DV_OK;
 }
 
@@ -905,6 +962,173 @@ int dv_accept_sampled(dv_handle *h, const float *logits, const int32_t *tokens, 
     return DV_OK;
 }
 
+int dv_draft_init(const dv_config *cfg, const dv_weights *w, const dv_dgf_weights *dgf, void *stream,
+                  dv_handle **out)
+{
+    if (!cfg || !w || !dgf || !out) return set_err(nullptr, DV_EINVAL, "null argument");
+    if (cfg->weight_dtype != DV_BF16) return set_err(nullptr, DV_EINVAL, "the draft model needs bf16 weights");
+    if (!dgf->w_hidden || !dgf->w_embed || !dgf->w_gate) return set_err(nullptr, DV_EINVAL, "null DGF weight");
+    if (cfg->d_model % 4) return set_err(nullptr, DV_EINVAL, "d_model must be a multiple of 4");
+    dv_handle *h = nullptr;
+    int rc = dv_verify_init(cfg, w, stream, &h);
+    if (rc) return rc;
+    h->draft = true;
+    h->dgf_h = dgf->w_hidden;
+    h->dgf_e = dgf->w_embed;
+    h->dgf_g = dgf->w_gate;
+    const size_t fb = (size_t)(DV_TREE_MAX + 1) * cfg->d_model * sizeof(float);
+    bool ok = hipMalloc((void **)&h->feat_a, fb) == hipSuccess && hipMalloc((void **)&h->feat_b, fb) == hipSuccess &&
+              hipMalloc((void **)&h->tk_tok, DV_TREE_MAX * DV_TOPK_MAX * 4) == hipSuccess &&
+              hipMalloc((void **)&h->tk_p, DV_TREE_MAX * DV_TOPK_MAX * 4) == hipSuccess &&
+              hipHostMalloc((void **)&h->tk_tok_h, DV_TREE_MAX * DV_TOPK_MAX * 4, hipHostMallocDefault) == hipSuccess &&
+              hipHostMalloc((void **)&h->tk_p_h, DV_TREE_MAX * DV_TOPK_MAX * 4, hipHostMallocDefault) == hipSuccess;
+    if (!ok || pf_reserve(h, DV_TREE_MAX) != DV_OK) {
+        dv_verify_free(h);
+        return set_err(nullptr, DV_ENOMEM, "draft workspace allocation failed");
+    }
+    *out = h;
+    return DV_OK;
+}
+
+int dv_draft_forward(dv_handle *h, const int32_t *tokens, const int32_t *tree_parents, int32_t n_tree, dv_kv *kv,
+                     const float *feat_in, float *feat_out, float *out_logits)
+{
+    if (!h) return set_err(nullptr, DV_EINVAL, "null handle");
+    if (h->poisoned) return DV_EHIP;
+    if (!h->draft) return set_err(h, DV_ESTATE, "not a draft handle (dv_draft_init)");
+    if (!tokens || !tree_parents || !feat_in || !feat_out || !out_logits) return set_err(h, DV_EINVAL, "null argument");
+    for (const void *p : {(const void *)feat_in, (const void *)feat_out, (const void *)out_logits})
+        if (reinterpret_cast<uintptr_t>(p) % 16) return set_err(h, DV_EINVAL, "device buffers must be 16-byte aligned");
+    int rc = check_kv(h, kv);
+    if (rc) return rc;
+    if (n_tree < 1 || n_tree > h->cfg.max_tree)
+        return set_err(h, DV_EINVAL, "n_tree %d outside [1, %d]", n_tree, h->cfg.max_tree);
+    for (int i = 0; i < n_tree; ++i)
+        if (tokens[i] < 0 || tokens[i] >= h->cfg.vocab)
+            return set_err(h, DV_EINVAL, "token id %d at node %d outside [0, %d)", tokens[i], i, h->cfg.vocab);
+    int32_t pos[DV_MAX_TREE], depth[DV_MAX_TREE];
+    uint64_t anc[DV_MAX_TREE];
+    if ((rc = check_tree(h, tree_parents, n_tree, kv->len, pos, depth, anc))) return rc;
+    if ((long)kv->len + n_tree > kv->capacity || (long)kv->len + n_tree > h->cfg.max_ctx)
+        return set_err(h, DV_ECAPACITY, "len %d + n_tree %d exceeds capacity %d / max_ctx %d", kv->len, n_tree,
+                       kv->capacity, h->cfg.max_ctx);
+    if ((rc = draft_forward_impl(h, tokens, tree_parents, n_tree, kv, pos, depth, anc, feat_in, feat_out,
+                                 out_logits)))
+        return rc;
+    HIPCHK(h, hipStreamSynchronize(h->stream));
+    prof_collect(h);
+    h->pending = false;
+    return DV_OK;
+}
+
+int dv_draft_tree(dv_handle *h, int32_t root_token, const float *root_feature, dv_kv *kv, int32_t depth,
+                  int32_t width, int32_t n_tree, int32_t *out_tokens, int32_t *out_parents, float *out_scores)
+{
+    if (!h) return set_err(nullptr, DV_EINVAL, "null handle");
+    if (h->poisoned) return DV_EHIP;
+    if (!h->draft) return set_err(h, DV_ESTATE, "not a draft handle (dv_draft_init)");
+    if (!root_feature || !out_tokens || !out_parents) return set_err(h, DV_EINVAL, "null argument");
+    if (reinterpret_cast<uintptr_t>(root_feature) % 16) return set_err(h, DV_EINVAL, "root_feature must be 16-byte aligned");
+    int rc = check_kv(h, kv);
+    if (rc) return rc;
+    const dv_config &c = h->cfg;
+    if (root_token < 0 || root_token >= c.vocab) return set_err(h, DV_EINVAL, "root token %d outside [0, %d)", root_token, c.vocab);
+    if (depth < 1 || depth > DV_MAX_TREE - 1 || width < 1 || width > DV_TOPK_MAX || n_tree < 1 ||
+        n_tree > c.max_tree)
+        return set_err(h, DV_EINVAL, "depth %d, width %d or n_tree %d out of range (width <= %d, n_tree <= %d)", depth,
+                       width, n_tree, DV_TOPK_MAX, c.max_tree);
+    if ((long)kv->len + n_tree > kv->capacity || (long)kv->len + n_tree > c.max_ctx)
+        return set_err(h, DV_ECAPACITY, "len %d + n_tree %d exceeds capacity %d / max_ctx %d", kv->len, n_tree,
+                       kv->capacity, c.max_ctx);
+    const int d = c.d_model;
+    hipStream_t s = h->stream;
+    struct Node {
+        int32_t tok, parent;  // parent: node id
+        double score;
+    };
+    std::vector<Node> nodes{{root_token, -1, 1.0}};
+    std::vector<int> tree{0}, frontier{0};  // node ids; tree kept in creation order
+    std::vector<int> prev_row(1, -1);       // node id -> row of the last forward (-1: none)
+    // feat_a rows: the last forward's output features; row DV_TREE_MAX: the root's input
+    HIPCHK(h, hipMemcpyAsync(h->feat_a + (size_t)DV_TREE_MAX * d, root_feature, (size_t)d * sizeof(float),
+                             hipMemcpyDeviceToDevice, s));
+    auto better = [&](int a, int b) { return nodes[a].score > nodes[b].score || (nodes[a].score == nodes[b].score && a < b); };
+    for (int r = 0; r < depth && !frontier.empty(); ++r) {
+        std::vector<int> chosen = frontier;
+        std::sort(chosen.begin(), chosen.end(), better);
+        if ((int)chosen.size() > width) chosen.resize(width);
+        // one draft pass over the kept tree
+        const int n = (int)tree.size();
+        int32_t tok[DV_MAX_TREE], par[DV_MAX_TREE], pos[DV_MAX_TREE], dep[DV_MAX_TREE];
+        uint64_t anc[DV_MAX_TREE];
+        std::vector<int> row(nodes.size(), -1);
+        RowIndex gi{};
+        for (int i = 0; i < n; ++i) {
+            const Node &nd = nodes[tree[i]];
+            row[tree[i]] = i;
+            tok[i] = nd.tok;
+            par[i] = nd.parent < 0 ? -1 : row[nd.parent];
+            gi.idx[i] = nd.parent < 0 ? DV_TREE_MAX : prev_row[nd.parent];
+        }
+        if ((rc = check_tree(h, par, n, kv->len, pos, dep, anc))) return rc;
+        hipError_t e = launch_gather_rows(h->feat_a, gi, n, d, h->feat_b, s);
+        if (e != hipSuccess) return hip_fail(h, e, "feature gather");
+        // feat_b holds the inputs; the outputs go to feat_a rows [0, n)
+        if ((rc = draft_forward_impl(h, tok, par, n, kv, pos, dep, anc, h->feat_b, h->feat_a, h->logits_ws)))
+            return rc;
+        TopkArgs ta{};
+        for (size_t j = 0; j < chosen.size(); ++j) ta.rows[j] = row[chosen[j]];
+        ta.k = width;
+        ta.out_tok = h->tk_tok;
+        ta.out_p = h->tk_p;
+        prof_begin(h, DV_K_OTHER);
+        e = launch_topk_probs(h->logits_ws, c.vocab, ta, (int)chosen.size(), s);
+        prof_end(h);
+        if (e != hipSuccess) return hip_fail(h, e, "top-k launch");
+        HIPCHK(h, hipMemcpyAsync(h->tk_tok_h, h->tk_tok, chosen.size() * DV_TOPK_MAX * 4, hipMemcpyDeviceToHost, s));
+        HIPCHK(h, hipMemcpyAsync(h->tk_p_h, h->tk_p, chosen.size() * DV_TOPK_MAX * 4, hipMemcpyDeviceToHost, s));
+        HIPCHK(h, hipStreamSynchronize(s));
+        prof_collect(h);
+        prev_row = row;
+        // children, in the order the chosen nodes were ranked
+        std::vector<int> fresh;
+        for (size_t j = 0; j < chosen.size(); ++j)
+            for (int q = 0; q < width; ++q) {
+                nodes.push_back({h->tk_tok_h[j * DV_TOPK_MAX + q], chosen[j],
+                                 nodes[chosen[j]].score * (double)h->tk_p_h[j * DV_TOPK_MAX + q]});
+                fresh.push_back((int)nodes.size() - 1);
+            }
+        prev_row.resize(nodes.size(), -1);
+        // keep the root and the n_tree - 1 best others (a node outside them
+        // can never be selected later: its descendants score no higher)
+        std::vector<int> cand(tree.begin() + 1, tree.end());
+        cand.insert(cand.end(), fresh.begin(), fresh.end());
+        std::sort(cand.begin(), cand.end(), better);
+        if ((int)cand.size() > n_tree - 1) cand.resize(n_tree - 1);
+        std::sort(cand.begin(), cand.end());
+        tree.assign(1, 0);
+        tree.insert(tree.end(), cand.begin(), cand.end());
+        frontier.clear();
+        for (int f : fresh)
+            if (std::binary_search(cand.begin(), cand.end(), f)) frontier.push_back(f);
+    }
+    std::vector<int> row(nodes.size(), -1);
+    for (size_t i = 0; i < tree.size(); ++i) row[tree[i]] = (int)i;
+    for (size_t i = 0; i < tree.size(); ++i) {
+        const Node &nd = nodes[tree[i]];
+        out_tokens[i] = nd.tok;
+        out_parents[i] = nd.parent < 0 ? -1 : row[nd.parent];
+        if (out_scores) out_scores[i] = (float)nd.score;
+    }
+    for (int i = (int)tree.size(); i < n_tree; ++i) {
+        out_tokens[i] = -1;
+        out_parents[i] = -1;
+        if (out_scores) out_scores[i] = 0.f;
+    }
+    h->pending = false;
+    return (int)tree.size();
+}
+
 int dv_kv_commit(dv_handle *h, dv_kv *kv, const dv_accept *acc)
 {
     if (!h) return set_err(nullptr, DV_EINVAL, "null handle");
@@ -1001,6 +1225,10 @@ void dv_verify_free(dv_handle *h)
             if (p) (void)hipFree(p);
     if (h->pk_lm) (void)hipFree(h->pk_lm);
     if (h->ps_lm) (void)hipFree(h->ps_lm);
+    for (void *p : {(void *)h->feat_a, (void *)h->feat_b, (void *)h->tk_tok, (void *)h->tk_p})
+        if (p) (void)hipFree(p);
+    if (h->tk_tok_h) (void)hipHostFree(h->tk_tok_h);
+    if (h->tk_p_h) (void)hipHostFree(h->tk_p_h);
     for (void *p : {(void *)h->pf_tok, (void *)h->pf_x, (void *)h->pf_q, (void *)h->pf_D0, (void *)h->pf_D1,
                     (void *)h->pf_D2, (void *)h->pf_xs})
         if (p) (void)hipFree(p);

@@ -127,6 +127,7 @@ struct GemmShape {
 
 struct NormArgs {
     float *x;                  // [Mpad][d] residual stream (written)
+    const float *x_in;         // [M][d] input rows instead of embeddings, or null
     const void *embed;         // [V][d] token embeddings, weight dtype
     const void *gain;          // [d] weight dtype
     float *u;                  // [Mpad][d] x * gain (fp32), or
@@ -205,6 +206,27 @@ hipError_t launch_pf_qkv(const float *Dq, const float *Dk, const float *Dv, int 
 hipError_t launch_attn_causal(const float *q, const void *kc, const void *vc, int M, int P0, int H, int hd, int cap,
                               uint16_t *out, hipStream_t s);
 hipError_t launch_pf_argmax(const float *Dz, int V, DevAccept *acc, hipStream_t s);
+
+// Draft side
+#define DV_TOPK_MAX 16
+struct DgfTokens {
+    int32_t tok[DV_TREE_MAX];
+};
+struct RowIndex {
+    int32_t idx[DV_TREE_MAX];
+};
+struct TopkArgs {
+    int32_t rows[DV_TREE_MAX];  // logits rows to rank
+    int32_t k;
+    int32_t *out_tok;           // [rows][DV_TOPK_MAX]
+    float *out_p;               // [rows][DV_TOPK_MAX]
+};
+hipError_t launch_dgf_prep(const float *feat, const void *embed, const DgfTokens &t, int n, int d, uint16_t *bf,
+                           uint16_t *be, hipStream_t s);
+hipError_t launch_dgf_mid(float *D1, const float *D2, int n, int d, uint16_t *bc, hipStream_t s);
+hipError_t launch_dgf_out(const float *D3, const float *h1, const float *h2, int n, int d, float *x0, hipStream_t s);
+hipError_t launch_gather_rows(const float *src, const RowIndex &ix, int n, int d, float *dst, hipStream_t s);
+hipError_t launch_topk_probs(const float *logits, int V, const TopkArgs &a, int n_rows, hipStream_t s);
 
 struct BlasCtx;
 BlasCtx *blas_create();

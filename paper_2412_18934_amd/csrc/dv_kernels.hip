@@ -755,11 +755,16 @@ __global__ __launch_bounds__(DV_NORM_THREADS) void k_embed_norm(NormArgs a)
 #pragma unroll
     for (int c = 0; c < NV; ++c) idx[c] = min(c0 + 4 * tid + SPAN * c, c1 - 4);
     float4 v[NV];
-    const W *e = reinterpret_cast<const W *>(a.embed) + (size_t)a.tokens[m] * d;
+    if (a.x_in) {  // input rows given (the draft's fused inputs)
 #pragma unroll
-    for (int c = 0; c < NV; ++c)
-        v[c] = make_float4(Elem<W>::load(e, idx[c]), Elem<W>::load(e, idx[c] + 1),
-                           Elem<W>::load(e, idx[c] + 2), Elem<W>::load(e, idx[c] + 3));
+        for (int c = 0; c < NV; ++c) v[c] = *reinterpret_cast<const float4 *>(a.x_in + (size_t)m * d + idx[c]);
+    } else {
+        const W *e = reinterpret_cast<const W *>(a.embed) + (size_t)a.tokens[m] * d;
+#pragma unroll
+        for (int c = 0; c < NV; ++c)
+            v[c] = make_float4(Elem<W>::load(e, idx[c]), Elem<W>::load(e, idx[c] + 1),
+                               Elem<W>::load(e, idx[c] + 2), Elem<W>::load(e, idx[c] + 3));
+    }
     const W *gp = reinterpret_cast<const W *>(a.gain);
     float ss = 0.f;
 #pragma unroll
@@ -1851,6 +1856,131 @@ __global__ __launch_bounds__(1024) void k_pf_argmax(const float *Dz, int V, DevA
 }
 
 // ---------------------------------------------------------------------------
+// Draft side.  Dynamic Gated Fusion around three plain GEMMs (hipBLASLt, the
+// same [2n][K] hi/lo operand convention as the prefill):
+//   prep: parent features -> hi/lo rows; token embeddings -> bf16 rows
+//   mid:  h1 = W_h f (two halves), h2 = W_e e -> hi/lo rows of [h1 || h2]
+//   out:  g = sigmoid(W_g [h1 || h2]); x0 = g h1 + (1 - g) h2
+__global__ __launch_bounds__(PF_THREADS) void k_dgf_prep(const float *feat, const uint16_t *embed, DgfTokens t,
+                                                         int n, int d, uint16_t *bf, uint16_t *be)
+{
+    const int i = blockIdx.x;
+    for (int k = 4 * threadIdx.x; k < d; k += 4 * PF_THREADS) {
+        store_hilo4(bf, (size_t)i * d + k, (size_t)(n + i) * d + k,
+                    *reinterpret_cast<const float4 *>(feat + (size_t)i * d + k));
+        *reinterpret_cast<uint2 *>(be + (size_t)i * d + k) =
+            *reinterpret_cast<const uint2 *>(embed + (size_t)t.tok[i] * d + k);
+    }
+}
+
+__global__ __launch_bounds__(PF_THREADS) void k_dgf_mid(float *D1, const float *D2, int n, int d, uint16_t *bc)
+{
+    const int i = blockIdx.x;
+    for (int k = 4 * threadIdx.x; k < d; k += 4 * PF_THREADS) {
+        const float4 a = *reinterpret_cast<const float4 *>(D1 + (size_t)i * d + k);
+        const float4 b = *reinterpret_cast<const float4 *>(D1 + (size_t)(n + i) * d + k);
+        const float4 h1 = make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
+        *reinterpret_cast<float4 *>(D1 + (size_t)i * d + k) = h1;
+        const float4 h2 = *reinterpret_cast<const float4 *>(D2 + (size_t)i * d + k);
+        store_hilo4(bc, (size_t)i * 2 * d + k, (size_t)(n + i) * 2 * d + k, h1);
+        store_hilo4(bc, (size_t)i * 2 * d + d + k, (size_t)(n + i) * 2 * d + d + k, h2);
+    }
+}
+
+__global__ __launch_bounds__(PF_THREADS) void k_dgf_out(const float *D3, const float *h1, const float *h2, int n,
+                                                        int d, float *x0)
+{
+    const int i = blockIdx.x;
+    for (int k = threadIdx.x; k < d; k += PF_THREADS) {
+        const float z = D3[(size_t)i * d + k] + D3[(size_t)(n + i) * d + k];
+        const float g = 1.f / (1.f + expf(-z));
+        const float a = h1[(size_t)i * d + k], b = h2[(size_t)i * d + k];
+        x0[(size_t)i * d + k] = g * a + (1.f - g) * b;
+    }
+}
+
+// Row gather: dst[r] = src[idx[r]] (feature rows of d floats).
+__global__ __launch_bounds__(PF_THREADS) void k_gather_rows(const float *src, RowIndex ix, int d, float *dst)
+{
+    const int r = blockIdx.x;
+    const float *sp = src + (size_t)ix.idx[r] * d;
+    for (int k = 4 * threadIdx.x; k < d; k += 4 * PF_THREADS)
+        *reinterpret_cast<float4 *>(dst + (size_t)r * d + k) = *reinterpret_cast<const float4 *>(sp + k);
+}
+
+// The `k` most probable tokens of logits row rows[b] (one workgroup per row):
+// p = softmax(z) in fp32 (max, then the sum of exp in a fixed order), then k
+// rounds of a block-wide arg-max over the ids not taken yet (larger p, then
+// lower id).  V <= 32 * 1024.
+__global__ __launch_bounds__(1024) void k_topk_probs(const float *logits, int V, TopkArgs a)
+{
+    __shared__ float red[16];
+    __shared__ float bv[16];
+    __shared__ int bi[16];
+    __shared__ int win;
+    const int tid = threadIdx.x;
+    const float *z = logits + (size_t)a.rows[blockIdx.x] * V;
+    float zv[32];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int c = 0; c < 32; ++c) {
+        const int v = tid + 1024 * c;
+        zv[c] = v < V ? z[v] : -INFINITY;
+        mx = fmaxf(mx, zv[c]);
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+    if ((tid & 63) == 0) red[tid >> 6] = mx;
+    __syncthreads();
+    mx = red[0];
+    for (int w = 1; w < 16; ++w) mx = fmaxf(mx, red[w]);
+    float sum = 0.f;
+#pragma unroll
+    for (int c = 0; c < 32; ++c) {
+        zv[c] = zv[c] == -INFINITY ? 0.f : expf(zv[c] - mx);
+        sum += zv[c];
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) sum += __shfl_xor(sum, off);
+    __syncthreads();
+    if ((tid & 63) == 0) red[tid >> 6] = sum;
+    __syncthreads();
+    float tot = 0.f;
+    for (int w = 0; w < 16; ++w) tot += red[w];
+    uint32_t taken = 0;
+    for (int r = 0; r < a.k; ++r) {
+        float best = -1.f;
+        int bid = 0x7fffffff;
+#pragma unroll
+        for (int c = 0; c < 32; ++c) {
+            const int v = tid + 1024 * c;
+            if (v < V && !((taken >> c) & 1u) && zv[c] > best) { best = zv[c]; bid = v; }
+        }
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) {
+            const float v2 = __shfl_xor(best, off);
+            const int i2 = __shfl_xor(bid, off);
+            arg_better(best, bid, v2, i2);
+        }
+        if ((tid & 63) == 0) {
+            bv[tid >> 6] = best;
+            bi[tid >> 6] = bid;
+        }
+        __syncthreads();
+        if (tid == 0) {
+            float b = bv[0];
+            int id = bi[0];
+            for (int w = 1; w < 16; ++w) arg_better(b, id, bv[w], bi[w]);
+            win = id;
+            a.out_tok[blockIdx.x * DV_TOPK_MAX + r] = id;
+            a.out_p[blockIdx.x * DV_TOPK_MAX + r] = b / tot;
+        }
+        __syncthreads();
+        if (win % 1024 == tid) taken |= 1u << (win / 1024);
+    }
+}
+
+// ---------------------------------------------------------------------------
 // KV commit: slot P+k <- slot P+path[k] for k < n, for every (layer, head)
 // of K (blockIdx.y = 0, rows [cap][hd]) and V (1, columns of [hd][cap]).  A
 // destination can be the source of another k, so every entry is read into
@@ -2091,5 +2221,40 @@ hipError_t launch_attn_causal(const float *q, const void *kc, const void *vc, in
 hipError_t launch_pf_argmax(const float *Dz, int V, DevAccept *acc, hipStream_t s)
 {
     hipLaunchKernelGGL(k_pf_argmax, dim3(1), dim3(1024), 0, s, Dz, V, acc);
+    return hipGetLastError();
+}
+
+hipError_t launch_dgf_prep(const float *feat, const void *embed, const DgfTokens &t, int n, int d, uint16_t *bf,
+                           uint16_t *be, hipStream_t s)
+{
+    if (n < 1 || n > DV_TREE_MAX || d % 4) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_dgf_prep, dim3(n), dim3(PF_THREADS), 0, s, feat, static_cast<const uint16_t *>(embed), t, n, d,
+                       bf, be);
+    return hipGetLastError();
+}
+
+hipError_t launch_dgf_mid(float *D1, const float *D2, int n, int d, uint16_t *bc, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_dgf_mid, dim3(n), dim3(PF_THREADS), 0, s, D1, D2, n, d, bc);
+    return hipGetLastError();
+}
+
+hipError_t launch_dgf_out(const float *D3, const float *h1, const float *h2, int n, int d, float *x0, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_dgf_out, dim3(n), dim3(PF_THREADS), 0, s, D3, h1, h2, n, d, x0);
+    return hipGetLastError();
+}
+
+hipError_t launch_gather_rows(const float *src, const RowIndex &ix, int n, int d, float *dst, hipStream_t s)
+{
+    if (n < 1 || n > DV_TREE_MAX || d % 4) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_gather_rows, dim3(n), dim3(PF_THREADS), 0, s, src, ix, d, dst);
+    return hipGetLastError();
+}
+
+hipError_t launch_topk_probs(const float *logits, int V, const TopkArgs &a, int n_rows, hipStream_t s)
+{
+    if (n_rows < 1 || n_rows > DV_TREE_MAX || a.k < 1 || a.k > DV_TOPK_MAX || V > 32 * 1024) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_topk_probs, dim3(n_rows), dim3(1024), 0, s, logits, V, a);
     return hipGetLastError();
 }

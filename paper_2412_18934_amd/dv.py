@@ -21,6 +21,7 @@ DV_K_GEMM, DV_K_ATTN, DV_K_NORM, DV_K_OTHER = 0, 1, 2, 3
 
 # every symbol include/dv.h declares
 EXPORTS = ("dv_verify_init", "dv_verify_step", "dv_verify_step_sampled", "dv_accept_sampled",
+           "dv_draft_init", "dv_draft_forward", "dv_draft_tree",
            "dv_kv_commit", "dv_prefill", "dv_verify_free", "dv_last_error", "dv_tree_prepare",
            "dv_profile_enable", "dv_profile_read")
 
@@ -50,6 +51,10 @@ class dv_weights(ctypes.Structure):
                 ("w_down", _PP), ("lm_head_scale", ctypes.c_void_p), ("wq_scale", _PP),
                 ("wk_scale", _PP), ("wv_scale", _PP), ("wo_scale", _PP), ("w_gate_scale", _PP),
                 ("w_up_scale", _PP), ("w_down_scale", _PP)]
+
+
+class dv_dgf_weights(ctypes.Structure):
+    _fields_ = [("w_hidden", ctypes.c_void_p), ("w_embed", ctypes.c_void_p), ("w_gate", ctypes.c_void_p)]
 
 
 class dv_kv(ctypes.Structure):
@@ -95,6 +100,13 @@ def lib():
         L.dv_accept_sampled.argtypes = [vp, vp, i32p, i32p, i32, vp, ctypes.c_float, f32p, f32p,
                                         ctypes.POINTER(dv_accept)]
         L.dv_accept_sampled.restype = ctypes.c_int
+        L.dv_draft_init.argtypes = [ctypes.POINTER(dv_config), ctypes.POINTER(dv_weights),
+                                    ctypes.POINTER(dv_dgf_weights), vp, ctypes.POINTER(vp)]
+        L.dv_draft_init.restype = ctypes.c_int
+        L.dv_draft_forward.argtypes = [vp, i32p, i32p, i32, ctypes.POINTER(dv_kv), vp, vp, vp]
+        L.dv_draft_forward.restype = ctypes.c_int
+        L.dv_draft_tree.argtypes = [vp, i32, vp, ctypes.POINTER(dv_kv), i32, i32, i32, i32p, i32p, f32p]
+        L.dv_draft_tree.restype = ctypes.c_int
         L.dv_kv_commit.argtypes = [vp, ctypes.POINTER(dv_kv), ctypes.POINTER(dv_accept)]
         L.dv_kv_commit.restype = ctypes.c_int
         L.dv_prefill.argtypes = [vp, i32p, i32, ctypes.POINTER(dv_kv), i32p]
@@ -185,6 +197,34 @@ def dv_accept_sampled(h, logits: int, tokens, tree_parents, draft_probs: int, te
                                  ctypes.byref(acc))
     _check(rc, h)
     return acc
+
+
+def dv_draft_init(cfg: dv_config, weights: dv_weights, dgf: dv_dgf_weights, stream: int = 0):
+    h = ctypes.c_void_p()
+    rc = lib().dv_draft_init(ctypes.byref(cfg), ctypes.byref(weights), ctypes.byref(dgf),
+                             ctypes.c_void_p(stream or None), ctypes.byref(h))
+    _check(rc, None)
+    return h
+
+
+def dv_draft_forward(h, tokens, tree_parents, kv: dv_kv, feat_in: int, feat_out: int, out_logits: int):
+    """feat_in / feat_out / out_logits: device addresses."""
+    t, p = _i32(tokens), _i32(tree_parents)
+    rc = lib().dv_draft_forward(h, _ptr(t), _ptr(p), len(t), ctypes.byref(kv), ctypes.c_void_p(feat_in or None),
+                                ctypes.c_void_p(feat_out or None), ctypes.c_void_p(out_logits or None))
+    _check(rc, h)
+
+
+def dv_draft_tree(h, root_token: int, root_feature: int, kv: dv_kv, depth: int, width: int, n_tree: int):
+    """Returns (tokens, parents, scores) of the constructed tree (numpy)."""
+    tok = np.full(n_tree, -1, dtype=np.int32)
+    par = np.full(n_tree, -1, dtype=np.int32)
+    sc = np.zeros(n_tree, dtype=np.float32)
+    rc = lib().dv_draft_tree(h, int(root_token), ctypes.c_void_p(root_feature or None), ctypes.byref(kv), depth,
+                             width, n_tree, _ptr(tok), _ptr(par), _fptr(sc))
+    if rc < 0:
+        _check(rc, h)
+    return tok[:rc], par[:rc], sc[:rc]
 
 
 def dv_kv_commit(h, kv: dv_kv, accept: dv_accept):

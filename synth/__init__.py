@@ -333,6 +333,28 @@ def draft_rows(seed: int, m: int, vocab: int, sharp: float = 8.0, stream: int = 
     return (w / w.sum(axis=1, keepdims=True)).astype(np.float32)
 
 
+T_DGF = 900000             # DGF weights of a draft: ids T_DGF + 0, 1, 2
+T_FEATURE = 900010         # hidden states handed to a draft
+
+
+def draft_cfg(target: ModelCfg, n_blocks: int) -> ModelCfg:
+    """The draft's block stack: n_blocks Llama blocks of the target's width."""
+    return replace(target, n_layers=n_blocks)
+
+
+def dgf_weights(cfg: ModelCfg, seed: int) -> dict:
+    """DGF weights (bf16 bits): w_hidden, w_embed [d][d], w_gate [d][2d]."""
+    d, s = cfg.d_model, cfg.init_std
+    return {"w_hidden": normal(seed, T_DGF, d * d, s, "bf16").reshape(d, d),
+            "w_embed": normal(seed, T_DGF + 1, d * d, s, "bf16").reshape(d, d),
+            "w_gate": normal(seed, T_DGF + 2, 2 * d * d, s, "bf16").reshape(d, 2 * d)}
+
+
+def features(seed: int, n: int, d: int, sigma: float = 1.0, stream: int = 0) -> np.ndarray:
+    """n hidden-state rows [n][d] float32, N(0, sigma^2)."""
+    return normal(seed, T_FEATURE + stream, n * d, sigma, "f32").reshape(n, d)
+
+
 def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
     """Storage conversion for uploading/reading bf16 buffers (exact)."""
     return (bits.astype(np.uint32) << 16).view(np.float32)
