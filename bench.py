@@ -204,14 +204,25 @@ def draft_leg(args, mc, sd, cap, n_blocks=1, depth=7, width=10, n_tree=16):
         for _ in range(reps):
             tok, par, _ = dv.dv_draft_tree(h, root, rf.data_ptr(), kv.c, depth, width, n_tree)
         ms = (time.perf_counter() - t0) / reps * 1e3
+        # draft passes actually run (construction stops once no expandable
+        # node can still reach the final selection): every pass issues
+        # 4 projections per block, the lm_head and the three DGF GEMMs
+        dv.dv_profile_enable(h, 1 << dv.DV_K_GEMM)
+        dv.dv_profile_read(h, dv.DV_K_GEMM, reset=True)
+        dv.dv_draft_tree(h, root, rf.data_ptr(), kv.c, depth, width, n_tree)
+        dv.dv_profile_enable(h, 0)
+        _, n_gemm = dv.dv_profile_read(h, dv.DV_K_GEMM, reset=True)
+        passes = n_gemm // (4 * n_blocks + 4)
     finally:
         dv.dv_verify_free(h)
     del Wd, dg, kv
     torch.cuda.empty_cache()
     log("draft tree (%d block(s), depth %d, width %d, %d nodes): %.3f ms" % (n_blocks, depth, width, len(tok), ms))
-    info = ov_tree_depth(par)
+    pass_bytes = 2 * (n_blocks * dcfg.layer_params() + 4 * dcfg.d_model ** 2 + dcfg.vocab * dcfg.d_model)
     return {"blocks": n_blocks, "depth": depth, "width": width, "n_tree": n_tree, "nodes": int(len(tok)),
-            "tree_depth": info, "ms_per_tree": round(ms, 3), "ms_per_pass": round(ms / depth, 3)}
+            "tree_depth": ov_tree_depth(par), "passes": int(passes), "ms_per_tree": round(ms, 3),
+            "ms_per_pass": round(ms / max(passes, 1), 3),
+            "pass_weight_gbs": round(pass_bytes / (ms / max(passes, 1) * 1e-3) / 1e9, 1)}
 
 
 def ov_tree_depth(par):
