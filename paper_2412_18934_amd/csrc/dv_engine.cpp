@@ -740,7 +740,11 @@ int dv_verify_init(const dv_config *cfg, const dv_weights *w, void *stream, dv_h
         }
     h->ssq_max = std::max({DV_NORM_SLICES, h->p_o.n_groups, h->p_down.n_groups});
     h->attn_split_max = std::max(ceil_div(c.max_ctx, DV_ATTN_SPLIT_KEYS), ceil_div(512, H));
-    // the attention partials are addressed with 32-bit byte offsets
+    // the split-K and attention partials are addressed with 32-bit byte offsets
+    if ((double)part_elems * 4 >= 2147483648.0) {
+        dv_verify_free(h);
+        return set_err(nullptr, DV_EINVAL, "model too large for the split-K partial buffer");
+    }
     if ((double)H * h->attn_split_max * DV_TREE_MAX * hd * 4 >= 2147483648.0) {
         dv_verify_free(h);
         return set_err(nullptr, DV_EINVAL, "max_ctx too large for the attention split buffers");

@@ -578,16 +578,17 @@ __global__ __launch_bounds__(64 * NW) void k_proj(GemmArgs a)
         }
         bool mine = true;
         if (EPI == EPI_RESID && KS > 1) {
-            // publish this split's partial; the last arriver folds them
-            float *pp = a.part + (size_t)unit * NE * 4;
+            // publish this split's partial (16-byte stores written through to
+            // the device-coherent level, cache policy sc1); the last arriver
+            // folds them
+            const __amdgpu_buffer_rsrc_t pr =
+                __builtin_amdgcn_make_buffer_rsrc(a.part, (short)0, 0x7fffffff, 0x00020000);
 #pragma unroll
             for (int c = 0; c < (NE + 64 * NW - 1) / (64 * NW); ++c) {
                 const int e = tid + 64 * NW * c;
-                if (e < NE) {
-#pragma unroll
-                    for (int q = 0; q < 4; ++q)
-                        __hip_atomic_store(pp + e * 4 + q, v[c][q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                }
+                if (e < NE)
+                    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v[c]), pr,
+                                                           (uint32_t)(((size_t)unit * NE + e) * 16), 0, 16);
             }
             // the partial is globally visible once the stores completed
             asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -604,12 +605,10 @@ __global__ __launch_bounds__(64 * NW) void k_proj(GemmArgs a)
                     const int e = tid + 64 * NW * c;
                     v[c] = (f32x4){0.f, 0.f, 0.f, 0.f};
                     if (e < NE) {
-                        for (int k = 0; k < KS; ++k) {
-                            const float *q = a.part + ((size_t)(g * KS + k) * NE + e) * 4;
-#pragma unroll
-                            for (int j = 0; j < 4; ++j)
-                                v[c][j] += __hip_atomic_load(q + j, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                        }
+                        for (int k = 0; k < KS; ++k)
+                            v[c] += __builtin_bit_cast(
+                                f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                           pr, (uint32_t)(((size_t)(g * KS + k) * NE + e) * 16), 0, 16));
                     }
                 }
                 if (tid == 0) __hip_atomic_store(a.cnt + g, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -2020,8 +2019,8 @@ static const void *proj_kernel_mt(int mt)
     switch (mt) {
     case 1: return (const void *)k_proj<1, EPI, KV, 4, U1, RB, Q8>;
     case 2: return (const void *)k_proj<2, EPI, KV, 4, 2, RB, Q8>;
-    case 3: return (const void *)k_proj<3, EPI, KV, 4, 1, RB, Q8>;
-    case 4: return (const void *)k_proj<4, EPI, KV, 4, 1, RB, Q8>;
+    case 3: return (const void *)k_proj<3, EPI, KV, 4, 2, RB, Q8>;
+    case 4: return (const void *)k_proj<4, EPI, KV, 4, 2, RB, Q8>;
     default: return nullptr;
     }
 }
