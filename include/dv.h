@@ -111,8 +111,9 @@ typedef struct dv_weights {
 
 /* KV cache: device buffers of weight_dtype, per layer and head
  *   k: [n_layers][n_heads][capacity][head_dim]   (key-major rows)
- *   v: [n_layers][n_heads][head_dim][capacity]   (dim-major: entry j of a
- *      head is column j, so consecutive cache slots of one dim are adjacent)
+ *   v: [n_layers][n_heads][capacity/32][head_dim][32]   (32-slot tiles:
+ *      value (slot s, dim j) of a head at element ((s/32) head_dim + j) 32
+ *      + s%32, so the 32 slots of a tile are one contiguous block, dim-major)
  * Slots [0, len) are committed.  capacity must be a positive multiple of 32
  * (DV_EINVAL otherwise).  len is host state that dv_kv_commit and
  * dv_prefill advance. */

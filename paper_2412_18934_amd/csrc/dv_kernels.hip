@@ -54,6 +54,18 @@ template <> struct Elem<uint16_t> {
 };
 
 // ---------------------------------------------------------------------------
+// V cache layout: per (layer, head), 32-slot tiles one after another, each
+// tile dim-major ([hd][32]): entry (dim j, slot s) at element
+// ((s / 32) hd + j) 32 + s % 32 of the head, so one tile of 32 keys is one
+// contiguous hd x 64-byte block and 8 consecutive slots of a dim are 16
+// contiguous bytes (the PV B-operand).
+
+__device__ __forceinline__ size_t v_index(int j, int s, int hd)
+{
+    return ((size_t)(s >> 5) * hd + j) * 32 + (s & 31);
+}
+
+// ---------------------------------------------------------------------------
 // split layout of activations (see dv_internal.h)
 
 __device__ __forceinline__ size_t split_index(int m, int k, int MT)
@@ -296,11 +308,10 @@ __device__ void qkv_epilogue(const GemmArgs &a, const float *Y, int ld, int t, c
                 const size_t row = ((size_t)h * a.cap + a.P + m) * a.hd;
                 Elem<KV>::store(c, row + j, y1);
                 Elem<KV>::store(c, row + j + half, y2);
-            } else {                // V: [H][hd][cap]
-                KV *c = reinterpret_cast<KV *>(a.vc);
-                const size_t col = (size_t)h * a.hd * a.cap + a.P + m;
-                Elem<KV>::store(c, col + (size_t)j * a.cap, y1);
-                Elem<KV>::store(c, col + (size_t)(j + half) * a.cap, y2);
+            } else {                // V: [H][cap/32][hd][32]
+                KV *c = reinterpret_cast<KV *>(a.vc) + (size_t)h * a.hd * a.cap;
+                Elem<KV>::store(c, v_index(j, a.P + m, a.hd), y1);
+                Elem<KV>::store(c, v_index(j + half, a.P + m, a.hd), y2);
             }
         }
     }
@@ -799,7 +810,8 @@ __global__ __launch_bounds__(DV_NORM_THREADS) void k_embed_norm(NormArgs a)
 // ---------------------------------------------------------------------------
 // Tree-masked attention, split over keys (flash-decoding style).
 //
-// Cache layouts: K [H][cap][hd] (key-major), V [H][hd][cap] (dim-major).
+// Cache layouts: K [H][cap][hd] (key-major), V [H][cap/32][hd][32] (32-slot
+// tiles, dim-major within a tile; see v_index).
 // Workgroup (split s, head h) covers keys [s*kps, (s+1)*kps) of the P + M
 // cache slots; the tree's own keys/values were written to slots P.. by the
 // QKV epilogue.  Key j is visible to node i iff j < P or bit (j-P) of
@@ -866,7 +878,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mfma(AttnArgs a)
         // allocation (capacity is a multiple of 32); they are masked below
 #pragma unroll
         for (int dt = 0; dt < ND; ++dt)
-            T.v[dt] = *reinterpret_cast<const u32x4 *>(vc + (size_t)(dt * 16 + n) * a.cap + k0 + 8 * g);
+            T.v[dt] = *reinterpret_cast<const u32x4 *>(vc + ((size_t)(k0 >> 5) * HD + dt * 16 + n) * 32 + 8 * g);
     };
 
     for (int q0 = 0; q0 < M; q0 += 16) {
@@ -1144,7 +1156,7 @@ __global__ __launch_bounds__(256) void k_attn_f32(AttnArgs a)
                 const int j = e / HD, d = e % HD;
                 kt[j][d] = j < nk ? kc[(size_t)(t0 + j) * HD + d] : 0.f;
                 const int jv = e % DV_ATTN_TILE, dv = e / DV_ATTN_TILE;
-                vt[jv][dv] = jv < nk ? vc[(size_t)dv * a.cap + t0 + jv] : 0.f;
+                vt[jv][dv] = jv < nk ? vc[v_index(dv, t0 + jv, HD)] : 0.f;
             }
             __syncthreads();
             for (int e = tid; e < 16 * DV_ATTN_TILE; e += 256) {
@@ -1680,7 +1692,7 @@ __global__ __launch_bounds__(PF_THREADS) void k_pf_qkv(const float *Dq, const fl
     const int nt = min(64, M - i0);
     for (int e = threadIdx.x; e < HD * 64; e += PF_THREADS) {
         const int j = e / 64, t = e - j * 64;
-        if (t < nt) vc[((size_t)h * HD + j) * cap + P0 + i0 + t] = f2bf(vt[j][t]);
+        if (t < nt) vc[(size_t)h * HD * cap + v_index(j, P0 + i0 + t, HD)] = f2bf(vt[j][t]);
     }
 }
 
@@ -1728,7 +1740,7 @@ __global__ __launch_bounds__(256) void k_attn_causal(const float *q, const uint1
         }
 #pragma unroll
         for (int dt = 0; dt < ND; ++dt)
-            T.v[dt] = *reinterpret_cast<const u32x4 *>(vc + (size_t)(dt * 16 + n) * cap + k0 + 8 * g);
+            T.v[dt] = *reinterpret_cast<const u32x4 *>(vc + ((size_t)(k0 >> 5) * HD + dt * 16 + n) * 32 + 8 * g);
     };
     float m_run = -INFINITY, l_run = 0.f;
     f32x4 o[ND];
@@ -1981,7 +1993,7 @@ __global__ __launch_bounds__(1024) void k_topk_probs(const float *logits, int V,
 
 // ---------------------------------------------------------------------------
 // KV commit: slot P+k <- slot P+path[k] for k < n, for every (layer, head)
-// of K (blockIdx.y = 0, rows [cap][hd]) and V (1, columns of [hd][cap]).  A
+// of K (blockIdx.y = 0, rows [cap][hd]) and V (1, entries at v_index).  A
 // destination can be the source of another k, so every entry is read into
 // LDS before any entry is written.
 
@@ -1994,14 +2006,14 @@ __global__ __launch_bounds__(256) void k_kv_commit(CommitArgs a)
     const int nel = a.n * a.hd;
     for (int e = threadIdx.x; e < nel; e += blockDim.x) {
         const int k = e / a.hd, d = e % a.hd;
-        const size_t src = is_v ? (size_t)d * a.cap + a.P + a.path[k] : (size_t)(a.P + a.path[k]) * a.hd + d;
+        const size_t src = is_v ? v_index(d, a.P + a.path[k], a.hd) : (size_t)(a.P + a.path[k]) * a.hd + d;
         buf[e] = base[src];
     }
     __syncthreads();
     for (int e = threadIdx.x; e < nel; e += blockDim.x) {
         const int k = e / a.hd, d = e % a.hd;
         if (a.path[k] == k) continue;
-        const size_t dst = is_v ? (size_t)d * a.cap + a.P + k : (size_t)(a.P + k) * a.hd + d;
+        const size_t dst = is_v ? v_index(d, a.P + k, a.hd) : (size_t)(a.P + k) * a.hd + d;
         base[dst] = buf[e];
     }
 }

@@ -75,14 +75,15 @@ class DeviceWeights:
 
 
 class DeviceKV:
-    """KV cache: K [L][H][capacity][hd], V [L][H][hd][capacity] (dim-major),
-    weight dtype.  capacity must be a multiple of 32."""
+    """KV cache: K [L][H][capacity][hd], V [L][H][capacity/32][hd][32] (32-slot
+    tiles, dim-major within a tile), weight dtype.  capacity must be a
+    multiple of 32."""
 
     def __init__(self, n_layers, n_heads, head_dim, capacity, weight_dtype, device="cuda:0",
                  fill=None):
         dt = torch.float32 if weight_dtype == "f32" else torch.bfloat16  # int8 models keep a bf16 cache
         kshape = (n_layers, n_heads, capacity, head_dim)
-        vshape = (n_layers, n_heads, head_dim, capacity)
+        vshape = (n_layers, n_heads, capacity // 32, head_dim, 32)
         if fill is None:
             self.k = torch.zeros(kshape, dtype=dt, device=device)
             self.v = torch.zeros(vshape, dtype=dt, device=device)
@@ -99,7 +100,16 @@ class DeviceKV:
         """Write committed entries [0, n) of layer l from host arrays [H][n][hd]."""
         n = k.shape[1]
         self.k[l, :, :n].copy_(to_device(k, self.k.device))
-        self.v[l, :, :, :n].copy_(to_device(v, self.v.device).transpose(1, 2))
+        slots = self._v_slots(l).clone()           # [H][capacity][hd]
+        slots[:, :n] = to_device(v, self.v.device)
+        h, cap, hd = slots.shape
+        self.v[l].copy_(slots.reshape(h, cap // 32, 32, hd).transpose(2, 3))
+
+    def _v_slots(self, l: int) -> torch.Tensor:
+        """V of layer l viewed slot-major, [H][capacity][hd] (a copy)."""
+        v = self.v[l]
+        h, nt, hd, _ = v.shape
+        return v.transpose(2, 3).reshape(h, nt * 32, hd)
 
     def layer_host(self, l: int, n: int):
         """Entries [0, n) of layer l as host arrays [H][n][hd] in the stored format."""
@@ -108,4 +118,4 @@ class DeviceKV:
             if t.dtype == torch.bfloat16:
                 return t.view(torch.int16).numpy().view(np.uint16)
             return t.numpy()
-        return host(self.k[l, :, :n]), host(self.v[l, :, :, :n].transpose(1, 2))
+        return host(self.k[l, :, :n]), host(self._v_slots(l)[:, :n])
