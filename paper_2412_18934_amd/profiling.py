@@ -1,15 +1,17 @@
 """Summaries of rocprofv3 output for libdv kernels (text, for profiles/).
 
     python -m paper_2412_18934_amd.profiling stats <kernel_stats.csv> <kernel_trace.csv> <out.md> <command>
-    python -m paper_2412_18934_amd.profiling hbm <fetch counter_collection.csv> <write counter_collection.csv> <out.txt> <command>
+    python -m paper_2412_18934_amd.profiling hbm <fetch counter_collection.csv> <write counter_collection.csv> <out.txt> <command> <ref bytes>
 
 ``stats`` writes a per-kernel table (calls, average, share) plus the average
 duration of the projection kernels (k_proj, k_gemm_valu), the figure bench.py's roofline
 uses.  ``hbm`` turns FETCH_SIZE / WRITE_SIZE (KiB per dispatch) into bytes per
-dispatch, scaled by what the same counters read for a reference copy of known
-size (the 256 MiB device copy bench.py --calibrate-copy issues: 256 MiB read
-and 256 MiB written), and records a hash of the kernel source so that a reader
-can tell whether the numbers still describe the current kernels.
+dispatch, scaled by what the same counters read for a plain copy of known
+size: the weight-packing kernel k_pack_blocks, which at init reads every
+projection matrix once and writes its packed copy once (<ref bytes> in total
+each way, over all its dispatches).  It records a hash of the kernel source
+so that a reader can tell whether the numbers still describe the current
+kernels.
 """
 from __future__ import annotations
 
@@ -23,11 +25,11 @@ import sys
 PKG = os.path.dirname(os.path.abspath(__file__))
 KERNEL_SOURCES = ("csrc/dv_kernels.hip", "csrc/dv_engine.cpp", "csrc/dv_internal.h")
 PROJ_PREFIXES = ("k_proj", "k_gemm")
+REF_KERNEL = "k_pack_blocks"
 
 
 def is_projection(name: str) -> bool:
     return name.startswith(PROJ_PREFIXES)
-CALIB_BYTES = 256 << 20
 
 
 def source_hash() -> str:
@@ -79,23 +81,23 @@ def summarize_stats(stats_csv, trace_csv, out_path, command):
         fh.write("\n".join(lines) + "\n")
 
 
-def summarize_hbm(fetch_csv, write_csv, out_path, command):
+def summarize_hbm(fetch_csv, write_csv, out_path, command, ref_bytes):
     def per_kernel(path):
         agg = collections.defaultdict(list)
         for r in csv.DictReader(open(path)):
             agg[_short(r["Kernel_Name"])].append(float(r["Counter_Value"]))
         return agg
     f, w = per_kernel(fetch_csv), per_kernel(write_csv)
-    # reference: the copy that reads CALIB_BYTES (largest copyBuffer dispatch)
-    f_ref = max(f.get("__amd_rocclr_copyBuffer", [0.0]))
-    w_ref = max(w.get("__amd_rocclr_copyBuffer", [0.0]))
-    fs = CALIB_BYTES / (f_ref * 1024) if f_ref else float("nan")
-    ws = CALIB_BYTES / (w_ref * 1024) if w_ref else float("nan")
+    ref_bytes = float(ref_bytes)
+    f_ref, w_ref = sum(f.get(REF_KERNEL, [])), sum(w.get(REF_KERNEL, []))
+    fs = ref_bytes / (f_ref * 1024) if f_ref else float("nan")
+    ws = ref_bytes / (w_ref * 1024) if w_ref else float("nan")
     lines = ["# HBM bytes per dispatch (rocprofv3 FETCH_SIZE / WRITE_SIZE)", "",
              "command: " + command,
              "source_hash: %s" % source_hash(),
-             "reference copy: %d bytes; FETCH_SIZE reads %.1f KiB -> scale %.4f; "
-             "WRITE_SIZE reads %.1f KiB -> scale %.4f" % (CALIB_BYTES, f_ref, fs, w_ref, ws), ""]
+             "reference: %s, %d dispatches reading and writing %.0f bytes in total; FETCH_SIZE reads "
+             "%.1f KiB -> scale %.4f; WRITE_SIZE reads %.1f KiB -> scale %.4f"
+             % (REF_KERNEL, len(f.get(REF_KERNEL, [])), ref_bytes, f_ref, fs, w_ref, ws), ""]
     for k in sorted(set(f) & set(w)):
         if not k.startswith("k_"):
             continue
@@ -141,6 +143,6 @@ if __name__ == "__main__":
     if sys.argv[1] == "stats":
         summarize_stats(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5])
     elif sys.argv[1] == "hbm":
-        summarize_hbm(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5])
+        summarize_hbm(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5], sys.argv[6])
     else:
         raise SystemExit(__doc__)
