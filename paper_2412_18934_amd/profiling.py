@@ -2,6 +2,7 @@
 
     python -m paper_2412_18934_amd.profiling stats <kernel_stats.csv> <kernel_trace.csv> <out.md> <command>
     python -m paper_2412_18934_amd.profiling hbm <fetch counter_collection.csv> <write counter_collection.csv> <out.txt> <command> <ref bytes>
+    python -m paper_2412_18934_amd.profiling mfma <counter_collection.csv> <out.txt> <command>
 
 ``stats`` writes a per-kernel table (calls, average, share) plus the average
 duration of the projection kernels (k_proj, k_gemm_valu), the figure bench.py's roofline
@@ -11,7 +12,11 @@ size: the weight-packing kernel k_pack_blocks, which at init reads every
 projection matrix once and writes its packed copy once (<ref bytes> in total
 each way, over all its dispatches).  It records a hash of the kernel source
 so that a reader can tell whether the numbers still describe the current
-kernels.
+kernels.  ``mfma`` reads SQ_VALU_MFMA_BUSY_CYCLES and
+SQ_INSTS_VALU_MFMA_MOPS_BF16 per dispatch and reports, per kernel that issues
+bf16 MFMAs, the MFMA busy fraction (busy cycles over duration x 2.4 GHz x
+1024 SIMDs) and the executed MFMA rate (512 flops per MOP over the dispatch
+duration) against the 2.5 PFLOP/s dense bf16 peak.
 """
 from __future__ import annotations
 
@@ -26,6 +31,9 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 KERNEL_SOURCES = ("csrc/dv_kernels.hip", "csrc/dv_engine.cpp", "csrc/dv_internal.h")
 PROJ_PREFIXES = ("k_proj", "k_gemm")
 REF_KERNEL = "k_pack_blocks"
+CLOCK_HZ = 2.4e9      # peak engine clock
+N_SIMD = 256 * 4      # compute units x SIMDs
+BF16_PEAK = 2.5e15    # dense bf16 MFMA flop/s
 
 
 def is_projection(name: str) -> bool:
@@ -109,6 +117,34 @@ def summarize_hbm(fetch_csv, write_csv, out_path, command, ref_bytes):
         fh.write("\n".join(lines) + "\n")
 
 
+def summarize_mfma(counter_csv, out_path, command):
+    per = collections.defaultdict(lambda: collections.defaultdict(dict))
+    for r in csv.DictReader(open(counter_csv)):
+        k = _short(r["Kernel_Name"])
+        d = per[k][r["Dispatch_Id"]]
+        d[r["Counter_Name"]] = float(r["Counter_Value"])
+        d["dur"] = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e9
+    lines = ["# MFMA utilisation per dispatch (rocprofv3 SQ_VALU_MFMA_BUSY_CYCLES, SQ_INSTS_VALU_MFMA_MOPS_BF16)",
+             "", "command: " + command, "source_hash: %s" % source_hash(),
+             "busy = busy cycles / (duration x %.1f GHz x %d SIMDs); rate = 512 x MOPS / duration, "
+             "against %.1f PFLOP/s dense bf16; durations are those of the counter run" %
+             (CLOCK_HZ / 1e9, N_SIMD, BF16_PEAK / 1e15), "",
+             "| kernel | dispatches | avg us | MFMA busy | executed TFLOP/s | of bf16 peak |",
+             "|---|---|---|---|---|---|"]
+    for k, ds in sorted(per.items()):
+        vals = [d for d in ds.values() if d.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0) > 0 and d["dur"] > 0]
+        if not vals:
+            continue
+        dur = statistics.mean(d["dur"] for d in vals)
+        busy = statistics.mean(d.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) / (d["dur"] * CLOCK_HZ * N_SIMD)
+                               for d in vals)
+        rate = statistics.mean(512 * d["SQ_INSTS_VALU_MFMA_MOPS_BF16"] / d["dur"] for d in vals)
+        lines.append("| `%s` | %d | %.1f | %.1f%% | %.1f | %.1f%% |"
+                     % (k[:90], len(vals), dur * 1e6, 100 * busy, rate / 1e12, 100 * rate / BF16_PEAK))
+    with open(out_path, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+
+
 def read_hbm_summary(path):
     """(source_hash, {kernel: (dispatches, fetch_bytes, write_bytes)})."""
     out, sh = {}, None
@@ -144,5 +180,7 @@ if __name__ == "__main__":
         summarize_stats(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5])
     elif sys.argv[1] == "hbm":
         summarize_hbm(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5], sys.argv[6])
+    elif sys.argv[1] == "mfma":
+        summarize_mfma(sys.argv[2], sys.argv[3], sys.argv[4])
     else:
         raise SystemExit(__doc__)
