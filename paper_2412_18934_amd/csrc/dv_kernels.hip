@@ -1697,23 +1697,35 @@ __global__ __launch_bounds__(PF_THREADS) void k_pf_qkv(const float *Dq, const fl
 }
 
 // Causal attention of the chunk's queries (positions P0 + i) over cache slots
-// [0, P0 + i].  Workgroup = 64 queries of one head, each wave 16 of them and
-// every key tile up to its last query, two tiles in flight; the scores and
-// the running softmax follow the tree-attention kernel (MFMA with q split in
-// hi + lo, exp2 in log2 units), the output goes to rows i / M + i of the O
+// [0, P0 + i].  Workgroup = 64 queries of one head, each wave 16 of them; the
+// workgroup stages every 32-key tile up to its last query in LDS once (K rows
+// and the tile's V block, rows padded against bank conflicts; the next tile's
+// global loads are in flight while the current one is used), and each wave
+// uses the tiles up to its own last query.  The scores and the running
+// softmax follow the tree-attention kernel (MFMA with q split in hi + lo,
+// exp2 in log2 units); the output goes to rows i / M + i of the O
 // projection's operand.
 template <int HD>
 __global__ __launch_bounds__(256) void k_attn_causal(const float *q, const uint16_t *kc_l, const uint16_t *vc_l,
                                                      int M, int P0, int H, int cap, uint16_t *out)
 {
     constexpr int NC = HD / 32, ND = HD / 16;
-    const int h = blockIdx.y, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    constexpr int KROW = HD * 2 + 16;          // bytes per staged key row (padded)
+    constexpr int VROW = 80;                   // bytes per staged dim row of 32 values (padded)
+    constexpr int KBYTES = 32 * KROW, VBYTES = HD * VROW;
+    constexpr int KCH = 32 * HD / 8, VCH = HD * 4;  // 16-byte chunks of a tile's K and V
+    constexpr int CPT = (KCH + VCH + 255) / 256;     // chunks per thread
+    __shared__ __align__(16) unsigned char smem[2][KBYTES + VBYTES];
+    const int h = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int n = lane & 15, g = lane >> 4;
-    const int qb = blockIdx.x * 64 + wave * 16;  // first query of this wave
-    if (qb >= M) return;                         // no block-wide barriers below
+    const int q0 = blockIdx.x * 64;
+    const int qb = q0 + wave * 16;               // first query of this wave
     const int D = H * HD;
+    const int kend_wg = P0 + min(q0 + 64, M);    // keys the workgroup may see
+    const int ntile = (kend_wg + 31) / 32;
+    const bool active = qb < M;
     const int kend = P0 + min(qb + 16, M);       // keys this wave may see
-    const int ntile = (kend + 31) / 32;
+    const int wtiles = active ? (kend + 31) / 32 : 0;
     const float scale2 = 1.4426950408889634f / sqrtf((float)HD);
     const uint16_t *kc = kc_l + (size_t)h * cap * HD;
     const uint16_t *vc = vc_l + (size_t)h * HD * cap;
@@ -1726,33 +1738,52 @@ __global__ __launch_bounds__(256) void k_attn_causal(const float *q, const uint1
         const float *qp = q + (size_t)qi * D + h * HD + 32 * c + 8 * g;
         split_hi_lo(*reinterpret_cast<const float4 *>(qp), *reinterpret_cast<const float4 *>(qp + 4), qh[c], ql[c]);
     }
-    struct Tile {
-        u32x4 ka[NC], kb[NC], v[ND];
-    };
-    auto load = [&](int t, Tile &T) {
+    // global -> registers -> LDS staging of tile t: chunk e < KCH is 16 bytes
+    // of key row e / (HD / 8) (rows past the workgroup's last key repeat it),
+    // the rest 16 bytes of the tile's V block (dim row, 8 slots)
+    u32x4 stg[CPT];
+    auto fetch = [&](int t) {
         const int k0 = 32 * t;
-        const int ka = min(k0 + 8 * (n >> 2) + (n & 3), kend - 1);
-        const int kb = min(k0 + 8 * (n >> 2) + 4 + (n & 3), kend - 1);
 #pragma unroll
-        for (int c = 0; c < NC; ++c) {
-            T.ka[c] = *reinterpret_cast<const u32x4 *>(kc + (size_t)ka * HD + 32 * c + 8 * g);
-            T.kb[c] = *reinterpret_cast<const u32x4 *>(kc + (size_t)kb * HD + 32 * c + 8 * g);
+        for (int i = 0; i < CPT; ++i) {
+            const int e = tid + 256 * i;
+            if (e < KCH) {
+                const int r = e / (HD / 8), c8 = e % (HD / 8);
+                const int key = min(k0 + r, kend_wg - 1);
+                stg[i] = *reinterpret_cast<const u32x4 *>(kc + (size_t)key * HD + 8 * c8);
+            } else if (e < KCH + VCH) {
+                const int ev = e - KCH;
+                stg[i] = *reinterpret_cast<const u32x4 *>(vc + (size_t)(k0 >> 5) * HD * 32 + 8 * ev);
+            }
         }
-#pragma unroll
-        for (int dt = 0; dt < ND; ++dt)
-            T.v[dt] = *reinterpret_cast<const u32x4 *>(vc + ((size_t)(k0 >> 5) * HD + dt * 16 + n) * 32 + 8 * g);
     };
+    auto stash = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < CPT; ++i) {
+            const int e = tid + 256 * i;
+            if (e < KCH) {
+                const int r = e / (HD / 8), c8 = e % (HD / 8);
+                *reinterpret_cast<u32x4 *>(&smem[buf][r * KROW + 16 * c8]) = stg[i];
+            } else if (e < KCH + VCH) {
+                const int ev = e - KCH, dr = ev >> 2, c8 = ev & 3;
+                *reinterpret_cast<u32x4 *>(&smem[buf][KBYTES + dr * VROW + 16 * c8]) = stg[i];
+            }
+        }
+    };
+
     float m_run = -INFINITY, l_run = 0.f;
     f32x4 o[ND];
 #pragma unroll
     for (int dt = 0; dt < ND; ++dt) o[dt] = (f32x4){0.f, 0.f, 0.f, 0.f};
-    auto process = [&](int t, Tile &cur) {
+    auto process = [&](int t, int buf) {
         const int k0 = 32 * t;
+        const unsigned char *ks = smem[buf], *vs = smem[buf] + KBYTES;
+        const int ra = 8 * (n >> 2) + (n & 3), rb = ra + 4;
         f32x4 sa = (f32x4){0.f, 0.f, 0.f, 0.f}, sb = sa;
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
-            const bf16x8 ka8 = __builtin_bit_cast(bf16x8, cur.ka[c]);
-            const bf16x8 kb8 = __builtin_bit_cast(bf16x8, cur.kb[c]);
+            const bf16x8 ka8 = *reinterpret_cast<const bf16x8 *>(ks + ra * KROW + 64 * c + 16 * g);
+            const bf16x8 kb8 = *reinterpret_cast<const bf16x8 *>(ks + rb * KROW + 64 * c + 16 * g);
             sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka8, qh[c], sa, 0, 0, 0);
             sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb8, qh[c], sb, 0, 0, 0);
             sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka8, ql[c], sa, 0, 0, 0);
@@ -1784,6 +1815,10 @@ __global__ __launch_bounds__(256) void k_attn_causal(const float *q, const uint1
         float al[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) al[j] = __shfl(alpha, 4 * g + j);
+        u32x4 vt[ND];
+#pragma unroll
+        for (int dt = 0; dt < ND; ++dt)
+            vt[dt] = *reinterpret_cast<const u32x4 *>(vs + (dt * 16 + n) * VROW + 16 * g);
         if (k0 + 32 > kend) {
             // slots past the wave's last key hold nothing of this chunk yet
 #pragma unroll
@@ -1791,10 +1826,10 @@ __global__ __launch_bounds__(256) void k_attn_causal(const float *q, const uint1
 #pragma unroll
                 for (int w = 0; w < 4; ++w) {
                     const int key = k0 + 8 * g + 2 * w;
-                    uint32_t x = cur.v[dt][w];
+                    uint32_t x = vt[dt][w];
                     if (key >= kend) x &= 0xffff0000u;
                     if (key + 1 >= kend) x &= 0x0000ffffu;
-                    cur.v[dt][w] = x;
+                    vt[dt][w] = x;
                 }
         }
         bf16x8 ph, pl;
@@ -1803,20 +1838,22 @@ __global__ __launch_bounds__(256) void k_attn_causal(const float *q, const uint1
         for (int dt = 0; dt < ND; ++dt) {
 #pragma unroll
             for (int j = 0; j < 4; ++j) o[dt][j] *= al[j];
-            const bf16x8 v8 = __builtin_bit_cast(bf16x8, cur.v[dt]);
+            const bf16x8 v8 = __builtin_bit_cast(bf16x8, vt[dt]);
             o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph, v8, o[dt], 0, 0, 0);
             o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pl, v8, o[dt], 0, 0, 0);
         }
     };
-    Tile b0, b1;
-    load(0, b0);
-    for (int t = 0; t < ntile; t += 2) {
-        if (t + 1 < ntile) load(t + 1, b1);
-        process(t, b0);
-        if (t + 1 >= ntile) break;
-        if (t + 2 < ntile) load(t + 2, b0);
-        process(t + 1, b1);
+    fetch(0);
+    stash(0);
+    __syncthreads();
+    for (int t = 0; t < ntile; ++t) {
+        const int buf = t & 1;
+        if (t + 1 < ntile) fetch(t + 1);  // in flight while tile t is used
+        if (t < wtiles) process(t, buf);
+        if (t + 1 < ntile) stash(buf ^ 1);
+        __syncthreads();
     }
+    if (!active) return;
     // rows of o are queries qb + 4g + j; their sums l sit in lanes 4g + j
     float lr[4];
 #pragma unroll
