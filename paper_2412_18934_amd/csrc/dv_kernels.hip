@@ -838,7 +838,9 @@ __global__ __launch_bounds__(DV_NORM_THREADS) void k_embed_norm(NormArgs a)
 // DB: two register tiles per wave (next tile loads while the current one is
 // used; for long key ranges); without DB every wave holds one tile, which
 // leaves room for 8 waves when a split has at most one tile per wave.
-template <int HD, int NW, bool DB>
+// QT query tiles of 16 are held at once (M <= 16 QT): every loaded key tile
+// serves all of them, each with its own running max, sum and output.
+template <int HD, int NW, bool DB, int QT>
 __global__ __launch_bounds__(64 * NW) void k_attn_mfma(AttnArgs a)
 {
     constexpr int NC = HD / 32;  // QK k-steps over dims
@@ -858,7 +860,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mfma(AttnArgs a)
     // split partials (device-coherent 16-byte stores and loads)
     const __amdgpu_buffer_rsrc_t po = __builtin_amdgcn_make_buffer_rsrc(a.part_o, (short)0, 0x7fffffff, 0x00020000);
 
-    __shared__ u32x4 sm_q[NC * 2 * 64];  // [k-step][hi/lo][lane] B operands
+    __shared__ u32x4 sm_q[QT][NC * 2 * 64];  // per query tile: [k-step][hi/lo][lane] B operands
     __shared__ float sm_m[NW][16], sm_l[NW][16];
     __shared__ __align__(16) float sm_o[NW][16][HD + 4];
 
@@ -881,48 +883,70 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mfma(AttnArgs a)
             T.v[dt] = *reinterpret_cast<const u32x4 *>(vc + ((size_t)(k0 >> 5) * HD + dt * 16 + n) * 32 + 8 * g);
     };
 
-    for (int q0 = 0; q0 < M; q0 += 16) {
-        const int tok = q0 + n;
-        const bool tok_ok = tok < M;
-        // thread e < 2*HD converts 8 dims (c, group qg) of query row qt
+    // queries of all tiles into LDS (hi + lo B operands) with the first key
+    // tile's loads in flight
+    Tile buf0;
+    Tile buf1;  // used with DB only
+    if (wave < ntile) load(wave, buf0);
+    uint64_t anc[QT];
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) {
+        const int tok = 16 * qt + n;
+        anc[qt] = tok < M ? a.tm.anc[tok] : 0ull;
+        // thread e < 2*HD converts 8 dims (c, group qg) of query row qr
         const int e = threadIdx.x;
-        const int qt = e / (2 * NC * 2) % 16, qc = (e >> 2) % NC, qg = e & 3;
-        float4 x0 = make_float4(0.f, 0.f, 0.f, 0.f), x1 = x0;
+        const int qr = e / (2 * NC * 2) % 16, qc = (e >> 2) % NC, qg = e & 3;
         if (e < 2 * HD) {
-            const float *qp = a.q + (size_t)min(q0 + qt, M - 1) * D + h * HD + qc * 32 + qg * 8;
-            x0 = *reinterpret_cast<const float4 *>(qp);
-            x1 = *reinterpret_cast<const float4 *>(qp + 4);
-        }
-        const uint64_t anc_raw = a.tm.anc[min(tok, M - 1)];
-        Tile buf0;
-        Tile buf1;  // used with DB only
-        if (wave < ntile) load(wave, buf0);
-        const uint64_t anc = tok_ok ? anc_raw : 0ull;
-        if (e < 2 * HD) {
-            const float qs = q0 + qt < M ? 1.f : 0.f;
-            x0.x *= qs; x0.y *= qs; x0.z *= qs; x0.w *= qs;
-            x1.x *= qs; x1.y *= qs; x1.z *= qs; x1.w *= qs;
+            const int row = 16 * qt + qr;
+            float4 x0 = make_float4(0.f, 0.f, 0.f, 0.f), x1 = x0;
+            if (row < M) {
+                const float *qp = a.q + (size_t)row * D + h * HD + qc * 32 + qg * 8;
+                x0 = *reinterpret_cast<const float4 *>(qp);
+                x1 = *reinterpret_cast<const float4 *>(qp + 4);
+            }
             bf16x8 hh, ll;
             split_hi_lo(x0, x1, hh, ll);
-            sm_q[(qc * 2 + 0) * 64 + 16 * qg + qt] = __builtin_bit_cast(u32x4, hh);
-            sm_q[(qc * 2 + 1) * 64 + 16 * qg + qt] = __builtin_bit_cast(u32x4, ll);
+            sm_q[qt][(qc * 2 + 0) * 64 + 16 * qg + qr] = __builtin_bit_cast(u32x4, hh);
+            sm_q[qt][(qc * 2 + 1) * 64 + 16 * qg + qr] = __builtin_bit_cast(u32x4, ll);
         }
-        __syncthreads();
+    }
+    __syncthreads();
 
-        float m_run = -INFINITY, l_run = 0.f;
-        f32x4 o[ND];
+    float m_run[QT], l_run[QT];
+    f32x4 o[QT][ND];
 #pragma unroll
-        for (int dt = 0; dt < ND; ++dt) o[dt] = (f32x4){0.f, 0.f, 0.f, 0.f};
+    for (int qt = 0; qt < QT; ++qt) {
+        m_run[qt] = -INFINITY;
+        l_run[qt] = 0.f;
+#pragma unroll
+        for (int dt = 0; dt < ND; ++dt) o[qt][dt] = (f32x4){0.f, 0.f, 0.f, 0.f};
+    }
 
-        auto process = [&](int t, Tile &cur) {
-            const int k0 = kbeg + 32 * t;
+    auto process = [&](int t, Tile &cur) {
+        const int k0 = kbeg + 32 * t;
+        if (k0 + 32 > kend) {
+            // ragged last tile: values of slots past the split end are dropped
+#pragma unroll
+            for (int dt = 0; dt < ND; ++dt)
+#pragma unroll
+                for (int w = 0; w < 4; ++w) {
+                    const int key = k0 + 8 * g + 2 * w;
+                    uint32_t x = cur.v[dt][w];
+                    if (key >= kend) x &= 0xffff0000u;
+                    if (key + 1 >= kend) x &= 0x0000ffffu;
+                    cur.v[dt][w] = x;
+                }
+        }
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt) {
+            if (16 * qt >= M) break;
             f32x4 sa = (f32x4){0.f, 0.f, 0.f, 0.f}, sb = sa;
 #pragma unroll
             for (int c = 0; c < NC; ++c) {
                 const bf16x8 ka8 = __builtin_bit_cast(bf16x8, cur.ka[c]);
                 const bf16x8 kb8 = __builtin_bit_cast(bf16x8, cur.kb[c]);
-                const bf16x8 qh = __builtin_bit_cast(bf16x8, sm_q[(c * 2 + 0) * 64 + lane]);
-                const bf16x8 ql = __builtin_bit_cast(bf16x8, sm_q[(c * 2 + 1) * 64 + lane]);
+                const bf16x8 qh = __builtin_bit_cast(bf16x8, sm_q[qt][(c * 2 + 0) * 64 + lane]);
+                const bf16x8 ql = __builtin_bit_cast(bf16x8, sm_q[qt][(c * 2 + 1) * 64 + lane]);
                 sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka8, qh, sa, 0, 0, 0);
                 sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb8, qh, sb, 0, 0, 0);
                 sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka8, ql, sa, 0, 0, 0);
@@ -934,7 +958,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mfma(AttnArgs a)
             for (int i = 0; i < 8; ++i) {
                 const int key = k0 + 8 * g + i;
                 const int sh = key - P;
-                const bool tree_ok = sh < 0 || ((anc >> (sh & 63)) & 1ull);
+                const bool tree_ok = sh < 0 || ((anc[qt] >> (sh & 63)) & 1ull);
                 const bool vis = key < kend && tree_ok;
                 const float sc = (i < 4 ? sa[i] : sb[i - 4]) * scale2;
                 sv[i] = vis ? sc : -INFINITY;
@@ -942,8 +966,8 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mfma(AttnArgs a)
             }
             mt = fmaxf(mt, __shfl_xor(mt, 16));
             mt = fmaxf(mt, __shfl_xor(mt, 32));
-            const float mnew = fmaxf(m_run, mt);
-            const float alpha = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - mnew);
+            const float mnew = fmaxf(m_run[qt], mt);
+            const float alpha = m_run[qt] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run[qt] - mnew);
             float ps = 0.f, pv[8];
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
@@ -952,67 +976,58 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mfma(AttnArgs a)
             }
             ps += __shfl_xor(ps, 16);
             ps += __shfl_xor(ps, 32);
-            l_run = l_run * alpha + ps;
-            m_run = mnew;
-            // O rows held by this lane are tokens 4g + j
+            l_run[qt] = l_run[qt] * alpha + ps;
+            m_run[qt] = mnew;
+            // O rows held by this lane are tokens 4g + j of the tile
             float al[4];
 #pragma unroll
             for (int j = 0; j < 4; ++j) al[j] = __shfl(alpha, 4 * g + j);
-            if (k0 + 32 > kend) {
-                // ragged last tile: values of slots past the split end are dropped
-#pragma unroll
-                for (int dt = 0; dt < ND; ++dt)
-#pragma unroll
-                    for (int w = 0; w < 4; ++w) {
-                        const int key = k0 + 8 * g + 2 * w;
-                        uint32_t x = cur.v[dt][w];
-                        if (key >= kend) x &= 0xffff0000u;
-                        if (key + 1 >= kend) x &= 0x0000ffffu;
-                        cur.v[dt][w] = x;
-                    }
-            }
             bf16x8 ph, pl;
             split_hi_lo(make_float4(pv[0], pv[1], pv[2], pv[3]), make_float4(pv[4], pv[5], pv[6], pv[7]), ph, pl);
 #pragma unroll
             for (int dt = 0; dt < ND; ++dt) {
 #pragma unroll
-                for (int j = 0; j < 4; ++j) o[dt][j] *= al[j];
+                for (int j = 0; j < 4; ++j) o[qt][dt][j] *= al[j];
                 const bf16x8 v8 = __builtin_bit_cast(bf16x8, cur.v[dt]);
-                o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph, v8, o[dt], 0, 0, 0);
-                o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pl, v8, o[dt], 0, 0, 0);
-            }
-        };
-        if (DB) {
-            // two register buffers used in turn (no copies between them, so a
-            // load in flight is never waited on before its tile is used)
-            for (int t = wave; t < ntile; t += 2 * NW) {
-                if (t + NW < ntile) load(t + NW, buf1);
-                process(t, buf0);
-                if (t + NW >= ntile) break;
-                if (t + 2 * NW < ntile) load(t + 2 * NW, buf0);
-                process(t + NW, buf1);
-            }
-        } else {
-            for (int t = wave; t < ntile; t += NW) {
-                if (t != wave) load(t, buf0);
-                process(t, buf0);
+                o[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph, v8, o[qt][dt], 0, 0, 0);
+                o[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pl, v8, o[qt][dt], 0, 0, 0);
             }
         }
+    };
+    if (DB) {
+        // two register buffers used in turn (no copies between them, so a
+        // load in flight is never waited on before its tile is used)
+        for (int t = wave; t < ntile; t += 2 * NW) {
+            if (t + NW < ntile) load(t + NW, buf1);
+            process(t, buf0);
+            if (t + NW >= ntile) break;
+            if (t + 2 * NW < ntile) load(t + 2 * NW, buf0);
+            process(t + NW, buf1);
+        }
+    } else {
+        for (int t = wave; t < ntile; t += NW) {
+            if (t != wave) load(t, buf0);
+            process(t, buf0);
+        }
+    }
 
-        // combine the waves (fixed wave order)
+    // combine the waves (fixed wave order), one query tile at a time
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) {
+        if (16 * qt >= M) break;
         if (g == 0) {
-            sm_m[wave][n] = m_run;
-            sm_l[wave][n] = l_run;
+            sm_m[wave][n] = m_run[qt];
+            sm_l[wave][n] = l_run[qt];
         }
 #pragma unroll
         for (int dt = 0; dt < ND; ++dt)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) sm_o[wave][4 * g + j][dt * 16 + n] = o[dt][j];
+            for (int j = 0; j < 4; ++j) sm_o[wave][4 * g + j][dt * 16 + n] = o[qt][dt][j];
         __syncthreads();
         // 4 consecutive dims of one node per thread
         for (int e4 = threadIdx.x; e4 < 16 * (HD / 4); e4 += 64 * NW) {
             const int i = e4 / (HD / 4), d0 = 4 * (e4 % (HD / 4));
-            const int ti = q0 + i;
+            const int ti = 16 * qt + i;
             float mx = -INFINITY;
 #pragma unroll
             for (int w = 0; w < NW; ++w) mx = fmaxf(mx, sm_m[w][i]);
@@ -2183,14 +2198,28 @@ hipError_t launch_attention(const AttnArgs &a, int kv_bf16, hipStream_t s)
     // splits: 4 waves with two tiles in flight each
     const bool short_split = a.keys_per_split <= 8 * DV_ATTN_TILE;
     const dim3 b8(512), b4(256);
+    // more than 16 nodes: every key tile serves all query tiles (4 waves, one
+    // tile in flight each, so that the per-tile outputs fit the registers)
+    const int qt = a.tm.Mpad / 16;
+    if (qt < 1 || qt > 4) return hipErrorInvalidValue;
+    if (!kv_bf16) {
+        if (a.hd == 128) hipLaunchKernelGGL(k_attn_f32<128>, grid, block, 0, s, a);
+        else if (a.hd == 64) hipLaunchKernelGGL(k_attn_f32<64>, grid, block, 0, s, a);
+        else return hipErrorInvalidValue;
+        return hipGetLastError();
+    }
     if (a.hd == 128) {
-        if (!kv_bf16) hipLaunchKernelGGL(k_attn_f32<128>, grid, block, 0, s, a);
-        else if (short_split) hipLaunchKernelGGL((k_attn_mfma<128, 8, false>), grid, b8, 0, s, a);
-        else hipLaunchKernelGGL((k_attn_mfma<128, 4, true>), grid, b4, 0, s, a);
+        if (qt == 1 && short_split) hipLaunchKernelGGL((k_attn_mfma<128, 8, false, 1>), grid, b8, 0, s, a);
+        else if (qt == 1) hipLaunchKernelGGL((k_attn_mfma<128, 4, true, 1>), grid, b4, 0, s, a);
+        else if (qt == 2) hipLaunchKernelGGL((k_attn_mfma<128, 4, false, 2>), grid, b4, 0, s, a);
+        else if (qt == 3) hipLaunchKernelGGL((k_attn_mfma<128, 4, false, 3>), grid, b4, 0, s, a);
+        else hipLaunchKernelGGL((k_attn_mfma<128, 4, false, 4>), grid, b4, 0, s, a);
     } else if (a.hd == 64) {
-        if (!kv_bf16) hipLaunchKernelGGL(k_attn_f32<64>, grid, block, 0, s, a);
-        else if (short_split) hipLaunchKernelGGL((k_attn_mfma<64, 8, false>), grid, b8, 0, s, a);
-        else hipLaunchKernelGGL((k_attn_mfma<64, 4, true>), grid, b4, 0, s, a);
+        if (qt == 1 && short_split) hipLaunchKernelGGL((k_attn_mfma<64, 8, false, 1>), grid, b8, 0, s, a);
+        else if (qt == 1) hipLaunchKernelGGL((k_attn_mfma<64, 4, true, 1>), grid, b4, 0, s, a);
+        else if (qt == 2) hipLaunchKernelGGL((k_attn_mfma<64, 4, false, 2>), grid, b4, 0, s, a);
+        else if (qt == 3) hipLaunchKernelGGL((k_attn_mfma<64, 4, false, 3>), grid, b4, 0, s, a);
+        else hipLaunchKernelGGL((k_attn_mfma<64, 4, false, 4>), grid, b4, 0, s, a);
     } else {
         return hipErrorInvalidValue;
     }
