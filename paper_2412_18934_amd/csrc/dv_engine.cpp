@@ -56,6 +56,8 @@ struct dv_handle {
     int ssq_max = 0;
     float *part_gemm = nullptr;  // split-K partials of the residual projections
     uint32_t *cnt = nullptr;     // their per-row-group arrival counters
+    size_t part_elems = 0;       // floats in part_gemm
+    int cnt_n = 0;               // counters in cnt
     uint16_t *u_s = nullptr, *attn_s = nullptr, *h_s = nullptr;  // split-layout activations
     float *part_o = nullptr, *part_m = nullptr, *part_l = nullptr;
     uint32_t *attn_cnt = nullptr;  // per-head arrivals of the attention splits
@@ -78,6 +80,10 @@ struct dv_handle {
     // draft side
     bool draft = false;
     const void *dgf_h = nullptr, *dgf_e = nullptr, *dgf_g = nullptr;  // W_h, W_e [d][d], W_g [d][2d]
+    GemmPlan p_dgf_d, p_dgf_g;    // projections of W_h / W_e (K = d) and W_g (K = 2 d)
+    uint16_t *pk_dh = nullptr, *pk_de = nullptr, *pk_dg = nullptr;  // their MFMA block order
+    uint16_t *dgf_xf = nullptr, *dgf_xe = nullptr, *dgf_xg = nullptr;  // split-layout operands
+    float *dgf_h1 = nullptr, *dgf_h2 = nullptr, *dgf_z = nullptr;       // [64][d] outputs
     const float *x_in = nullptr;  // stack input rows for the next forward (null: embeddings)
     float *feat_a = nullptr, *feat_b = nullptr;  // [DV_TREE_MAX + 1][d] draft features (row 64: the root's input)
     int32_t *tk_tok = nullptr, *tk_tok_h = nullptr;
@@ -573,29 +579,46 @@ int draft_forward_impl(dv_handle *h, const int32_t *tokens, const int32_t *paren
     hipStream_t s = h->stream;
     int rc = pf_reserve(h, std::max(n, 1));
     if (rc) return rc;
-    auto gemm = [&](const void *w, int m, int rows, int k, const uint16_t *B, float *D) -> int {
-        prof_begin(h, DV_K_GEMM);
-        const int r = blas_gemm_tn(h->blas, m, rows, k, static_cast<const uint16_t *>(w), B, k, D, s);
-        prof_end(h);
-        return r ? set_err(h, DV_EHIP, "hipBLASLt GEMM %dx%dx%d failed", m, rows, k) : DV_OK;
+    // gated fusion on the weight-streaming projections: h1 = W_h f, h2 = W_e e,
+    // z = W_g [h1 || h2], x0 = sigmoid(z) h1 + (1 - sigmoid(z)) h2
+    const int Mpad = round_up(n, 16);
+    auto gemm = [&](const GemmPlan &p, const uint16_t *pk, int K, const uint16_t *xs, float *D) -> int {
+        GemmArgs a{};
+        a.packed = pk;
+        a.xs = xs;
+        a.N = d;
+        a.K = K;
+        a.n_tiles = p.n_tiles;
+        a.rb = p.rb;
+        a.n_groups = p.n_groups;
+        a.ks = p.ks;
+        a.n_units = gemm_units(p);
+        a.M = n;
+        a.Mpad = Mpad;
+        a.out = D;
+        a.part = h->part_gemm;
+        a.cnt = h->cnt;
+        const int grid = gemm_grid(p, EPI_PLAIN, W_BF16, Mpad / 16, h->n_cu);
+        ProfEv *ev = prof_pair(h, DV_K_GEMM);
+        hipError_t e = launch_gemm(a, grid, EPI_PLAIN, W_BF16, 1, s, ev ? ev->a : nullptr, ev ? ev->b : nullptr);
+        return e == hipSuccess ? DV_OK : hip_fail(h, e, "DGF projection launch");
     };
     DgfTokens t{};
     for (int i = 0; i < n; ++i) t.tok[i] = tokens[i];
-    // operands: pf_xs holds the feature hi/lo rows [2n][d] and then the
-    // [h1 || h2] rows [2n][2d]; the embedding rows go after the first
-    uint16_t *bf = h->pf_xs, *be = h->pf_xs + (size_t)2 * n * d;
     prof_begin(h, DV_K_OTHER);
-    hipError_t e = launch_dgf_prep(feat_in, h->embed, t, n, d, bf, be, s);
+    hipError_t e = launch_dgf_in(feat_in, h->embed, t, n, Mpad, d, h->dgf_xf, h->dgf_xe, s);
     prof_end(h);
-    if (e != hipSuccess) return hip_fail(h, e, "dgf prep");
-    if ((rc = gemm(h->dgf_h, d, 2 * n, d, bf, h->pf_D0)) || (rc = gemm(h->dgf_e, d, n, d, be, h->pf_D1))) return rc;
+    if (e != hipSuccess) return hip_fail(h, e, "dgf operands");
+    if ((rc = gemm(h->p_dgf_d, h->pk_dh, d, h->dgf_xf, h->dgf_h1)) ||
+        (rc = gemm(h->p_dgf_d, h->pk_de, d, h->dgf_xe, h->dgf_h2)))
+        return rc;
     prof_begin(h, DV_K_OTHER);
-    e = launch_dgf_mid(h->pf_D0, h->pf_D1, n, d, h->pf_xs, s);
+    e = launch_dgf_gate_in(h->dgf_h1, h->dgf_h2, n, Mpad, d, h->dgf_xg, s);
     prof_end(h);
     if (e != hipSuccess) return hip_fail(h, e, "dgf gate input");
-    if ((rc = gemm(h->dgf_g, d, 2 * n, 2 * d, h->pf_xs, h->pf_D2))) return rc;
+    if ((rc = gemm(h->p_dgf_g, h->pk_dg, 2 * d, h->dgf_xg, h->dgf_z))) return rc;
     prof_begin(h, DV_K_OTHER);
-    e = launch_dgf_out(h->pf_D2, h->pf_D0, h->pf_D1, n, d, h->pf_x, s);
+    e = launch_dgf_mix(h->dgf_z, h->dgf_h1, h->dgf_h2, n, d, h->pf_x, s);
     prof_end(h);
     if (e != hipSuccess) return hip_fail(h, e, "dgf output");
     fill_desc(h->h_sd, tokens, parents, n, kv->len, pos, depth, anc);
@@ -739,6 +762,8 @@ int dv_verify_init(const dv_config *cfg, const dv_weights *w, void *stream, dv_h
             cnt_n = std::max(cnt_n, p->n_groups);
         }
     h->ssq_max = std::max({DV_NORM_SLICES, h->p_o.n_groups, h->p_down.n_groups});
+    h->part_elems = part_elems;
+    h->cnt_n = cnt_n;
     h->attn_split_max = std::max(ceil_div(c.max_ctx, DV_ATTN_SPLIT_KEYS), ceil_div(512, H));
     // the split-K and attention partials are addressed with 32-bit byte offsets
     if ((double)part_elems * 4 >= 2147483648.0) {
@@ -980,6 +1005,57 @@ int dv_draft_init(const dv_config *cfg, const dv_weights *w, const dv_dgf_weight
     h->dgf_h = dgf->w_hidden;
     h->dgf_e = dgf->w_embed;
     h->dgf_g = dgf->w_gate;
+    // the gated fusion's matrices in MFMA block order, split over K like the
+    // residual projections (d_model output rows)
+    const int d = cfg->d_model;
+    h->p_dgf_d = make_plan(d / DV_GEMM_TILE, d, 1, true, h->n_cu);
+    h->p_dgf_g = make_plan(d / DV_GEMM_TILE, 2 * d, 1, true, h->n_cu);
+    size_t need = h->part_elems;
+    int need_cnt = h->cnt_n;
+    for (const GemmPlan *p : {&h->p_dgf_d, &h->p_dgf_g})
+        if (p->ks > 1) {
+            need = std::max(need, (size_t)gemm_units(*p) * p->rb * 4 * 64 * 4);
+            need_cnt = std::max(need_cnt, p->n_groups);
+        }
+    auto zalloc = [](void **p, size_t bytes) -> bool {
+        return hipMalloc(p, bytes) == hipSuccess && hipMemset(*p, 0, bytes) == hipSuccess;
+    };
+    bool okd = true;
+    if (need > h->part_elems) {
+        (void)hipFree(h->part_gemm);
+        h->part_gemm = nullptr;
+        okd = zalloc((void **)&h->part_gemm, need * 4);
+        h->part_elems = okd ? need : 0;
+    }
+    if (okd && need_cnt > h->cnt_n) {
+        (void)hipFree(h->cnt);
+        h->cnt = nullptr;
+        okd = zalloc((void **)&h->cnt, (size_t)need_cnt * 4);
+        h->cnt_n = okd ? need_cnt : 0;
+    }
+    auto pack = [&](const GemmPlan &p, const void *w, int K, uint16_t **dst) -> bool {
+        if (hipMalloc((void **)dst, (size_t)p.n_tiles * DV_GEMM_TILE * K * 2) != hipSuccess) return false;
+        GemmArgs a{};
+        a.w0 = w;
+        a.N = d;
+        a.K = K;
+        a.n_tiles = p.n_tiles;
+        a.rb = p.rb;
+        a.n_groups = p.n_groups;
+        return launch_pack(a, EPI_PLAIN, W_BF16, *dst, nullptr) == hipSuccess;
+    };
+    okd = okd && h->p_dgf_d.mfma && h->p_dgf_g.mfma && pack(h->p_dgf_d, h->dgf_h, d, &h->pk_dh) &&
+          pack(h->p_dgf_d, h->dgf_e, d, &h->pk_de) && pack(h->p_dgf_g, h->dgf_g, 2 * d, &h->pk_dg) &&
+          zalloc((void **)&h->dgf_xf, (size_t)d * 2 * DV_TREE_MAX * 2) &&
+          zalloc((void **)&h->dgf_xe, (size_t)d * 2 * DV_TREE_MAX * 2) &&
+          zalloc((void **)&h->dgf_xg, (size_t)2 * d * 2 * DV_TREE_MAX * 2) &&
+          zalloc((void **)&h->dgf_h1, (size_t)DV_TREE_MAX * d * 4) &&
+          zalloc((void **)&h->dgf_h2, (size_t)DV_TREE_MAX * d * 4) &&
+          zalloc((void **)&h->dgf_z, (size_t)DV_TREE_MAX * d * 4) && hipDeviceSynchronize() == hipSuccess;
+    if (!okd) {
+        dv_verify_free(h);
+        return set_err(nullptr, DV_ENOMEM, "draft gated-fusion workspace allocation failed");
+    }
     const size_t fb = (size_t)(DV_TREE_MAX + 1) * cfg->d_model * sizeof(float);
     bool ok = hipMalloc((void **)&h->feat_a, fb) == hipSuccess && hipMalloc((void **)&h->feat_b, fb) == hipSuccess &&
               hipMalloc((void **)&h->tk_tok, DV_TREE_MAX * DV_TOPK_MAX * 4) == hipSuccess &&
@@ -1229,7 +1305,9 @@ void dv_verify_free(dv_handle *h)
             if (p) (void)hipFree(p);
     if (h->pk_lm) (void)hipFree(h->pk_lm);
     if (h->ps_lm) (void)hipFree(h->ps_lm);
-    for (void *p : {(void *)h->feat_a, (void *)h->feat_b, (void *)h->tk_tok, (void *)h->tk_p})
+    for (void *p : {(void *)h->feat_a, (void *)h->feat_b, (void *)h->tk_tok, (void *)h->tk_p, (void *)h->pk_dh,
+                    (void *)h->pk_de, (void *)h->pk_dg, (void *)h->dgf_xf, (void *)h->dgf_xe, (void *)h->dgf_xg,
+                    (void *)h->dgf_h1, (void *)h->dgf_h2, (void *)h->dgf_z})
         if (p) (void)hipFree(p);
     if (h->tk_tok_h) (void)hipHostFree(h->tk_tok_h);
     if (h->tk_p_h) (void)hipHostFree(h->tk_p_h);

@@ -40,7 +40,9 @@ struct DevAccept {
     int32_t argmax[DV_TREE_MAX];
 };
 
-enum GemmEpi { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LOGITS = 3 };
+// EPI_PLAIN: the sums themselves, out [M][N] fp32 (no input norm; the draft's
+// gated fusion)
+enum GemmEpi { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LOGITS = 3, EPI_PLAIN = 4 };
 
 // "Split layout" of an activation matrix [Mpad][K] (Mpad = 16 MT) for the
 // MFMA projections: each fp32 value v is stored as bf16 hi = v truncated and
@@ -221,10 +223,13 @@ struct TopkArgs {
     int32_t *out_tok;           // [rows][DV_TOPK_MAX]
     float *out_p;               // [rows][DV_TOPK_MAX]
 };
-hipError_t launch_dgf_prep(const float *feat, const void *embed, const DgfTokens &t, int n, int d, uint16_t *bf,
-                           uint16_t *be, hipStream_t s);
-hipError_t launch_dgf_mid(float *D1, const float *D2, int n, int d, uint16_t *bc, hipStream_t s);
-hipError_t launch_dgf_out(const float *D3, const float *h1, const float *h2, int n, int d, float *x0, hipStream_t s);
+// DGF: the n feature rows and token embeddings as split-layout operands of
+// K = d (rows n..Mpad zero); the gate input [h1 || h2] (K = 2 d); the mix
+// x0 = g h1 + (1 - g) h2 with g = sigmoid(z)
+hipError_t launch_dgf_in(const float *feat, const void *embed, const DgfTokens &t, int n, int Mpad, int d,
+                         uint16_t *xf, uint16_t *xe, hipStream_t s);
+hipError_t launch_dgf_gate_in(const float *h1, const float *h2, int n, int Mpad, int d, uint16_t *xg, hipStream_t s);
+hipError_t launch_dgf_mix(const float *z, const float *h1, const float *h2, int n, int d, float *x0, hipStream_t s);
 hipError_t launch_gather_rows(const float *src, const RowIndex &ix, int n, int d, float *dst, hipStream_t s);
 hipError_t launch_topk_probs(const float *logits, int V, const TopkArgs &a, int n_rows, hipStream_t s);
 

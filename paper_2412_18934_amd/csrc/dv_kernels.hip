@@ -353,6 +353,18 @@ __device__ void logits_epilogue(const GemmArgs &a, const float *Y, int ld, int r
     }
 }
 
+// PLAIN: rows [row0, row0 + nrows) of every token, 4 consecutive rows per
+// thread.
+__device__ void plain_epilogue(const GemmArgs &a, const float *Y, int ld, int row0, int nrows)
+{
+    const int nc = nrows >> 2;
+    for (int e = threadIdx.x; e < a.M * nc; e += blockDim.x) {
+        const int m = e / nc, r = 4 * (e - m * nc);
+        const float *y = Y + m * ld + r;
+        *reinterpret_cast<float4 *>(a.out + (size_t)m * a.N + row0 + r) = make_float4(y[0], y[1], y[2], y[3]);
+    }
+}
+
 // ---------------------------------------------------------------------------
 // MFMA projection for bf16 weights (block layout) and split-layout
 // activations.
@@ -538,7 +550,7 @@ __global__ __launch_bounds__(64 * NW) void k_proj(GemmArgs a)
                     rs[b] = *reinterpret_cast<const f32x4 *>(a.scale + (g * RB + b) * 16 + 4 * (lane >> 4));
             }
             stage(g);
-            if (EPI != EPI_RESID && !have_rinv) {
+            if (EPI != EPI_RESID && EPI != EPI_PLAIN && !have_rinv) {
                 // the first unit's loads are in flight; the norm scalars of
                 // the input arrive meanwhile
                 input_rinv(a, rinv);
@@ -564,7 +576,7 @@ __global__ __launch_bounds__(64 * NW) void k_proj(GemmArgs a)
             }
         } else {
             stage(g);
-            if (EPI != EPI_RESID && !have_rinv) {
+            if (EPI != EPI_RESID && EPI != EPI_PLAIN && !have_rinv) {
                 input_rinv(a, rinv);
                 have_rinv = true;
             }
@@ -588,7 +600,7 @@ __global__ __launch_bounds__(64 * NW) void k_proj(GemmArgs a)
             }
         }
         bool mine = true;
-        if (EPI == EPI_RESID && KS > 1) {
+        if (KS > 1) {
             // publish this split's partial (16-byte stores written through to
             // the device-coherent level, cache policy sc1); the last arriver
             // folds them
@@ -644,6 +656,8 @@ __global__ __launch_bounds__(64 * NW) void k_proj(GemmArgs a)
                 resid_epilogue<uint16_t>(a, Y, LD, g * ROWS, ROWS, g, true, stage_s);
             } else if (EPI == EPI_LOGITS) {
                 logits_epilogue(a, Y, LD, g * ROWS, ROWS, g, rinv);
+            } else if (EPI == EPI_PLAIN) {
+                plain_epilogue(a, Y, LD, g * ROWS, ROWS);
             } else if (EPI == EPI_SWIGLU) {
                 swiglu_epilogue(a, Y, LD, g * (RB / 2), RB / 2, rinv);
             } else {
@@ -1924,41 +1938,50 @@ __global__ __launch_bounds__(1024) void k_pf_argmax(const float *Dz, int V, DevA
 //   prep: parent features -> hi/lo rows; token embeddings -> bf16 rows
 //   mid:  h1 = W_h f (two halves), h2 = W_e e -> hi/lo rows of [h1 || h2]
 //   out:  g = sigmoid(W_g [h1 || h2]); x0 = g h1 + (1 - g) h2
-__global__ __launch_bounds__(PF_THREADS) void k_dgf_prep(const float *feat, const uint16_t *embed, DgfTokens t,
-                                                         int n, int d, uint16_t *bf, uint16_t *be)
+// DGF operands in split layout (the projection kernel's B operand), one
+// workgroup per token row m < Mpad: feature rows and the token embeddings
+// (bf16, so exact: lo = 0); rows n..Mpad are zero.
+__global__ __launch_bounds__(PF_THREADS) void k_dgf_in(const float *feat, const uint16_t *embed, DgfTokens t, int n,
+                                                       int d, int MT, uint16_t *xf, uint16_t *xe)
 {
-    const int i = blockIdx.x;
+    const int m = blockIdx.x;
     for (int k = 4 * threadIdx.x; k < d; k += 4 * PF_THREADS) {
-        store_hilo4(bf, (size_t)i * d + k, (size_t)(n + i) * d + k,
-                    *reinterpret_cast<const float4 *>(feat + (size_t)i * d + k));
-        *reinterpret_cast<uint2 *>(be + (size_t)i * d + k) =
-            *reinterpret_cast<const uint2 *>(embed + (size_t)t.tok[i] * d + k);
+        float4 f = make_float4(0.f, 0.f, 0.f, 0.f), e = f;
+        if (m < n) {
+            f = *reinterpret_cast<const float4 *>(feat + (size_t)m * d + k);
+            const uint2 eb = *reinterpret_cast<const uint2 *>(embed + (size_t)t.tok[m] * d + k);
+            e = make_float4(bf2f(eb.x & 0xffffu), bf2f(eb.x >> 16), bf2f(eb.y & 0xffffu), bf2f(eb.y >> 16));
+        }
+        store_split4(xf, m, k, MT, f);
+        store_split4(xe, m, k, MT, e);
     }
 }
 
-__global__ __launch_bounds__(PF_THREADS) void k_dgf_mid(float *D1, const float *D2, int n, int d, uint16_t *bc)
+// gate input [h1 || h2] (K = 2 d) in split layout
+__global__ __launch_bounds__(PF_THREADS) void k_dgf_gate_in(const float *h1, const float *h2, int n, int d, int MT,
+                                                            uint16_t *xg)
 {
-    const int i = blockIdx.x;
+    const int m = blockIdx.x;
     for (int k = 4 * threadIdx.x; k < d; k += 4 * PF_THREADS) {
-        const float4 a = *reinterpret_cast<const float4 *>(D1 + (size_t)i * d + k);
-        const float4 b = *reinterpret_cast<const float4 *>(D1 + (size_t)(n + i) * d + k);
-        const float4 h1 = make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
-        *reinterpret_cast<float4 *>(D1 + (size_t)i * d + k) = h1;
-        const float4 h2 = *reinterpret_cast<const float4 *>(D2 + (size_t)i * d + k);
-        store_hilo4(bc, (size_t)i * 2 * d + k, (size_t)(n + i) * 2 * d + k, h1);
-        store_hilo4(bc, (size_t)i * 2 * d + d + k, (size_t)(n + i) * 2 * d + d + k, h2);
+        float4 a = make_float4(0.f, 0.f, 0.f, 0.f), b = a;
+        if (m < n) {
+            a = *reinterpret_cast<const float4 *>(h1 + (size_t)m * d + k);
+            b = *reinterpret_cast<const float4 *>(h2 + (size_t)m * d + k);
+        }
+        store_split4(xg, m, k, MT, a);
+        store_split4(xg, m, d + k, MT, b);
     }
 }
 
-__global__ __launch_bounds__(PF_THREADS) void k_dgf_out(const float *D3, const float *h1, const float *h2, int n,
-                                                        int d, float *x0)
+// x0 = g h1 + (1 - g) h2, g = sigmoid(z)
+__global__ __launch_bounds__(PF_THREADS) void k_dgf_mix(const float *z, const float *h1, const float *h2, int d,
+                                                        float *x0)
 {
     const int i = blockIdx.x;
     for (int k = threadIdx.x; k < d; k += PF_THREADS) {
-        const float z = D3[(size_t)i * d + k] + D3[(size_t)(n + i) * d + k];
-        const float g = 1.f / (1.f + expf(-z));
-        const float a = h1[(size_t)i * d + k], b = h2[(size_t)i * d + k];
-        x0[(size_t)i * d + k] = g * a + (1.f - g) * b;
+        const size_t o = (size_t)i * d + k;
+        const float g = 1.f / (1.f + expf(-z[o]));
+        x0[o] = g * h1[o] + (1.f - g) * h2[o];
     }
 }
 
@@ -2092,15 +2115,22 @@ static const void *proj_kernel_mt(int mt)
 template <int EPI>
 static const void *gemm_kernel(int wkind, int use_mfma, int mt, int rb)
 {
-    if (wkind != W_F32 && use_mfma) {
-        const bool q8 = wkind == W_I8;
-        if (rb == 4) return q8 ? proj_kernel_mt<EPI, uint16_t, 4, true>(mt) : proj_kernel_mt<EPI, uint16_t, 4, false>(mt);
-        if (rb == 2) return q8 ? proj_kernel_mt<EPI, uint16_t, 2, true>(mt) : proj_kernel_mt<EPI, uint16_t, 2, false>(mt);
+    if constexpr (EPI == EPI_PLAIN) {  // bf16 weights, MFMA path only
+        if (wkind != W_BF16 || !use_mfma) return nullptr;
+        if (rb == 4) return proj_kernel_mt<EPI, uint16_t, 4, false>(mt);
+        if (rb == 2) return proj_kernel_mt<EPI, uint16_t, 2, false>(mt);
         return nullptr;
+    } else {
+        if (wkind != W_F32 && use_mfma) {
+            const bool q8 = wkind == W_I8;
+            if (rb == 4) return q8 ? proj_kernel_mt<EPI, uint16_t, 4, true>(mt) : proj_kernel_mt<EPI, uint16_t, 4, false>(mt);
+            if (rb == 2) return q8 ? proj_kernel_mt<EPI, uint16_t, 2, true>(mt) : proj_kernel_mt<EPI, uint16_t, 2, false>(mt);
+            return nullptr;
+        }
+        if (wkind == W_BF16) return (const void *)k_gemm_valu<uint16_t, EPI, uint16_t>;
+        if (wkind == W_F32) return (const void *)k_gemm_valu<float, EPI, float>;
+        return nullptr;  // int8 weights have no VALU kernel
     }
-    if (wkind == W_BF16) return (const void *)k_gemm_valu<uint16_t, EPI, uint16_t>;
-    if (wkind == W_F32) return (const void *)k_gemm_valu<float, EPI, float>;
-    return nullptr;  // int8 weights have no VALU kernel
 }
 
 static const void *gemm_kernel_any(int epi, int wkind, int use_mfma, int mt, int rb)
@@ -2110,6 +2140,7 @@ static const void *gemm_kernel_any(int epi, int wkind, int use_mfma, int mt, int
     case EPI_RESID: return gemm_kernel<EPI_RESID>(wkind, use_mfma, mt, rb);
     case EPI_SWIGLU: return gemm_kernel<EPI_SWIGLU>(wkind, use_mfma, mt, rb);
     case EPI_LOGITS: return gemm_kernel<EPI_LOGITS>(wkind, use_mfma, mt, rb);
+    case EPI_PLAIN: return gemm_kernel<EPI_PLAIN>(wkind, use_mfma, mt, rb);
     }
     return nullptr;
 }
@@ -2121,9 +2152,9 @@ static int gemm_threads(int wkind, int use_mfma, int rb)
 
 int gemm_blocks_per_cu(int epi, int wkind, int use_mfma, int mt, int rb)
 {
-    static int cache[4][3][2][5][2];
-    if (wkind < 0 || wkind > 2) return 1;
-    int &c = cache[epi & 3][wkind][use_mfma ? 1 : 0][(mt >= 1 && mt <= 4) ? mt : 0][rb == 4];
+    static int cache[5][3][2][5][2];
+    if (wkind < 0 || wkind > 2 || epi < 0 || epi > 4) return 1;
+    int &c = cache[epi][wkind][use_mfma ? 1 : 0][(mt >= 1 && mt <= 4) ? mt : 0][rb == 4];
     if (c == 0) {
         const void *k = gemm_kernel_any(epi, wkind, use_mfma, mt, rb);
         int n = 0;
@@ -2301,24 +2332,26 @@ hipError_t launch_pf_argmax(const float *Dz, int V, DevAccept *acc, hipStream_t 
     return hipGetLastError();
 }
 
-hipError_t launch_dgf_prep(const float *feat, const void *embed, const DgfTokens &t, int n, int d, uint16_t *bf,
-                           uint16_t *be, hipStream_t s)
+hipError_t launch_dgf_in(const float *feat, const void *embed, const DgfTokens &t, int n, int Mpad, int d,
+                         uint16_t *xf, uint16_t *xe, hipStream_t s)
 {
-    if (n < 1 || n > DV_TREE_MAX || d % 4) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_dgf_prep, dim3(n), dim3(PF_THREADS), 0, s, feat, static_cast<const uint16_t *>(embed), t, n, d,
-                       bf, be);
+    if (n < 1 || n > Mpad || Mpad > DV_TREE_MAX || Mpad % 16 || d % 32) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_dgf_in, dim3(Mpad), dim3(PF_THREADS), 0, s, feat, static_cast<const uint16_t *>(embed), t, n, d,
+                       Mpad / 16, xf, xe);
     return hipGetLastError();
 }
 
-hipError_t launch_dgf_mid(float *D1, const float *D2, int n, int d, uint16_t *bc, hipStream_t s)
+hipError_t launch_dgf_gate_in(const float *h1, const float *h2, int n, int Mpad, int d, uint16_t *xg, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_dgf_mid, dim3(n), dim3(PF_THREADS), 0, s, D1, D2, n, d, bc);
+    if (n < 1 || n > Mpad || Mpad > DV_TREE_MAX || Mpad % 16 || d % 32) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_dgf_gate_in, dim3(Mpad), dim3(PF_THREADS), 0, s, h1, h2, n, d, Mpad / 16, xg);
     return hipGetLastError();
 }
 
-hipError_t launch_dgf_out(const float *D3, const float *h1, const float *h2, int n, int d, float *x0, hipStream_t s)
+hipError_t launch_dgf_mix(const float *z, const float *h1, const float *h2, int n, int d, float *x0, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_dgf_out, dim3(n), dim3(PF_THREADS), 0, s, D3, h1, h2, n, d, x0);
+    if (n < 1 || n > DV_TREE_MAX) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_dgf_mix, dim3(n), dim3(PF_THREADS), 0, s, z, h1, h2, d, x0);
     return hipGetLastError();
 }
 
