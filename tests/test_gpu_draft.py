@@ -33,8 +33,8 @@ TARGET = dict(n_layers=2, d_model=256, n_heads=2, head_dim=128, d_ffn=512, vocab
 class DraftCase:
     """A draft of n_blocks blocks sharing the target's embedding and lm_head."""
 
-    def __init__(self, n_blocks, seed, capacity=128):
-        tcfg = small_cfg(**TARGET)
+    def __init__(self, n_blocks, seed, capacity=128, target=TARGET):
+        tcfg = small_cfg(**target)
         self.cfg = synth.draft_cfg(tcfg, n_blocks)
         tw = Weights(tcfg, seed)                 # the target's embedding / lm_head
         self.w = Weights(self.cfg, seed + 1)     # the draft's blocks
@@ -87,6 +87,33 @@ def test_draft_forward_matches_oracle(draft2, m):
     fo = f_out.cpu().numpy()
     rms = np.sqrt(np.mean(hidden ** 2))
     assert float(np.abs(fo - hidden).max()) <= 5e-3 * rms
+
+
+def test_draft_forward_split_k_fusion():
+    """d_model 1024: the gated fusion's projections split K (2 splits for W_h and
+    W_e, 4 for W_g) and the last split of each row group folds them."""
+    wide = dict(n_layers=2, d_model=1024, n_heads=8, head_dim=128, d_ffn=2816, vocab=4096,
+                weight_dtype="bf16", init_std=0.05)
+    c = DraftCase(1, 305, target=wide)
+    try:
+        kv, kv_o = c.kv(306, 33)
+        for m in (5, 19):
+            toks, par = synth.random_tree(307 + m, m, 4, c.cfg.vocab)
+            feat = synth.features(308 + m, m, c.cfg.d_model)
+            f_in = torch.from_numpy(feat).to("cuda:0")
+            f_out = torch.full((m, c.cfg.d_model), float("nan"), device="cuda:0")
+            lg = torch.full((m, c.cfg.vocab), float("nan"), device="cuda:0")
+            dv.dv_draft_forward(c.h, toks, par, kv.c, f_in.data_ptr(), f_out.data_ptr(), lg.data_ptr())
+            logits, hidden = c.om.forward(kv_o, toks, par, feat)
+            assert float(np.abs(lg.cpu().numpy() - logits).max()) <= 2e-2
+            rms = np.sqrt(np.mean(hidden ** 2))
+            assert float(np.abs(f_out.cpu().numpy() - hidden).max()) <= 5e-3 * rms
+            # the same pass again: bitwise reproducible
+            f2 = torch.full_like(f_out, float("nan"))
+            dv.dv_draft_forward(c.h, toks, par, kv.c, f_in.data_ptr(), f2.data_ptr(), lg.data_ptr())
+            assert torch.equal(f_out, f2)
+    finally:
+        c.close()
 
 
 def _clear(trace, rel=1e-2):
