@@ -292,8 +292,8 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1:
-        print("bench.py measures one GPU only: the verification step is not split across "
-              "GPUs in this build (requested --gpus %d)" % args.gpus, file=sys.stderr)
+        print("bench.py measures one GPU only: the verification step runs on a single GPU "
+              "and is not split across several (requested --gpus %d)" % args.gpus, file=sys.stderr)
         sys.exit(2)
 
     if args.workload.startswith("sweep-"):
