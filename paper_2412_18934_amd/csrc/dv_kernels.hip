@@ -2098,16 +2098,21 @@ __global__ __launch_bounds__(256) void k_kv_commit(CommitArgs a)
 
 GemmShape gemm_shape(int rb) { return rb == 4 ? GemmShape{4, 2} : GemmShape{4, 4}; }
 
-// more token tiles hold more accumulators and operands: fewer steps in flight
+// Waves per workgroup of the MFMA projection.  More than one token tile
+// holds more accumulators and operands per wave, so each wave keeps fewer
+// steps in flight; with bf16 weights 8 waves (two per SIMD) then keep the
+// loads coming (int8 weights: 4, their dequantisation registers would spill).
+static int proj_waves(int wkind, int mt, int rb) { return mt >= 2 && wkind == W_BF16 ? 8 : gemm_shape(rb).nw; }
+
 template <int EPI, typename KV, int RB, bool Q8>
 static const void *proj_kernel_mt(int mt)
 {
-    constexpr int U1 = RB == 4 ? 2 : 4;
+    constexpr int U1 = RB == 4 ? 2 : 4, NWM = Q8 ? 4 : 8;
     switch (mt) {
     case 1: return (const void *)k_proj<1, EPI, KV, 4, U1, RB, Q8>;
-    case 2: return (const void *)k_proj<2, EPI, KV, 4, 2, RB, Q8>;
-    case 3: return (const void *)k_proj<3, EPI, KV, 4, 2, RB, Q8>;
-    case 4: return (const void *)k_proj<4, EPI, KV, 4, 2, RB, Q8>;
+    case 2: return (const void *)k_proj<2, EPI, KV, NWM, 2, RB, Q8>;
+    case 3: return (const void *)k_proj<3, EPI, KV, NWM, 2, RB, Q8>;
+    case 4: return (const void *)k_proj<4, EPI, KV, NWM, 2, RB, Q8>;
     default: return nullptr;
     }
 }
@@ -2145,9 +2150,9 @@ static const void *gemm_kernel_any(int epi, int wkind, int use_mfma, int mt, int
     return nullptr;
 }
 
-static int gemm_threads(int wkind, int use_mfma, int rb)
+static int gemm_threads(int wkind, int use_mfma, int mt, int rb)
 {
-    return (wkind != W_F32 && use_mfma) ? 64 * gemm_shape(rb).nw : 256;
+    return (wkind != W_F32 && use_mfma) ? 64 * proj_waves(wkind, mt, rb) : 256;
 }
 
 int gemm_blocks_per_cu(int epi, int wkind, int use_mfma, int mt, int rb)
@@ -2158,7 +2163,7 @@ int gemm_blocks_per_cu(int epi, int wkind, int use_mfma, int mt, int rb)
     if (c == 0) {
         const void *k = gemm_kernel_any(epi, wkind, use_mfma, mt, rb);
         int n = 0;
-        if (!k || hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k, gemm_threads(wkind, use_mfma, rb), 0) !=
+        if (!k || hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k, gemm_threads(wkind, use_mfma, mt, rb), 0) !=
                       hipSuccess || n < 1)
             n = 1;
         c = n;
@@ -2174,7 +2179,7 @@ hipError_t launch_gemm(const GemmArgs &a, int grid, int epi, int wkind, int use_
     if (wkind == W_I8 && (!a.scale || a.K % 64)) return hipErrorInvalidValue;
     GemmArgs arg = a;
     void *params[] = {&arg};
-    const dim3 block(gemm_threads(wkind, use_mfma, a.rb));
+    const dim3 block(gemm_threads(wkind, use_mfma, a.Mpad / 16, a.rb));
     // with events: timestamps taken by the dispatch itself (no extra packets)
     if (ev_start && ev_stop) return hipExtLaunchKernel(k, dim3(grid), block, params, 0, s, ev_start, ev_stop, 0);
     return hipLaunchKernel(k, dim3(grid), block, params, 0, s);
