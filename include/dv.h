@@ -256,11 +256,16 @@ int dv_draft_tree(dv_handle *h, int32_t root_token, const float *root_feature, d
  * chain of that step's tree.  Errors: DV_EINVAL, DV_ESTATE, DV_EHIP. */
 int dv_kv_commit(dv_handle *h, dv_kv *kv, const dv_accept *accept);
 
-/* Build the cache from a prompt: runs tokens[0..n) as chains of at most
- * max_tree tokens through the same kernels and commits all of them
- * (kv->len += n).  out_next_token (host, nullable) receives the argmax after
- * the last prompt token, the root of the first draft tree.
- * Errors: DV_EINVAL, DV_ECAPACITY, DV_EHIP. */
+/* Build the cache from a prompt (the target's prefill before the first
+ * draft round, Section 3.1; the Limitations section names long-context
+ * prefill as the method's bottleneck): appends the K/V of tokens[0..n) after the kv->len
+ * committed entries and commits all of them (kv->len += n).  With bf16
+ * weights and n > max_tree the prompt runs as causal chunks of up to 1024
+ * tokens (library GEMMs for the projections, a causal attention kernel);
+ * otherwise as chains of at most max_tree tokens through the verify step's
+ * kernels.  out_next_token (host, nullable) receives the argmax after the
+ * last prompt token, the root of the first draft tree.  Synchronises the
+ * stream.  Errors: DV_EINVAL, DV_ECAPACITY, DV_EHIP. */
 int dv_prefill(dv_handle *h, const int32_t *tokens, int32_t n, dv_kv *kv,
                int32_t *out_next_token);
 
