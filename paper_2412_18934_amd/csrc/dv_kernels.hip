@@ -1733,7 +1733,9 @@ __global__ __launch_bounds__(PF_THREADS) void k_pf_qkv(const float *Dq, const fl
 // uses the tiles up to its own last query.  The scores and the running
 // softmax follow the tree-attention kernel (MFMA with q split in hi + lo,
 // exp2 in log2 units); the output goes to rows i / M + i of the O
-// projection's operand.
+// projection's operand.  Grid (heads, query blocks) with the last query
+// block first: workgroups are dispatched in order, so the longest ones (the
+// most keys) start first and the short ones fill in behind them.
 template <int HD>
 __global__ __launch_bounds__(256) void k_attn_causal(const float *q, const uint16_t *kc_l, const uint16_t *vc_l,
                                                      int M, int P0, int H, int cap, uint16_t *out)
@@ -1745,9 +1747,9 @@ __global__ __launch_bounds__(256) void k_attn_causal(const float *q, const uint1
     constexpr int KCH = 32 * HD / 8, VCH = HD * 4;  // 16-byte chunks of a tile's K and V
     constexpr int CPT = (KCH + VCH + 255) / 256;     // chunks per thread
     __shared__ __align__(16) unsigned char smem[2][KBYTES + VBYTES];
-    const int h = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int h = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int n = lane & 15, g = lane >> 4;
-    const int q0 = blockIdx.x * 64;
+    const int q0 = (gridDim.y - 1 - blockIdx.y) * 64;
     const int qb = q0 + wave * 16;               // first query of this wave
     const int D = H * HD;
     const int kend_wg = P0 + min(q0 + 64, M);    // keys the workgroup may see
@@ -2323,7 +2325,7 @@ hipError_t launch_pf_qkv(const float *Dq, const float *Dk, const float *Dv, int 
 hipError_t launch_attn_causal(const float *q, const void *kc, const void *vc, int M, int P0, int H, int hd, int cap,
                               uint16_t *out, hipStream_t s)
 {
-    const dim3 grid((M + 63) / 64, H);
+    const dim3 grid(H, (M + 63) / 64);
     const uint16_t *k16 = static_cast<const uint16_t *>(kc), *v16 = static_cast<const uint16_t *>(vc);
     if (hd == 128) hipLaunchKernelGGL(k_attn_causal<128>, grid, dim3(256), 0, s, q, k16, v16, M, P0, H, cap, out);
     else if (hd == 64) hipLaunchKernelGGL(k_attn_causal<64>, grid, dim3(256), 0, s, q, k16, v16, M, P0, H, cap, out);
