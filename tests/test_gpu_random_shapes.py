@@ -1,7 +1,8 @@
 """GPU path vs the CPU oracle over a seeded sweep of model and tree shapes.
 
 Each case draws head size, head count, FFN width (multiples of 16, so some
-down projections take the VALU kernel), vocabulary, weight type, layer count,
+down projections take the VALU kernel; 64 for int8 weights), vocabulary,
+weight type (fp32, bf16, and int8 with per-row scales), layer count,
 cache capacity, committed length P (including 0), tree size M in [1, 64] and
 depth.  One verify step is compared with the oracle to the same bars as the
 fixed parity cases; then a random root-to-node path is committed and the
@@ -22,7 +23,7 @@ if not torch.cuda.is_available():
 
 from paper_2412_18934_amd import dv  # noqa: E402
 
-N_CASES = 20
+N_CASES = 32   # cases 20.. use int8 weights
 
 
 def _draw(i):
@@ -43,6 +44,8 @@ def _draw(i):
         p = 0                  # empty context
     if i % 10 == 7:
         m, depth = 1, 1        # the root alone
+    if i >= 20:                # int8 weights with per-row scales
+        dtype, F = "i8", 64 * max(1, F // 64)
     cfg = small_cfg(n_layers=layers, d_model=d, n_heads=H, head_dim=hd, d_ffn=F, vocab=V,
                     weight_dtype=dtype, init_std=0.09 * np.sqrt(256.0 / d))
     return cfg, cap, m, p, depth
