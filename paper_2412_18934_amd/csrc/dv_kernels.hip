@@ -881,20 +881,22 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mfma(AttnArgs a)
     struct Tile {
         u32x4 ka[NC], kb[NC], v[ND];
     };
+    // keys and values are read once per step: non-temporal loads
     auto load = [&](int t, Tile &T) {
         const int k0 = kbeg + 32 * t;
         const int ka = min(k0 + 8 * (n >> 2) + (n & 3), kend - 1);
         const int kb = min(k0 + 8 * (n >> 2) + 4 + (n & 3), kend - 1);
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
-            T.ka[c] = *reinterpret_cast<const u32x4 *>(kc + (size_t)ka * HD + 32 * c + 8 * g);
-            T.kb[c] = *reinterpret_cast<const u32x4 *>(kc + (size_t)kb * HD + 32 * c + 8 * g);
+            T.ka[c] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(kc + (size_t)ka * HD + 32 * c + 8 * g));
+            T.kb[c] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(kc + (size_t)kb * HD + 32 * c + 8 * g));
         }
         // columns past the last cache slot of the tile stay inside the
         // allocation (capacity is a multiple of 32); they are masked below
 #pragma unroll
         for (int dt = 0; dt < ND; ++dt)
-            T.v[dt] = *reinterpret_cast<const u32x4 *>(vc + ((size_t)(k0 >> 5) * HD + dt * 16 + n) * 32 + 8 * g);
+            T.v[dt] = __builtin_nontemporal_load(
+                reinterpret_cast<const u32x4 *>(vc + ((size_t)(k0 >> 5) * HD + dt * 16 + n) * 32 + 8 * g));
     };
 
     // queries of all tiles into LDS (hi + lo B operands) with the first key
