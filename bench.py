@@ -85,7 +85,7 @@ def int8_leg(args):
     t0 = time.perf_counter()
     W = D.DeviceWeights(mc.n_layers, lambda l: synth.layer_weights(mc, sd["weights"], l),
                         synth.embed(mc, sd["weights"]), synth.lm_head(mc, sd["weights"]),
-                        synth.final_norm(mc), lm_head_scale=synth.lm_head_scale(mc, sd["weights"]))
+                        synth.final_norm(mc, sd["weights"]), lm_head_scale=synth.lm_head_scale(mc, sd["weights"]))
     cap = p + 64
     kv = D.DeviceKV(mc.n_layers, mc.n_heads, mc.head_dim, cap, mc.weight_dtype)
     for l in range(mc.n_layers):
@@ -181,7 +181,7 @@ def draft_leg(args, mc, sd, cap, n_blocks=1, depth=7, width=10, n_tree=16):
     dcfg = synth.draft_cfg(mc, n_blocks)
     dseed = sd["weights"] + 1000
     Wd = D.DeviceWeights(dcfg.n_layers, lambda l: synth.layer_weights(dcfg, dseed, l),
-                         synth.embed(mc, sd["weights"]), synth.lm_head(mc, sd["weights"]), synth.final_norm(dcfg))
+                         synth.embed(mc, sd["weights"]), synth.lm_head(mc, sd["weights"]), synth.final_norm(dcfg, dseed))
     dg = {k: D.to_device(v, "cuda:0") for k, v in synth.dgf_weights(dcfg, dseed).items()}
     dgf = dv.dv_dgf_weights(dg["w_hidden"].data_ptr(), dg["w_embed"].data_ptr(), dg["w_gate"].data_ptr())
     cfg = D.make_config(dcfg.n_layers, dcfg.d_model, dcfg.n_heads, dcfg.head_dim, dcfg.d_ffn, dcfg.vocab,
@@ -252,7 +252,7 @@ def cpu_baseline(wl, toks, par):
     del raw_kv
     om = ov.OracleModel(mc, lambda l: layers[l],
                         lambda ids: synth.embed_rows(mc, sd["weights"], ids),
-                        synth.lm_head(mc, sd["weights"]), synth.final_norm(mc),
+                        synth.lm_head(mc, sd["weights"]), synth.final_norm(mc, sd["weights"]),
                         lm_head_scale=synth.lm_head_scale(mc, sd["weights"]))
     log("cpu oracle inputs ready in %.1f s" % (time.perf_counter() - t0))
     t0 = time.perf_counter()
@@ -322,7 +322,7 @@ def main():
         return synth.layer_weights(mc, sd["weights"], l)
 
     W = D.DeviceWeights(mc.n_layers, layer_fn, synth.embed(mc, sd["weights"]),
-                        synth.lm_head(mc, sd["weights"]), synth.final_norm(mc),
+                        synth.lm_head(mc, sd["weights"]), synth.final_norm(mc, sd["weights"]),
                         lm_head_scale=synth.lm_head_scale(mc, sd["weights"]))
     cap = p + 64
     kv = D.DeviceKV(mc.n_layers, mc.n_heads, mc.head_dim, cap, mc.weight_dtype)

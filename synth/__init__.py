@@ -49,6 +49,8 @@ def _L():
         lib.dvs_normal_bf16.argtypes = [u64, u64, u64, u64, ctypes.c_double, p]
         lib.dvs_normal_f32.argtypes = [u64, u64, u64, u64, ctypes.c_double, p]
         lib.dvs_normal_i8.argtypes = [u64, u64, u64, u64, ctypes.c_double, p]
+        lib.dvs_gain_bf16.argtypes = [u64, u64, u64, u64, ctypes.c_double, p]
+        lib.dvs_gain_f32.argtypes = [u64, u64, u64, u64, ctypes.c_double, p]
         lib.dvs_u64.argtypes = [u64, u64, u64, u64, p]
         lib.dvs_uniform_int.argtypes = [u64, u64, u64, u64, ctypes.c_uint32, p]
         _lib = lib
@@ -70,6 +72,20 @@ def normal(seed: int, tensor: int, n: int, sigma: float, dtype: str, start: int 
     elif dtype == "f32":
         out = np.empty(n, dtype=np.float32)
         _L().dvs_normal_f32(seed, tensor, start, n, sigma, out.ctypes.data)
+    else:
+        raise ValueError(dtype)
+    return out
+
+
+def gain(seed: int, tensor: int, n: int, sigma: float, dtype: str) -> np.ndarray:
+    """``n`` norm gains 1 + N(0, sigma^2) stored as ``dtype`` ('bf16' -> uint16
+    bits, 'f32')."""
+    if dtype == "bf16":
+        out = np.empty(n, dtype=np.uint16)
+        _L().dvs_gain_bf16(seed, tensor, 0, n, sigma, out.ctypes.data)
+    elif dtype == "f32":
+        out = np.empty(n, dtype=np.float32)
+        _L().dvs_gain_f32(seed, tensor, 0, n, sigma, out.ctypes.data)
     else:
         raise ValueError(dtype)
     return out
@@ -191,6 +207,7 @@ def shrink(model: ModelCfg, **kw) -> ModelCfg:
 
 T_EMBED, T_LMHEAD, T_PROMPT, T_TREE_PARENT, T_TREE_TOKEN = 1, 2, 3, 4, 5
 T_UNIFORM, T_DRAFT = 6, 7
+T_FINAL_NORM = 8
 T_SCALE_OFFSET = 1 << 40   # row scales of the matrix with tensor id t use id t + T_SCALE_OFFSET
 LAYER_NAMES = ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down")
 
@@ -199,14 +216,18 @@ def _t_layer(l: int, name: str) -> int:
     return 1000 + 16 * l + LAYER_NAMES.index(name)
 
 
+def _t_norm(l: int, which: int) -> int:
+    """attention norm (which 0) and FFN norm (which 1) of layer l"""
+    return 1000 + 16 * l + len(LAYER_NAMES) + which
+
+
 def _t_kv(l: int, which: int) -> int:
     return 500000 + 2 * l + which
 
 
-def _ones(n: int, dtype: str) -> np.ndarray:
-    if dtype == "bf16":
-        return np.full(n, 0x3F80, dtype=np.uint16)
-    return np.ones(n, dtype=np.float32)
+# Norm gains: 1 + N(0, GAIN_SIGMA^2) per element, a distinct stream per layer
+# and norm, so that a gain applied in the wrong place changes the result.
+GAIN_SIGMA = 0.1
 
 
 I8_CODE_SIGMA = 127.0 / 4.0   # int8 codes: the clip sits at 4 standard deviations
@@ -228,16 +249,17 @@ def _matrix(cfg: ModelCfg, seed: int, tensor: int, rows: int, cols: int, out: di
 
 
 def layer_weights(cfg: ModelCfg, seed: int, l: int) -> dict:
-    """Weights of layer ``l``: matrices ``[out][in]``, norm gains = 1.  For
-    'i8' each matrix comes with ``<name>_scale`` (float32 per row)."""
+    """Weights of layer ``l``: matrices ``[out][in]`` and the two norm gains
+    (1 + N(0, GAIN_SIGMA^2) each).  For 'i8' each matrix comes with
+    ``<name>_scale`` (float32 per row)."""
     d, f = cfg.d_model, cfg.d_ffn
     shapes = dict(wq=(d, d), wk=(d, d), wv=(d, d), wo=(d, d),
                   w_gate=(f, d), w_up=(f, d), w_down=(d, f))
     out = {}
     for k, (a, b) in shapes.items():
         _matrix(cfg, seed, _t_layer(l, k), a, b, out, k)
-    out["attn_norm"] = _ones(d, cfg.dense_dtype)
-    out["ffn_norm"] = _ones(d, cfg.dense_dtype)
+    out["attn_norm"] = gain(seed, _t_norm(l, 0), d, GAIN_SIGMA, cfg.dense_dtype)
+    out["ffn_norm"] = gain(seed, _t_norm(l, 1), d, GAIN_SIGMA, cfg.dense_dtype)
     return out
 
 
@@ -266,8 +288,9 @@ def lm_head_scale(cfg: ModelCfg, seed: int):
     return row_scales(cfg, seed, T_LMHEAD + T_SCALE_OFFSET, cfg.vocab)
 
 
-def final_norm(cfg: ModelCfg) -> np.ndarray:
-    return _ones(cfg.d_model, cfg.dense_dtype)
+def final_norm(cfg: ModelCfg, seed: int) -> np.ndarray:
+    """Gains of the final norm (1 + N(0, GAIN_SIGMA^2))."""
+    return gain(seed, T_FINAL_NORM, cfg.d_model, GAIN_SIGMA, cfg.dense_dtype)
 
 
 def kv_sigma(cfg: ModelCfg) -> float:

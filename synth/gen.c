@@ -90,6 +90,20 @@ void dvs_normal_f32(uint64_t seed, uint64_t tensor, uint64_t start, uint64_t n,
     NORMAL_LOOP(out[i - start] = v)
 }
 
+/* Norm gains scattered around 1: out[e] = bf16(1 + sigma * N_{start+e}). */
+void dvs_gain_bf16(uint64_t seed, uint64_t tensor, uint64_t start, uint64_t n,
+                   double sigma, uint16_t *out)
+{
+    NORMAL_LOOP(out[i - start] = f32_to_bf16_bits(1.0f + v))
+}
+
+/* The same as fp32: out[e] = fp32(1 + sigma * N_{start+e}). */
+void dvs_gain_f32(uint64_t seed, uint64_t tensor, uint64_t start, uint64_t n,
+                  double sigma, float *out)
+{
+    NORMAL_LOOP(out[i - start] = 1.0f + v)
+}
+
 /* out[e] = int8(clamp(rint(sigma * N_{start+e}), -127, 127)), e < n: integer
  * codes with a Gaussian profile (sigma = 127/4 puts the clip at 4 standard
  * deviations). */

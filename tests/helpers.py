@@ -22,7 +22,7 @@ class Weights:
         self.embed = synth.embed(cfg, seed)
         self.lm_head = synth.lm_head(cfg, seed)
         self.lm_head_scale = synth.lm_head_scale(cfg, seed)
-        self.final_norm = synth.final_norm(cfg)
+        self.final_norm = synth.final_norm(cfg, seed)
 
     def oracle(self):
         return OracleModel(self.cfg, lambda l: self.layers[l], lambda ids: self.embed[ids],

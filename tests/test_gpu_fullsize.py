@@ -40,7 +40,7 @@ class _Model:
         self.embed = synth.embed(mc, seed)
         self.lm = synth.lm_head(mc, seed)
         self.lm_s = synth.lm_head_scale(mc, seed)
-        self.fn = synth.final_norm(mc)
+        self.fn = synth.final_norm(mc, seed)
         self.dev = D.DeviceWeights(mc.n_layers, lambda l: self.layers[l], self.embed, self.lm, self.fn,
                                    lm_head_scale=self.lm_s)
         self.om = ov.OracleModel(mc, lambda l: self.layers[l], lambda ids: self.embed[ids],

@@ -52,7 +52,7 @@ def _pow2_model(cfg, seed, transpose_scale=False):
     lm_s = np.ldexp(np.float32(1.0), -e).astype(np.float32)
     lm_d = np.ldexp(lm.astype(np.float32), -e[:, None]).astype(np.float32)
     emb = synth.embed(cfg, seed)
-    fn = synth.final_norm(cfg)
+    fn = synth.final_norm(cfg, seed)
     om_q = ov.OracleModel(cfg, lambda l: q_layers[l], lambda ids: emb[ids], lm, fn, lm_head_scale=lm_s)
     om_d = ov.OracleModel(cfg, lambda l: d_layers[l], lambda ids: synth.bf16_bits_to_f32(emb[ids]), lm_d,
                           synth.bf16_bits_to_f32(fn))

@@ -244,7 +244,40 @@ def _tree_info_sees_siblings(parents):
     return info
 
 
+def _layer_attn_ffn_swapped(self, l, dtype):
+    w = ov.__dict__["_orig_layer"](self, l, dtype)
+    w["attn_norm"], w["ffn_norm"] = w["ffn_norm"], w["attn_norm"]
+    return w
+
+
+def _layer_norms_of_layer0(self, l, dtype):
+    w = ov.__dict__["_orig_layer"](self, l, dtype)
+    w0 = ov.__dict__["_orig_layer"](self, 0, dtype)
+    w["attn_norm"], w["ffn_norm"] = w0["attn_norm"], w0["ffn_norm"]
+    return w
+
+
+class _FinalNormTakesLastLayerGain:
+    """rmsnorm whose last call of every pass (the final norm: a pass makes
+    2 n_layers + 1 calls) uses the gain of the call before it (the last
+    layer's FFN norm)."""
+
+    def __init__(self, n_layers):
+        self.per_pass, self.calls, self.prev = 2 * n_layers + 1, 0, None
+
+    def __call__(self, x, g, eps):
+        self.calls += 1
+        if self.calls % self.per_pass == 0:
+            g = self.prev
+        self.prev = g
+        return ov.__dict__["_orig_rmsnorm"](x, g, eps)
+
+
 _MUTANTS = {
+    "gain_ignored": ("rmsnorm", lambda x, g, eps: ov.__dict__["_orig_rmsnorm"](x, np.ones_like(g), eps)),
+    "attn_ffn_gains_swapped": ("OracleModel.layer", _layer_attn_ffn_swapped),
+    "every_layer_takes_layer0_gains": ("OracleModel.layer", _layer_norms_of_layer0),
+    "final_norm_takes_last_layer_gain": ("rmsnorm", _FinalNormTakesLastLayerGain(small_cfg().n_layers)),
     "rope_interleaved": ("rope", _rope_interleaved),
     "attention_unscaled": ("attention_node", _attention_unscaled),
     "positions_by_index": ("tree_info", _tree_info_index_positions),
@@ -260,7 +293,12 @@ def test_planted_oracle_mistakes_are_caught(name, monkeypatch):
     attr, fn = _MUTANTS[name]
     monkeypatch.setitem(ov.__dict__, "_orig_attention", ov.attention_node)
     monkeypatch.setitem(ov.__dict__, "_orig_tree_info", ov.tree_info)
-    monkeypatch.setattr(ov, attr, fn)
+    monkeypatch.setitem(ov.__dict__, "_orig_rmsnorm", ov.rmsnorm)
+    monkeypatch.setitem(ov.__dict__, "_orig_layer", ov.OracleModel.layer)
+    if attr == "OracleModel.layer":
+        monkeypatch.setattr(ov.OracleModel, "layer", fn)
+    else:
+        monkeypatch.setattr(ov, attr, fn)
     assert _hf_mismatch() > 1e-3
 
 
