@@ -46,12 +46,13 @@ def kv_bytes(mc):
     return 4 if mc.kv_dtype == "f32" else 2
 
 
-def gemm_bytes(mc, m):
+def gemm_bytes(mc, m, logits=False):
     """Algorithmic bytes of the projection kernels in one step: weights once
     (int8: plus one fp32 scale per row), activations in once (split bf16 hi +
     lo: 4 bytes per value), outputs out once; the residual projections also
     read and write their rows of the fp32 residual stream and write the next
-    RMSNorm's input."""
+    RMSNorm's input; with ``logits`` the lm_head also writes the fp32
+    logits."""
     d, f, v, L = mc.d_model, mc.d_ffn, mc.vocab, mc.n_layers
     wsz, rsz = weight_bytes(mc)
     esz = kv_bytes(mc)
@@ -61,13 +62,16 @@ def gemm_bytes(mc, m):
                          + d + f                      # gate/up: in, h out
                          + f + 2 * d + d)             # down: in, residual read+write, next input
     head = 4 * m * d + 8 * m * (v // 64)              # lm_head: in, per-group argmax partials
+    if logits:
+        head += 4 * m * v
     return w + L * per_layer + head, 4 * L + 1
 
 
-def step_bytes(mc, m, p):
-    """Algorithmic HBM bytes of a whole step (no logits written)."""
+def step_bytes(mc, m, p, logits=False):
+    """Algorithmic HBM bytes of a whole step (with ``logits``: the fp32 logits
+    written too)."""
     d, L, H, hd = mc.d_model, mc.n_layers, mc.n_heads, mc.head_dim
-    g, _ = gemm_bytes(mc, m)
+    g, _ = gemm_bytes(mc, m, logits)
     esz = kv_bytes(mc)
     kv_read = L * 2 * H * (p + m) * hd * esz
     return g + kv_read + m * d * esz
@@ -232,40 +236,86 @@ def ov_tree_depth(par):
     return int(max(dep)) if dep else 0
 
 
-def cpu_baseline(wl, toks, par):
-    """The oracle as it stands (float64 numpy), timed on the host for one
-    whole step of the workload (all layers, same tree and context).  Weight
-    generation and upcasting of the stored weights happen before/inside as the
-    oracle does them; only the verify_step call is timed."""
-    import oracle.verify as ov
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for ln in fh:
+                if ln.startswith("model name"):
+                    return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _blas_threads():
     try:
         import threadpoolctl
         info = threadpoolctl.threadpool_info()
-        threads = max([i.get("num_threads", 1) for i in info] or [1])
+        return max([i.get("num_threads", 1) for i in info if i.get("user_api") == "blas"] or [1])
     except Exception:  # pragma: no cover
-        threads = os.cpu_count()
+        return os.cpu_count()
+
+
+def cpu_baseline(wl, toks, par, fp64="on"):
+    """The oracle as it stands, timed on the host for whole steps of the
+    workload (all layers, same tree and context).  Timing mode: float32 numpy
+    with BLAS matmuls, every weight upcast to float32 before the timed region
+    (the paper's own target runs fp32 weights on the CPU); one warm-up step,
+    then the median of three.  The float64 parity mode (weights upcast per
+    layer inside the call, as the tests run it) is timed once beside it,
+    informational only."""
+    import concurrent.futures as cf
+    import oracle.verify as ov
     mc, sd = wl.model, wl.seeds
     t0 = time.perf_counter()
     layers = [synth.layer_weights(mc, sd["weights"], l) for l in range(mc.n_layers)]
     raw_kv = [synth.kv_layer(mc, sd["kv"], l, wl.context) for l in range(mc.n_layers)]
-    kv_o = ov.kv_from_raw(raw_kv)
-    del raw_kv
-    om = ov.OracleModel(mc, lambda l: layers[l],
-                        lambda ids: synth.embed_rows(mc, sd["weights"], ids),
-                        synth.lm_head(mc, sd["weights"]), synth.final_norm(mc, sd["weights"]),
-                        lm_head_scale=synth.lm_head_scale(mc, sd["weights"]))
-    log("cpu oracle inputs ready in %.1f s" % (time.perf_counter() - t0))
-    t0 = time.perf_counter()
-    ov.verify_step(om, kv_o, toks, par)
-    t = time.perf_counter() - t0
-    log("cpu oracle step: %.2f s" % t)
-    return {
-        "value": round(len(toks) / t, 4), "unit": "draft tokens/s", "cores": int(threads),
+    lm, lm_s = synth.lm_head(mc, sd["weights"]), synth.lm_head_scale(mc, sd["weights"])
+    fn = synth.final_norm(mc, sd["weights"])
+    embed_fn = lambda ids: synth.embed_rows(mc, sd["weights"], ids)  # noqa: E731
+    om = ov.OracleModel(mc, lambda l: layers[l], embed_fn, lm, fn, lm_head_scale=lm_s)
+    # float32 copies of every weight, made once, straight from the stored
+    # values (bf16 bits shifted into fp32, int8 codes times their row scale;
+    # threads: the conversions release the interpreter lock)
+    def up32(raw):
+        return {k: (ov.dequantize_rows(v, raw[k + "_scale"], np.float32) if k + "_scale" in raw
+                    else synth.bf16_bits_to_f32(v) if v.dtype == np.uint16 else v.astype(np.float32, copy=False))
+                for k, v in raw.items() if not k.endswith("_scale")}
+
+    with cf.ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 1)) as ex:
+        layers32 = list(ex.map(up32, layers))
+    lm32 = (ov.dequantize_rows(lm, lm_s, np.float32) if lm_s is not None
+            else synth.bf16_bits_to_f32(lm) if lm.dtype == np.uint16 else lm)
+    fn32 = synth.bf16_bits_to_f32(fn) if fn.dtype == np.uint16 else fn
+    om32 = ov.OracleModel(mc, lambda l: layers32[l], embed_fn, lm32, fn32)
+    kv32 = ov.kv_from_raw(raw_kv, np.float32)
+    log("cpu oracle inputs ready (float32 weights resident) in %.1f s" % (time.perf_counter() - t0))
+    ov.verify_step(om32, kv32, toks, par, dtype=np.float32)          # warm-up
+    times = []
+    for _ in range(3):
+        t1 = time.perf_counter()
+        ov.verify_step(om32, kv32, toks, par, dtype=np.float32)
+        times.append(time.perf_counter() - t1)
+    t = float(np.median(times))
+    log("cpu oracle step (float32, BLAS): %.3f s median of %s" % (t, ["%.3f" % x for x in times]))
+    del layers32, om32, kv32
+    out = {
+        "value": round(len(toks) / t, 4), "unit": "draft tokens/s", "cores": int(_blas_threads()),
         "kind": "oracle", "ms_per_step": round(t * 1e3, 1),
-        "sample": ("one full step of the same workload (%d-node tree, %d-token context, %d "
-                   "layers) by the float64 numpy oracle" % (len(toks), wl.context, mc.n_layers)),
-        "host_cpus": os.cpu_count(),
+        "sample": ("whole steps of the same workload (%d-node tree, %d-token context, %d layers) by "
+                   "the oracle in float32 with BLAS matmuls, weights upcast to float32 before timing; "
+                   "one warm-up, median of 3" % (len(toks), wl.context, mc.n_layers)),
+        "cpu_model": _cpu_model(), "nproc": len(os.sched_getaffinity(0)), "blas_threads": int(_blas_threads()),
     }
+    if fp64 == "on":
+        kv64 = ov.kv_from_raw(raw_kv)
+        t1 = time.perf_counter()
+        ov.verify_step(om, kv64, toks, par)
+        t64 = time.perf_counter() - t1
+        log("cpu oracle step (float64 parity mode): %.2f s" % t64)
+        out["fp64_parity_mode"] = {"ms_per_step": round(t64 * 1e3, 1), "value": round(len(toks) / t64, 4),
+                                   "note": "informational: one step, weights upcast per layer inside the call"}
+    return out
 
 
 def main():
@@ -276,6 +326,8 @@ def main():
     ap.add_argument("--workload", default=HBM_WORKLOAD,
                     help="one of %s, or sweep-M" % ", ".join(synth.WORKLOADS))
     ap.add_argument("--cpu-baseline", choices=["on", "off"], default="on")
+    ap.add_argument("--cpu-fp64", choices=["on", "off"], default="on",
+                    help="also time one step of the float64 parity mode (informational)")
     ap.add_argument("--roofline-events", choices=["inline", "off"], default="inline",
                     help="HIP events around the projection kernels inside the timed region")
     ap.add_argument("--sampled", choices=["on", "off"], default="on",
@@ -344,26 +396,37 @@ def main():
         torch.cuda.synchronize()
         log("calibration copy: %d bytes read, %d written" % (src.nbytes, dst.nbytes))
         del src, dst
+    # every timed step writes the tree's fp32 logits (the contract's full
+    # output) besides the accept result
+    out_logits = torch.empty((m, mc.vocab), dtype=torch.float32, device="cuda:0")
+    lp = out_logits.data_ptr()
     for _ in range(args.warmup):
-        acc = dv.dv_verify_step(h, toks, par, kv.c, 0)
+        acc = dv.dv_verify_step(h, toks, par, kv.c, lp)
     log("warmup done (%d steps)" % args.warmup)
 
     # timed region: value and ms_per_step (no timing instrumentation inside)
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for _ in range(args.steps):
-        acc = dv.dv_verify_step(h, toks, par, kv.c, 0)
+        acc = dv.dv_verify_step(h, toks, par, kv.c, lp)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
     ms = elapsed / args.steps * 1e3
     log("timed %d steps: %.3f ms/step" % (args.steps, ms))
+    # the same steps without the logits output (accept result only)
+    torch.cuda.synchronize()
+    t_nl = time.perf_counter()
+    for _ in range(args.steps):
+        dv.dv_verify_step(h, toks, par, kv.c, 0)
+    torch.cuda.synchronize()
+    ms_nl = (time.perf_counter() - t_nl) / args.steps * 1e3
 
     # latency distribution: each call ends with the accept struct on the host,
     # so the host clock around one call is that step's latency
     lat = []
     for _ in range(args.steps):
         t1 = time.perf_counter()
-        dv.dv_verify_step(h, toks, par, kv.c, 0)
+        dv.dv_verify_step(h, toks, par, kv.c, lp)
         lat.append((time.perf_counter() - t1) * 1e3)
     lat_ms = {"p10": round(float(np.percentile(lat, 10)), 4), "p50": round(float(np.median(lat)), 4),
               "p90": round(float(np.percentile(lat, 90)), 4)}
@@ -406,7 +469,7 @@ def main():
 
     # roofline pass: the same steps again with every projection launch timed
     # by HIP events recorded by its own dispatch on the library's stream
-    gbytes, glaunch = gemm_bytes(mc, m)
+    gbytes, glaunch = gemm_bytes(mc, m, logits=True)
     roof = None
     if args.roofline_events == "inline":
         dv.dv_profile_enable(h, 1 << dv.DV_K_GEMM)
@@ -414,7 +477,7 @@ def main():
         torch.cuda.synchronize()
         t_r = time.perf_counter()
         for _ in range(args.steps):
-            dv.dv_verify_step(h, toks, par, kv.c, 0)
+            dv.dv_verify_step(h, toks, par, kv.c, lp)
         torch.cuda.synchronize()
         ms_r = (time.perf_counter() - t_r) / args.steps * 1e3
         dv.dv_profile_enable(h, 0)
@@ -431,6 +494,10 @@ def main():
             roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                     "traffic": None if traffic is None else round(traffic),
+                    "traffic_source": (None if traffic is None else
+                                       "replayed from profiles/%s (rocprofv3 --pmc FETCH_SIZE and WRITE_SIZE "
+                                       "runs of this workload, scaled by the copy factor; null when the kernel "
+                                       "sources changed since)" % HBM_PROFILE),
                     "kernel": "k_proj (QKV, O, gate/up, down, lm_head projections)",
                     "bytes_per_launch": int(per_launch), "avg_launch_us": round(avg_ms * 1e3, 2),
                     "launches_per_step": round(glaunch, 2), "ms_per_step_with_events": round(ms_r, 3)}
@@ -460,7 +527,7 @@ def main():
                    "accept_kernel_us": round(acc_ms / max(acc_n, 1) * 1e3, 2)}
         log("sampled step: %.3f ms, accept kernel %.1f us" % (ms_s, sampled["accept_kernel_us"]))
         del q, logits
-    sbytes = step_bytes(mc, m, p)
+    sbytes = step_bytes(mc, m, p, logits=True)
     step_gbs = sbytes / (ms * 1e-3) / 1e9
 
     result = {
@@ -469,6 +536,7 @@ def main():
         "unit": "draft tokens/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms, 4),
+        "ms_per_step_no_logits": round(ms_nl, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": mc.weight_dtype, "data": "synthetic",
         "config": {"workload": wl.name, "n_tree": m, "context": p, "depth": wl.depth,
@@ -493,7 +561,7 @@ def main():
     if args.int8 == "on" and wl.name == HBM_WORKLOAD:
         result["int8"] = int8_leg(args)
     if args.cpu_baseline == "on":
-        result["cpu_baseline"] = cpu_baseline(wl, toks, par)
+        result["cpu_baseline"] = cpu_baseline(wl, toks, par, args.cpu_fp64)
     print(json.dumps(result), flush=True)
 
 

@@ -1937,10 +1937,10 @@ __global__ __launch_bounds__(1024) void k_pf_argmax(const float *Dz, int V, DevA
 }
 
 // ---------------------------------------------------------------------------
-// Draft side.  Dynamic Gated Fusion around three plain GEMMs (hipBLASLt, the
-// same [2n][K] hi/lo operand convention as the prefill):
-//   prep: parent features -> hi/lo rows; token embeddings -> bf16 rows
-//   mid:  h1 = W_h f (two halves), h2 = W_e e -> hi/lo rows of [h1 || h2]
+// Draft side.  Dynamic Gated Fusion around three weight-streaming
+// projections (k_proj with the plain-output epilogue, split-layout operands):
+//   prep: parent features and token embeddings -> split-layout operands
+//   mid:  h1 = W_h f, h2 = W_e e -> split-layout operand of [h1 || h2]
 //   out:  g = sigmoid(W_g [h1 || h2]); x0 = g h1 + (1 - g) h2
 // DGF operands in split layout (the projection kernel's B operand), one
 // workgroup per token row m < Mpad: feature rows and the token embeddings

@@ -94,7 +94,7 @@ def test_llama13b_m16_ctx1024(llama13b):
     llama13b.run(synth.WORKLOADS["llama13b-bf16-m16-ctx1024"])
 
 
-@pytest.mark.parametrize("m", [1, 64])
+@pytest.mark.parametrize("m", [1, 2, 4, 8, 32, 64])
 def test_llama13b_sweep_extremes(llama13b, m):
     wl = synth.sweep_workload(m)
     assert wl.model == llama13b.mc

@@ -95,7 +95,11 @@ def test_bf16_random_tree_parity(bf16_case, m):
         for got, want in ((k, ref["new_k"][l]), (v, ref["new_v"][l])):
             want = np.transpose(want, (1, 0, 2))
             rms = np.sqrt(np.mean(want ** 2))
-            np.testing.assert_allclose(ov.bf16_to_f64(got[:, p:]), want, rtol=2 ** -7,
+            g64 = ov.bf16_to_f64(got[:, p:])
+            # observed error beyond the one-rounding-step part, in units of the RMS
+            excess = float(np.max(np.abs(g64 - want) - 2 ** -7 * np.abs(want))) / rms
+            print("[kv-rows] M=%d layer %d: max excess over one bf16 step %.2e of RMS" % (m, l, excess))
+            np.testing.assert_allclose(g64, want, rtol=2 ** -7,
                                        atol=(1e-4 if l == 0 else 5e-3) * rms)
 
 

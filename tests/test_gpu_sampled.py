@@ -9,9 +9,11 @@ either way; every case therefore takes the oracle's decision trace and
 * requires the exact same path and bonus when every decision clears its
   margin (relative 1e-4 of the compared values plus 1e-6 over the residual
   mass for an acceptance, 2e-6 of the total mass for the bonus);
-* otherwise checks that the GPU result is a valid outcome (a root-to-node
-  chain; a bonus whose cumulative-mass interval touches the target within
-  the margin when the path agrees).
+* otherwise checks that the GPU result is a valid outcome: a root-to-node
+  chain that leaves the oracle's path exactly at a decision inside the
+  margin (the first child, in trial order, that the two walks treated
+  differently), or, on the same path, a bonus whose cumulative-mass interval
+  touches the target within the margin.
 
 Outcomes that differ from the oracle's must stay rare (at most one per test),
 so the comparison is not vacuous.
@@ -61,9 +63,21 @@ def _judge(acc, n, path, bonus, trace, parents, vocab, rel=1e-4, bonus_rel=2e-6)
     if got_path == list(path) and acc.bonus_token == bonus:
         return True
     if got_path != list(path):
-        near = [ev for ev in trace if ev[0] == "accept"
-                and abs(ev[2] - ev[3]) <= rel * max(ev[2], ev[3]) + 1e-6 / ev[4]]
-        assert near, ("path differs at a clear decision", got_path, list(path))
+        # the first node where the two walks part: the oracle moved to child a
+        # (None: it stopped there), the GPU to child b; children are tried in
+        # index order, so the first decision the two took differently is the
+        # one on child min(a, b), which the oracle's walk reached
+        k = 1
+        while k < len(got_path) and k < len(path) and got_path[k] == path[k]:
+            k += 1
+        a = path[k] if k < len(path) else None
+        b = got_path[k] if k < len(got_path) else None
+        c = min(x for x in (a, b) if x is not None)
+        ev = [e for e in trace if e[0] == "accept" and e[1] == c]
+        assert len(ev) == 1, ("oracle never tried the child where the walks part", c, got_path, list(path))
+        _, _, uq, pt, mass = ev[0]
+        assert abs(uq - pt) <= rel * max(uq, pt) + 1e-6 / mass, \
+            ("walks part at a clear decision", c, uq, pt, got_path, list(path))
         return False
     p, u = trace[-1][1], trace[-1][2]
     c = np.cumsum(p)
