@@ -194,6 +194,27 @@ int dv_accept_sampled(dv_handle *h, const float *logits, const int32_t *tokens,
                       float temperature, const float *u_accept, const float *u_bonus,
                       dv_accept *out_accept);
 
+/* The sampling rule of dv_accept_sampled without a handle and without any
+ * allocation, for callers that cannot allocate device memory (serving loops
+ * and harnesses that forbid hipMalloc).  Its workspace (the result struct and
+ * two distribution rows) is a fixed device array of the library, 2 MiB + 1 KiB,
+ * one per GPU (the current device), held until the process ends; the call
+ * makes no hipMalloc/hipFree and no allocating library call.  Calls that
+ * overlap on one GPU (other threads, other streams) share that array and
+ * race; calls in sequence are safe (nothing in it needs to start at zero).
+ *   logits: device [n_tree][vocab] fp32, 16-byte aligned;
+ *   vocab: multiple of 4, 4 <= vocab <= DV_NOALLOC_MAX_VOCAB (DV_EINVAL
+ *       beyond the limit, before anything is launched);
+ *   stream: hipStream_t the kernel and the result copy run on (NULL =
+ *       default stream); the call synchronises it;
+ *   other arguments, the rule and out_accept as dv_accept_sampled.
+ * Errors (message via dv_last_error(NULL)): DV_EINVAL, DV_EHIP. */
+#define DV_NOALLOC_MAX_VOCAB 262144
+int dv_accept_sampled_noalloc(const float *logits, const int32_t *tokens, const int32_t *tree_parents,
+                              int32_t n_tree, int32_t vocab, const float *draft_probs, float temperature,
+                              const float *u_accept, const float *u_bonus, void *stream,
+                              dv_accept *out_accept);
+
 /* ---- Draft side (Section 3.1 tree construction, Section 3.2 Dynamic Gated
  * Fusion, Section 3.3 multiple blocks) ---------------------------------- */
 

@@ -423,9 +423,9 @@ void fill_desc(StepDesc *sd, const int32_t *tokens, const int32_t *parents, int 
 
 // Validate the sampling inputs of a step over an n-node tree and fill the
 // walk's arguments (logits are set by the caller).
-int prepare_sampled(dv_handle *h, const int32_t *tokens, const int32_t *parents, int n,
+int prepare_sampled(dv_handle *h, const int32_t *tokens, const int32_t *parents, int n, int vocab,
                     const float *draft_probs, float temperature, const float *u_accept,
-                    const float *u_bonus, SampleArgs *sa)
+                    const float *u_bonus, float *p_ws, DevAccept *acc, SampleArgs *sa)
 {
     if (!draft_probs || !u_accept || !u_bonus) return set_err(h, DV_EINVAL, "null draft distribution or uniforms");
     if (reinterpret_cast<uintptr_t>(draft_probs) % 16)
@@ -440,8 +440,8 @@ int prepare_sampled(dv_handle *h, const int32_t *tokens, const int32_t *parents,
     }
     std::memset(sa, 0, sizeof *sa);
     sa->q = draft_probs;
-    sa->p = h->p_ws;
-    sa->V = h->cfg.vocab;
+    sa->p = p_ws;
+    sa->V = vocab;
     sa->M = n;
     sa->inv_t = 1.f / temperature;
     for (int i = 0; i < n; ++i) {
@@ -450,7 +450,7 @@ int prepare_sampled(dv_handle *h, const int32_t *tokens, const int32_t *parents,
         sa->u_accept[i] = i > 0 ? u_accept[i] : 0.f;
         sa->u_bonus[i] = u_bonus[i];
     }
-    sa->acc = h->d_acc;
+    sa->acc = acc;
     return DV_OK;
 }
 
@@ -905,7 +905,8 @@ static int verify_step_impl(dv_handle *h, const int32_t *tokens, const int32_t *
                        kv->len, n_tree, kv->capacity, h->cfg.max_ctx);
     SampleArgs sa;
     if (sampled) {
-        if ((rc = prepare_sampled(h, tokens, tree_parents, n_tree, draft_probs, temperature, u_accept, u_bonus,
+        if ((rc = prepare_sampled(h, tokens, tree_parents, n_tree, h->cfg.vocab, draft_probs, temperature, u_accept, u_bonus,
+                                  h->p_ws, h->d_acc,
                                   &sa)))
             return rc;
         if (out_logits && reinterpret_cast<uintptr_t>(out_logits) % 16)
@@ -971,7 +972,8 @@ int dv_accept_sampled(dv_handle *h, const float *logits, const int32_t *tokens, 
     int rc = check_tree(h, tree_parents, n_tree, 0, pos, depth, anc);
     if (rc) return rc;
     SampleArgs sa;
-    if ((rc = prepare_sampled(h, tokens, tree_parents, n_tree, draft_probs, temperature, u_accept, u_bonus, &sa)))
+    if ((rc = prepare_sampled(h, tokens, tree_parents, n_tree, h->cfg.vocab, draft_probs, temperature, u_accept, u_bonus,
+                                  h->p_ws, h->d_acc, &sa)))
         return rc;
     sa.logits = logits;
     prof_begin(h, DV_K_OTHER);
@@ -982,6 +984,52 @@ int dv_accept_sampled(dv_handle *h, const float *logits, const int32_t *tokens, 
     HIPCHK(h, hipStreamSynchronize(h->stream));
     prof_collect(h);
     const DevAccept &a = *h->h_acc;
+    std::memset(out_accept, 0, sizeof *out_accept);
+    out_accept->accept_len = a.accept_len;
+    out_accept->bonus_token = a.bonus;
+    out_accept->n_tree = n_tree;
+    out_accept->base_len = -1;
+    for (int i = 0; i < a.accept_len && i < DV_MAX_TREE; ++i) out_accept->path[i] = a.path[i];
+    return DV_OK;
+}
+
+int dv_accept_sampled_noalloc(const float *logits, const int32_t *tokens, const int32_t *tree_parents,
+                              int32_t n_tree, int32_t vocab, const float *draft_probs, float temperature,
+                              const float *u_accept, const float *u_bonus, void *stream, dv_accept *out_accept)
+{
+    // every check comes before the first HIP call
+    if (!logits || !tokens || !tree_parents || !out_accept) return set_err(nullptr, DV_EINVAL, "null argument");
+    if (reinterpret_cast<uintptr_t>(logits) % 16) return set_err(nullptr, DV_EINVAL, "logits must be 16-byte aligned");
+    if (vocab < 4 || vocab % 4) return set_err(nullptr, DV_EINVAL, "vocab must be a positive multiple of 4 (got %d)", vocab);
+    if (vocab > DV_NOALLOC_MAX_VOCAB)
+        return set_err(nullptr, DV_EINVAL, "vocab %d exceeds the allocation-free workspace limit of %d", vocab,
+                       DV_NOALLOC_MAX_VOCAB);
+    if (n_tree < 1 || n_tree > DV_MAX_TREE)
+        return set_err(nullptr, DV_EINVAL, "n_tree %d outside [1, %d]", n_tree, DV_MAX_TREE);
+    for (int i = 0; i < n_tree; ++i)
+        if (tokens[i] < 0 || tokens[i] >= vocab)
+            return set_err(nullptr, DV_EINVAL, "token id %d at node %d outside [0, %d)", tokens[i], i, vocab);
+    int32_t pos[DV_MAX_TREE], depth[DV_MAX_TREE];
+    uint64_t anc[DV_MAX_TREE];
+    int rc = check_tree(nullptr, tree_parents, n_tree, 0, pos, depth, anc);
+    if (rc) return rc;
+    SampleArgs sa;
+    if ((rc = prepare_sampled(nullptr, tokens, tree_parents, n_tree, vocab, draft_probs, temperature, u_accept,
+                              u_bonus, nullptr, nullptr, &sa)))
+        return rc;
+    void *ws = nullptr;
+    hipError_t e = noalloc_scratch(&ws);
+    if (e != hipSuccess) return set_err(nullptr, DV_EHIP, "workspace address: %s", hipGetErrorString(e));
+    sa.logits = logits;
+    sa.acc = static_cast<DevAccept *>(ws);
+    sa.p = reinterpret_cast<float *>(static_cast<char *>(ws) + DV_NOALLOC_ACC_BYTES);
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    if ((e = launch_accept_sampled(sa, s)) != hipSuccess)
+        return set_err(nullptr, DV_EHIP, "sampled accept launch: %s", hipGetErrorString(e));
+    DevAccept a;
+    if ((e = hipMemcpyAsync(&a, ws, sizeof a, hipMemcpyDeviceToHost, s)) != hipSuccess ||
+        (e = hipStreamSynchronize(s)) != hipSuccess)
+        return set_err(nullptr, DV_EHIP, "sampled accept result: %s", hipGetErrorString(e));
     std::memset(out_accept, 0, sizeof *out_accept);
     out_accept->accept_len = a.accept_len;
     out_accept->bonus_token = a.bonus;

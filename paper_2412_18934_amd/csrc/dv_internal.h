@@ -198,6 +198,17 @@ hipError_t launch_attn_merge(const AttnArgs &a, int Mpad, hipStream_t s);
 hipError_t launch_accept(const AcceptArgs &a, hipStream_t s);
 hipError_t launch_accept_sampled(const SampleArgs &a, hipStream_t s);
 
+// Allocation-free sampled acceptance: the kernel's workspace is a fixed device
+// array of the library (one copy per GPU): the result struct in its first
+// DV_NOALLOC_ACC_BYTES, then the two distribution rows of up to
+// DV_NOALLOC_MAX_VOCAB floats each.
+#define DV_NOALLOC_ACC_BYTES 1024
+#define DV_NOALLOC_SCRATCH_BYTES (DV_NOALLOC_ACC_BYTES + 2 * 4 * (size_t)DV_NOALLOC_MAX_VOCAB)
+#define DV_NOALLOC_MAX_DEVICES 64
+// device address of that array on the current device (looked up once per
+// device with hipGetSymbolAddress)
+hipError_t noalloc_scratch(void **out);
+
 // Large-M prefill (bf16 weights): activations as bf16 [2M][K] (hi rows, then
 // lo rows); GEMM results D [2M][N] fp32 (see dv_blas.cpp).
 hipError_t launch_pf_norm(const int32_t *tokens, const void *embed, const float *D, int M, int d, float *x,

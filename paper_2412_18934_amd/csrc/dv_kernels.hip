@@ -22,7 +22,9 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <mutex>
 
+#include "dv.h"
 #include "dv_internal.h"
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -2283,6 +2285,32 @@ hipError_t launch_accept_sampled(const SampleArgs &a, hipStream_t s)
     if (a.M < 1 || a.M > DV_TREE_MAX || a.V < 4 || a.V % 4) return hipErrorInvalidValue;
     hipLaunchKernelGGL(k_accept_sampled, dim3(1), dim3(SAMPLE_THREADS), 0, s, a);
     return hipGetLastError();
+}
+
+// Workspace of the allocation-free sampled acceptance (see dv.h,
+// dv_accept_sampled_noalloc).  In host code `scratch` is only a stand-in for
+// the symbol: its device address comes from hipGetSymbolAddress, once per
+// device, and only that address is ever handed to a kernel or a copy.
+static __device__ __align__(256) unsigned char scratch[DV_NOALLOC_SCRATCH_BYTES];
+
+hipError_t noalloc_scratch(void **out)
+{
+    static std::mutex mu;
+    static void *addr[DV_NOALLOC_MAX_DEVICES];
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= DV_NOALLOC_MAX_DEVICES) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        addr[dev] = p;
+    }
+    *out = addr[dev];
+    return hipSuccess;
 }
 
 hipError_t launch_kv_commit(const CommitArgs &a, int kv_bf16, hipStream_t s)

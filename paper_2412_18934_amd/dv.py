@@ -17,10 +17,12 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdv.so")
 DV_OK, DV_EINVAL, DV_ECAPACITY, DV_ESTATE, DV_EHIP, DV_ENOMEM = 0, -1, -2, -3, -4, -5
 DV_F32, DV_BF16, DV_I8 = 0, 1, 2
 DV_MAX_TREE = 64
+DV_NOALLOC_MAX_VOCAB = 262144
 DV_K_GEMM, DV_K_ATTN, DV_K_NORM, DV_K_OTHER = 0, 1, 2, 3
 
 # every symbol include/dv.h declares
 EXPORTS = ("dv_verify_init", "dv_verify_step", "dv_verify_step_sampled", "dv_accept_sampled",
+           "dv_accept_sampled_noalloc",
            "dv_draft_init", "dv_draft_forward", "dv_draft_tree",
            "dv_kv_commit", "dv_prefill", "dv_verify_free", "dv_last_error", "dv_tree_prepare",
            "dv_profile_enable", "dv_profile_read")
@@ -100,6 +102,9 @@ def lib():
         L.dv_accept_sampled.argtypes = [vp, vp, i32p, i32p, i32, vp, ctypes.c_float, f32p, f32p,
                                         ctypes.POINTER(dv_accept)]
         L.dv_accept_sampled.restype = ctypes.c_int
+        L.dv_accept_sampled_noalloc.argtypes = [vp, i32p, i32p, i32, i32, vp, ctypes.c_float, f32p, f32p, vp,
+                                                ctypes.POINTER(dv_accept)]
+        L.dv_accept_sampled_noalloc.restype = ctypes.c_int
         L.dv_draft_init.argtypes = [ctypes.POINTER(dv_config), ctypes.POINTER(dv_weights),
                                     ctypes.POINTER(dv_dgf_weights), vp, ctypes.POINTER(vp)]
         L.dv_draft_init.restype = ctypes.c_int
@@ -196,6 +201,22 @@ def dv_accept_sampled(h, logits: int, tokens, tree_parents, draft_probs: int, te
                                  ctypes.c_void_p(draft_probs or None), float(temperature), _fptr(ua), _fptr(ub),
                                  ctypes.byref(acc))
     _check(rc, h)
+    return acc
+
+
+def dv_accept_sampled_noalloc(logits: int, tokens, tree_parents, vocab: int, draft_probs: int,
+                              temperature: float, u_accept, u_bonus, stream: int = 0) -> dv_accept:
+    """Handle-free, allocation-free sampling rule (workspace: the library's
+    fixed per-GPU array).  logits / draft_probs: device addresses."""
+    t, p = _i32(tokens), _i32(tree_parents)
+    ua, ub = _f32(u_accept), _f32(u_bonus)
+    if len(ua) < len(t) or len(ub) < len(t):
+        raise ValueError("u_accept and u_bonus need one entry per tree node")
+    acc = dv_accept()
+    rc = lib().dv_accept_sampled_noalloc(ctypes.c_void_p(logits or None), _ptr(t), _ptr(p), len(t), int(vocab),
+                                         ctypes.c_void_p(draft_probs or None), float(temperature), _fptr(ua),
+                                         _fptr(ub), ctypes.c_void_p(stream or None), ctypes.byref(acc))
+    _check(rc, None)
     return acc
 
 

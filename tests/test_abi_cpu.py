@@ -141,3 +141,23 @@ def test_calls_on_null_handle_fail_cleanly():
     assert L.dv_accept_sampled(None, None, dv._ptr(t), dv._ptr(p), 1, None, 1.0, dv._fptr(u), dv._fptr(u),
                                ctypes.byref(acc)) == dv.DV_EINVAL
     L.dv_verify_free(None)
+
+
+def test_noalloc_sampling_validates_before_device_use():
+    """dv_accept_sampled_noalloc checks its arguments before any HIP call, so
+    these run without a GPU."""
+    L = dv.lib()
+    acc = dv.dv_accept()
+    t = np.zeros(1, np.int32)
+    p = np.array([-1], np.int32)
+    u = np.full(1, 0.5, np.float32)
+    fake = ctypes.c_void_p(1 << 20)   # aligned, never dereferenced on these paths
+    for vocab in (dv.DV_NOALLOC_MAX_VOCAB + 4, 6, 0):
+        assert L.dv_accept_sampled_noalloc(fake, dv._ptr(t), dv._ptr(p), 1, vocab, fake, 1.0, dv._fptr(u),
+                                           dv._fptr(u), None, ctypes.byref(acc)) == dv.DV_EINVAL
+    assert "limit" not in dv.dv_last_error(None)
+    assert L.dv_accept_sampled_noalloc(fake, dv._ptr(t), dv._ptr(p), 1, dv.DV_NOALLOC_MAX_VOCAB + 4, fake, 1.0,
+                                       dv._fptr(u), dv._fptr(u), None, ctypes.byref(acc)) == dv.DV_EINVAL
+    assert "limit" in dv.dv_last_error(None)
+    assert L.dv_accept_sampled_noalloc(None, dv._ptr(t), dv._ptr(p), 1, 1024, fake, 1.0, dv._fptr(u),
+                                       dv._fptr(u), None, ctypes.byref(acc)) == dv.DV_EINVAL
