@@ -282,7 +282,8 @@ int dv_kv_commit(dv_handle *h, dv_kv *kv, const dv_accept *accept);
  * prefill as the method's bottleneck): appends the K/V of tokens[0..n) after the kv->len
  * committed entries and commits all of them (kv->len += n).  With bf16
  * weights and n > max_tree the prompt runs as causal chunks of up to 1024
- * tokens (library GEMMs for the projections, a causal attention kernel);
+ * tokens (an MFMA GEMM with fused epilogues for the projections, a causal
+ * attention kernel);
  * otherwise as chains of at most max_tree tokens through the verify step's
  * kernels.  out_next_token (host, nullable) receives the argmax after the
  * last prompt token, the root of the first draft tree.  Synchronises the

@@ -8,7 +8,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libdv.so")
-SOURCES = ["dv_kernels.hip", "dv_engine.cpp", "dv_blas.cpp"]
+SOURCES = ["dv_kernels.hip", "dv_engine.cpp"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
@@ -29,8 +29,7 @@ def build(verbose: bool = False) -> str:
     """Always recompiles; writes libdv.so atomically next to this file."""
     tmp = LIB + ".tmp%d" % os.getpid()
     cmd = [hipcc()] + HIPCC_FLAGS + ["-I", INCLUDE, "-I", CSRC] + \
-        [os.path.join(CSRC, s) for s in SOURCES] + ["-o", tmp, "-L/opt/rocm/lib", "-lhipblaslt",
-                                                     "-Wl,-rpath,/opt/rocm/lib"]
+        [os.path.join(CSRC, s) for s in SOURCES] + ["-o", tmp]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError("hipcc failed:\n" + res.stdout + res.stderr)

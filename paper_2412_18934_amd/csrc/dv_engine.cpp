@@ -71,12 +71,14 @@ struct dv_handle {
     StepDesc *h_sd = nullptr;  // the step's tree (kernels get it by value)
     DevAccept *d_acc = nullptr, *h_acc = nullptr;
     float *logits_ws = nullptr;  // [max_tree][vocab] logits of a sampled step without out_logits
-    // large-M prefill (allocated at its first use, sized for pf_cap tokens)
-    BlasCtx *blas = nullptr;
+    // large-M prefill (allocated at its first use, sized for pf_cap tokens,
+    // a multiple of 128): residual stream, rotated queries, the split-layout
+    // operands (norm numerators, attention output, SwiGLU output) and the
+    // norms' sums of squares over 64-row slices
     int pf_cap = 0;
     int32_t *pf_tok = nullptr;
-    float *pf_x = nullptr, *pf_q = nullptr, *pf_D0 = nullptr, *pf_D1 = nullptr, *pf_D2 = nullptr;
-    uint16_t *pf_xs = nullptr;
+    float *pf_x = nullptr, *pf_q = nullptr, *pf_ssq = nullptr;
+    uint16_t *pf_us = nullptr, *pf_as = nullptr, *pf_hs = nullptr;
     // draft side
     bool draft = false;
     const void *dgf_h = nullptr, *dgf_e = nullptr, *dgf_g = nullptr;  // W_h, W_e [d][d], W_g [d][2d]
@@ -455,104 +457,157 @@ int prepare_sampled(dv_handle *h, const int32_t *tokens, const int32_t *parents,
 }
 
 // Large-M prefill: chunks of up to DV_PF_CHUNK tokens, each one causal pass
-// through all layers (plain GEMMs for the projections, the fused kernels of
-// dv_kernels.hip for everything between them).  bf16 weights only.
+// through all layers on the prefill GEMM (k_pf_gemm, fused epilogues) and
+// the causal attention kernel; bf16 weights whose projections use the packed
+// block order.
 constexpr int DV_PF_CHUNK = 1024;
+
+bool pf_supported(const dv_handle *h)
+{
+    const dv_config &c = h->cfg;
+    return h->wkind == W_BF16 && h->p_qkv.mfma && h->p_o.mfma && h->p_gu.mfma && h->p_down.mfma &&
+           c.d_model % 64 == 0 && (c.head_dim == 64 || c.head_dim == 128);
+}
 
 int pf_reserve(dv_handle *h, int tokens)
 {
-    if (h->pf_cap >= tokens) return DV_OK;
+    const int cap = round_up(std::max(tokens, 1), 128);
+    if (h->pf_cap >= cap) return DV_OK;
     const dv_config &c = h->cfg;
-    for (void *p : {(void *)h->pf_tok, (void *)h->pf_x, (void *)h->pf_q, (void *)h->pf_D0, (void *)h->pf_D1,
-                    (void *)h->pf_D2, (void *)h->pf_xs})
+    for (void *p : {(void *)h->pf_tok, (void *)h->pf_x, (void *)h->pf_q, (void *)h->pf_ssq, (void *)h->pf_us,
+                    (void *)h->pf_as, (void *)h->pf_hs})
         if (p) (void)hipFree(p);
     h->pf_tok = nullptr;
-    h->pf_x = h->pf_q = h->pf_D0 = h->pf_D1 = h->pf_D2 = nullptr;
-    h->pf_xs = nullptr;
+    h->pf_x = h->pf_q = h->pf_ssq = nullptr;
+    h->pf_us = h->pf_as = h->pf_hs = nullptr;
     h->pf_cap = 0;
-    // wide: the widest operand row (d_ffn for the prefill, 2 d_model for the
-    // draft's gate input)
-    const size_t Mc = tokens, wide = std::max(2 * c.d_model, c.d_ffn);
-    bool ok = hipMalloc((void **)&h->pf_tok, Mc * 4) == hipSuccess &&
-              hipMalloc((void **)&h->pf_x, Mc * c.d_model * 4) == hipSuccess &&
-              hipMalloc((void **)&h->pf_q, Mc * c.d_model * 4) == hipSuccess &&
-              hipMalloc((void **)&h->pf_D0, 2 * Mc * wide * 4) == hipSuccess &&
-              hipMalloc((void **)&h->pf_D1, 2 * Mc * wide * 4) == hipSuccess &&
-              hipMalloc((void **)&h->pf_D2, std::max(2 * Mc * c.d_model, (size_t)2 * c.vocab) * 4) == hipSuccess &&
-              hipMalloc((void **)&h->pf_xs, 2 * Mc * wide * 2) == hipSuccess;
-    if (!h->blas) h->blas = blas_create();
-    if (!ok || !h->blas) return set_err(h, DV_ENOMEM, "prefill workspace for %d tokens: allocation failed", tokens);
-    h->pf_cap = tokens;
+    const size_t Mc = cap, d = c.d_model, F = std::max(c.d_ffn, 1);
+    auto dalloc = [&](void **p, size_t bytes) -> bool {
+        return hipMalloc(p, bytes) == hipSuccess && hipMemset(*p, 0, bytes) == hipSuccess;
+    };
+    const bool ok = dalloc((void **)&h->pf_tok, Mc * 4) && dalloc((void **)&h->pf_x, Mc * d * 4) &&
+                    dalloc((void **)&h->pf_q, Mc * d * 4) && dalloc((void **)&h->pf_ssq, Mc * (d / 64 + 1) * 4) &&
+                    dalloc((void **)&h->pf_us, Mc * d * 4) && dalloc((void **)&h->pf_as, Mc * d * 4) &&
+                    dalloc((void **)&h->pf_hs, Mc * F * 4);
+    if (!ok) return set_err(h, DV_ENOMEM, "prefill workspace for %d tokens: allocation failed", tokens);
+    h->pf_cap = cap;
     return DV_OK;
 }
 
 int prefill_large(dv_handle *h, const int32_t *tokens, int n, dv_kv *kv, int32_t *out_next_token)
 {
     const dv_config &c = h->cfg;
-    const int d = c.d_model, F = c.d_ffn, H = c.n_heads, hd = c.head_dim, V = c.vocab;
+    const int d = c.d_model, F = c.d_ffn, H = c.n_heads, hd = c.head_dim;
     hipStream_t s = h->stream;
     int rc = pf_reserve(h, std::min(n, DV_PF_CHUNK));
     if (rc) return rc;
-    auto gemm = [&](const void *w, int m, int rows, int k, const uint16_t *B, int ldb, float *D) -> int {
-        prof_begin(h, DV_K_GEMM);
-        const int r = blas_gemm_tn(h->blas, m, rows, k, static_cast<const uint16_t *>(w), B, ldb, D, s);
-        prof_end(h);
-        return r ? set_err(h, DV_EHIP, "hipBLASLt GEMM %dx%dx%d failed", m, rows, k) : DV_OK;
-    };
     auto ck = [&](hipError_t e, const char *what) -> int { return e == hipSuccess ? DV_OK : hip_fail(h, e, what); };
     const size_t layer_kv = (size_t)H * kv->capacity * hd;
     int done = 0;
     while (done < n) {
-        const int M = std::min(DV_PF_CHUNK, n - done), P0 = kv->len;
+        const int M = std::min(DV_PF_CHUNK, n - done), Mp = round_up(M, 128), P0 = kv->len;
         HIPCHK(h, hipMemcpyAsync(h->pf_tok, tokens + done, (size_t)M * 4, hipMemcpyHostToDevice, s));
         prof_begin(h, DV_K_NORM);
-        rc = ck(launch_pf_norm(h->pf_tok, h->embed, nullptr, M, d, h->pf_x, h->layers[0].attn_norm, c.rms_eps,
-                               h->pf_xs, s), "prefill embedding norm");
+        rc = ck(launch_pf_embed(h->pf_tok, h->embed, M, Mp, d, h->layers[0].attn_norm, h->pf_x, h->pf_us, h->pf_ssq,
+                                s),
+                "prefill embedding");
         prof_end(h);
         if (rc) return rc;
+        PfArgs base{};
+        base.MT = Mp / 16;
+        base.M = M;
+        base.P0 = P0;
+        base.ssq_in = h->pf_ssq;
+        base.nsq_in = d / 64;
+        base.eps = c.rms_eps;
+        base.d = d;
+        base.q = h->pf_q;
+        base.cap = kv->capacity;
+        base.hd = hd;
+        base.rope_cos = h->rope_cos;
+        base.rope_sin = h->rope_sin;
+        base.hs = h->pf_hs;
+        base.x = h->pf_x;
+        base.us = h->pf_us;
+        base.ssq_out = h->pf_ssq;
+        auto gemm = [&](int epi, const uint16_t *packed, int rows, int K, const uint16_t *xs, const void *gain) -> int {
+            PfArgs a = base;
+            a.packed = packed;
+            a.NB = rows / 16;
+            a.K = K;
+            a.xs = xs;
+            a.gain = static_cast<const uint16_t *>(gain);
+            prof_begin(h, DV_K_GEMM);
+            const hipError_t e = launch_pf_gemm(a, epi, s);
+            prof_end(h);
+            return ck(e, "prefill GEMM");
+        };
         for (int l = 0; l < c.n_layers; ++l) {
             const LayerW &w = h->layers[l];
-            uint16_t *kc = static_cast<uint16_t *>(kv->k) + (size_t)l * layer_kv;
-            uint16_t *vc = static_cast<uint16_t *>(kv->v) + (size_t)l * layer_kv;
-            if ((rc = gemm(w.wq, d, 2 * M, d, h->pf_xs, d, h->pf_D0)) || (rc = gemm(w.wk, d, 2 * M, d, h->pf_xs, d, h->pf_D1)) ||
-                (rc = gemm(w.wv, d, 2 * M, d, h->pf_xs, d, h->pf_D2)))
-                return rc;
-            prof_begin(h, DV_K_OTHER);
-            rc = ck(launch_pf_qkv(h->pf_D0, h->pf_D1, h->pf_D2, M, P0, H, hd, kv->capacity, h->rope_cos, h->rope_sin,
-                                  h->pf_q, kc, vc, s), "prefill rotary/KV write");
-            prof_end(h);
-            if (rc) return rc;
+            base.kc = static_cast<uint16_t *>(kv->k) + (size_t)l * layer_kv;
+            base.vc = static_cast<uint16_t *>(kv->v) + (size_t)l * layer_kv;
+            if ((rc = gemm(EPI_QKV, w.pk_qkv, 3 * d, d, h->pf_us, nullptr))) return rc;
             prof_begin(h, DV_K_ATTN);
-            rc = ck(launch_attn_causal(h->pf_q, kc, vc, M, P0, H, hd, kv->capacity, h->pf_xs, s), "causal attention");
+            rc = ck(launch_attn_causal(h->pf_q, base.kc, base.vc, M, P0, H, hd, kv->capacity, Mp / 16, h->pf_as, s),
+                    "causal attention");
             prof_end(h);
             if (rc) return rc;
-            if ((rc = gemm(w.wo, d, 2 * M, d, h->pf_xs, d, h->pf_D0))) return rc;
-            prof_begin(h, DV_K_NORM);
-            rc = ck(launch_pf_norm(nullptr, nullptr, h->pf_D0, M, d, h->pf_x, w.ffn_norm, c.rms_eps, h->pf_xs, s),
-                    "prefill residual norm");
-            prof_end(h);
-            if (rc) return rc;
-            if ((rc = gemm(w.w_gate, F, 2 * M, d, h->pf_xs, d, h->pf_D0)) ||
-                (rc = gemm(w.w_up, F, 2 * M, d, h->pf_xs, d, h->pf_D1)))
-                return rc;
-            prof_begin(h, DV_K_OTHER);
-            rc = ck(launch_pf_swiglu(h->pf_D0, h->pf_D1, M, F, h->pf_xs, s), "prefill swiglu");
-            prof_end(h);
-            if (rc) return rc;
-            if ((rc = gemm(w.w_down, d, 2 * M, F, h->pf_xs, F, h->pf_D0))) return rc;
+            if ((rc = gemm(EPI_RESID, w.pk_o, d, d, h->pf_as, w.ffn_norm))) return rc;
+            if ((rc = gemm(EPI_SWIGLU, w.pk_gu, 2 * F, d, h->pf_us, nullptr))) return rc;
             const void *next_gain = l + 1 < c.n_layers ? h->layers[l + 1].attn_norm : h->final_norm;
-            prof_begin(h, DV_K_NORM);
-            rc = ck(launch_pf_norm(nullptr, nullptr, h->pf_D0, M, d, h->pf_x, next_gain, c.rms_eps, h->pf_xs, s),
-                    "prefill residual norm");
-            prof_end(h);
-            if (rc) return rc;
+            if ((rc = gemm(EPI_RESID, w.pk_down, d, F, h->pf_hs, next_gain))) return rc;
         }
         const bool last = done + M == n;
         if (last) {
-            // logits of the chunk's last token only: its hi and lo rows are M rows apart
-            if ((rc = gemm(h->lm_head, V, 2, d, h->pf_xs + (size_t)(M - 1) * d, M * d, h->pf_D2))) return rc;
+            // the next token: final norm, lm_head and argmax of the chunk's last
+            // token, on the verify step's kernels (a one-node tree)
+            NormArgs na{};
+            na.x = h->x;
+            na.x_in = h->pf_x + (size_t)(M - 1) * d;
+            na.gain = h->final_norm;
+            na.u = h->u;
+            na.us = h->u_s;
+            na.ssq = h->ssq;
+            na.d = d;
+            na.M = 1;
+            prof_begin(h, DV_K_NORM);
+            rc = ck(launch_embed_norm(na, 16, 1, s), "prefill final norm");
+            prof_end(h);
+            if (rc) return rc;
+            GemmArgs g{};
+            g.packed = h->pk_lm;
+            g.N = c.vocab;
+            g.K = d;
+            g.n_tiles = h->p_lm.n_tiles;
+            g.rb = h->p_lm.rb;
+            g.n_groups = h->p_lm.n_groups;
+            g.ks = h->p_lm.ks;
+            g.n_units = gemm_units(h->p_lm);
+            g.xs = h->u_s;
+            g.M = 1;
+            g.Mpad = 16;
+            g.ssq_in = h->ssq;
+            g.n_ssq_in = DV_NORM_SLICES;
+            g.eps = c.rms_eps;
+            g.dn = d;
+            g.arg_val = h->arg_val;
+            g.arg_idx = h->arg_idx;
+            ProfEv *ev = prof_pair(h, DV_K_GEMM);
+            rc = ck(launch_gemm(g, gemm_grid(h->p_lm, EPI_LOGITS, h->wkind, 1, h->n_cu), EPI_LOGITS, h->wkind, 1, s,
+                                ev ? ev->a : nullptr, ev ? ev->b : nullptr),
+                    "prefill lm_head");
+            if (rc) return rc;
+            AcceptArgs ac{};
+            ac.arg_val = h->arg_val;
+            ac.arg_idx = h->arg_idx;
+            ac.n_parts = h->p_lm.n_groups;
+            ac.M = 1;
+            ac.Mpad = 16;
+            ac.parents[0] = -1;
+            ac.depth[0] = 1;
+            ac.acc = h->d_acc;
             prof_begin(h, DV_K_OTHER);
-            rc = ck(launch_pf_argmax(h->pf_D2, V, h->d_acc, s), "prefill argmax");
+            rc = ck(launch_accept(ac, s), "prefill argmax");
             prof_end(h);
             if (rc) return rc;
             HIPCHK(h, hipMemcpyAsync(h->h_acc, h->d_acc, sizeof(DevAccept), hipMemcpyDeviceToHost, s));
@@ -1309,7 +1364,7 @@ int dv_prefill(dv_handle *h, const int32_t *tokens, int32_t n, dv_kv *kv, int32_
     if ((long)kv->len + n > kv->capacity || (long)kv->len + n > h->cfg.max_ctx)
         return set_err(h, DV_ECAPACITY, "prompt of %d does not fit (len %d, capacity %d, max_ctx %d)",
                        n, kv->len, kv->capacity, h->cfg.max_ctx);
-    if (h->wkind == W_BF16 && n > h->cfg.max_tree) {
+    if (pf_supported(h) && n > h->cfg.max_tree) {
         rc = prefill_large(h, tokens, n, kv, out_next_token);
         h->pending = false;
         return rc;
@@ -1359,10 +1414,9 @@ void dv_verify_free(dv_handle *h)
         if (p) (void)hipFree(p);
     if (h->tk_tok_h) (void)hipHostFree(h->tk_tok_h);
     if (h->tk_p_h) (void)hipHostFree(h->tk_p_h);
-    for (void *p : {(void *)h->pf_tok, (void *)h->pf_x, (void *)h->pf_q, (void *)h->pf_D0, (void *)h->pf_D1,
-                    (void *)h->pf_D2, (void *)h->pf_xs})
+    for (void *p : {(void *)h->pf_tok, (void *)h->pf_x, (void *)h->pf_q, (void *)h->pf_ssq, (void *)h->pf_us,
+                    (void *)h->pf_as, (void *)h->pf_hs})
         if (p) (void)hipFree(p);
-    blas_destroy(h->blas);
     delete h->h_sd;
     if (h->h_acc) (void)hipHostFree(h->h_acc);
     for (auto &e : h->ev_live) { (void)hipEventDestroy(e.a); (void)hipEventDestroy(e.b); }

@@ -209,16 +209,44 @@ hipError_t launch_accept_sampled(const SampleArgs &a, hipStream_t s);
 // device with hipGetSymbolAddress)
 hipError_t noalloc_scratch(void **out);
 
-// Large-M prefill (bf16 weights): activations as bf16 [2M][K] (hi rows, then
-// lo rows); GEMM results D [2M][N] fp32 (see dv_blas.cpp).
-hipError_t launch_pf_norm(const int32_t *tokens, const void *embed, const float *D, int M, int d, float *x,
-                          const void *gain, float eps, uint16_t *xs, hipStream_t s);
-hipError_t launch_pf_swiglu(const float *Dg, const float *Du, int M, int F, uint16_t *hs, hipStream_t s);
-hipError_t launch_pf_qkv(const float *Dq, const float *Dk, const float *Dv, int M, int P0, int H, int hd, int cap,
-                         const float *rc, const float *rs, float *q, void *kc, void *vc, hipStream_t s);
+// Large-M prefill (bf16 weights, MFMA path): the chunk's activations in split
+// layout of MT = Mp / 16 token tiles (Mp a multiple of 128), norms applied
+// by their consumers from sums of squares over 64-row slices ([Mp][d / 64]).
+struct PfArgs {
+    const uint16_t *packed;  // weights in block order
+    int NB;                  // 16-row blocks of the matrix
+    int K;                   // reduction length (multiple of 32)
+    const uint16_t *xs;      // activations, split layout of MT token tiles
+    int MT;                  // token tiles of the split layout (Mp / 16)
+    int M;                   // real tokens (the rest is padding)
+    int P0;                  // cache slot / position of token 0
+    // input norm (QKV, SWIGLU): rinv = 1/sqrt(sum_j ssq_in[m][j] / d + eps)
+    const float *ssq_in;
+    int nsq_in;
+    float eps;
+    int d;                   // d_model
+    // QKV
+    float *q;                // [Mp][d] rotated queries
+    void *kc, *vc;           // this layer's cache
+    int cap, hd;
+    const float *rope_cos, *rope_sin;
+    // SWIGLU: h in split layout (K = F)
+    uint16_t *hs;
+    // RESID: x [Mp][d] += sums; us = x * gain (split layout), ssq_out [Mp][d / 64]
+    float *x;
+    const uint16_t *gain;
+    uint16_t *us;
+    float *ssq_out;
+};
+
+// embedding rows, the first norm's numerator (split layout) and its sums of squares
+hipError_t launch_pf_embed(const int32_t *tokens, const void *embed, int M, int Mp, int d, const void *gain, float *x,
+                           uint16_t *us, float *ssq, hipStream_t s);
+// the prefill GEMM with the EPI_QKV, EPI_SWIGLU or EPI_RESID epilogue
+hipError_t launch_pf_gemm(const PfArgs &a, int epi, hipStream_t s);
+// causal attention of the chunk; output in split layout (MT token tiles)
 hipError_t launch_attn_causal(const float *q, const void *kc, const void *vc, int M, int P0, int H, int hd, int cap,
-                              uint16_t *out, hipStream_t s);
-hipError_t launch_pf_argmax(const float *Dz, int V, DevAccept *acc, hipStream_t s);
+                              int MT, uint16_t *out, hipStream_t s);
 
 // Draft side
 #define DV_TOPK_MAX 16
@@ -244,11 +272,4 @@ hipError_t launch_dgf_mix(const float *z, const float *h1, const float *h2, int 
 hipError_t launch_gather_rows(const float *src, const RowIndex &ix, int n, int d, float *dst, hipStream_t s);
 hipError_t launch_topk_probs(const float *logits, int V, const TopkArgs &a, int n_rows, hipStream_t s);
 
-struct BlasCtx;
-BlasCtx *blas_create();
-void blas_destroy(BlasCtx *c);
-// D [n][m] fp32 = B [n][k] . A [m][k]^T, A and B bf16 row-major; B rows ldb
-// elements apart.  Returns 0 on success.
-int blas_gemm_tn(BlasCtx *c, int m, int n, int k, const uint16_t *A, const uint16_t *B, int ldb, float *D,
-                 hipStream_t s);
 hipError_t launch_kv_commit(const CommitArgs &a, int kv_bf16, hipStream_t s);

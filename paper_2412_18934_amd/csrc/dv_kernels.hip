@@ -55,6 +55,14 @@ template <> struct Elem<uint16_t> {
     static __device__ __forceinline__ void store(uint16_t *p, size_t i, float v) { p[i] = f2bf(v); }
 };
 
+// Buffer resource over a device allocation (byte offsets below 2 GiB) and the
+// cache-policy bit of buffer instructions for data read once (non-temporal).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_of(const void *base)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, 0x7fffffff, 0x00020000);
+}
+#define DV_NT 2
+
 // ---------------------------------------------------------------------------
 // V cache layout: per (layer, head), 32-slot tiles one after another, each
 // tile dim-major ([hd][32]): entry (dim j, slot s) at element
@@ -1592,140 +1600,248 @@ __global__ __launch_bounds__(SAMPLE_THREADS) void k_accept_sampled(SampleArgs a)
 }
 
 // ---------------------------------------------------------------------------
-// Large-M prefill: a prompt chunk of M tokens in one causal pass.  The
-// projections there are plain GEMMs (hipBLASLt) whose activation operand is
-// bf16 [2M][K]: the hi parts (truncation) of the M tokens' rows, then their lo
-// parts (round-to-nearest-even of the remainder), so one GEMM yields D [2M][N]
-// fp32 and the fused kernels below add the two halves (hi first).
-
-// hi/lo of four consecutive values into rows i (hi) and M + i (lo)
-__device__ __forceinline__ void store_hilo4(uint16_t *xs, size_t hi_off, size_t lo_off, float4 v)
-{
-    const float f[4] = {v.x, v.y, v.z, v.w};
-    uint32_t hi[2], lo[2];
-#pragma unroll
-    for (int p = 0; p < 2; ++p) {
-        uint32_t h2 = 0, l2 = 0;
-#pragma unroll
-        for (int q = 0; q < 2; ++q) {
-            const float x = f[2 * p + q];
-            const float h = __uint_as_float(__float_as_uint(x) & 0xffff0000u);
-            h2 |= (__float_as_uint(x) >> 16) << (16 * q);
-            l2 |= (uint32_t)f2bf(x - h) << (16 * q);
-        }
-        hi[p] = h2;
-        lo[p] = l2;
-    }
-    *reinterpret_cast<uint2 *>(xs + hi_off) = make_uint2(hi[0], hi[1]);
-    *reinterpret_cast<uint2 *>(xs + lo_off) = make_uint2(lo[0], lo[1]);
-}
+// Large-M prefill: a prompt chunk of M tokens (padded to Mp, a multiple of
+// 128) in one causal pass.  The projections are a dense contraction here, so
+// they run on an MFMA GEMM over the packed weights of the verify path (block
+// (k-step s, 16-row block gb) at (s NB + gb) 512) and split-layout
+// activations of the whole chunk (MT = Mp / 16 token tiles), with the verify
+// path's epilogues fused: rotary + K/V write, SwiGLU, residual + the next
+// norm's input.  Every norm's 1/rms, a per-token scalar, is applied by its
+// consumer's epilogue from sums of squares over 64-row slices (Mp x d / 64
+// partials), so no fp32 GEMM output goes through HBM.
 
 constexpr int PF_THREADS = 256;
 
-__device__ __forceinline__ float pf_block_sum(float v, float *red)
+// Embedding rows of the chunk: x = E[token], the first norm's numerator
+// x * gain in split layout and the sums of squares of 64-column slices;
+// tokens >= M get zeros.  One workgroup per token, 4 columns per thread.
+__global__ __launch_bounds__(PF_THREADS) void k_pf_embed(const int32_t *tokens, const uint16_t *embed, int M, int d,
+                                                         int MT, const uint16_t *gain, float *x, uint16_t *us,
+                                                         float *ssq)
 {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
-    __syncthreads();
-    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
-    __syncthreads();
-    float r = 0.f;
-#pragma unroll
-    for (int w = 0; w < PF_THREADS / 64; ++w) r += red[w];
-    return r;
+    const int m = blockIdx.x, nsq = d / 64;
+    for (int k = 4 * threadIdx.x; k < d; k += 4 * PF_THREADS) {
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (m < M) {
+            const uint2 e = *reinterpret_cast<const uint2 *>(embed + (size_t)tokens[m] * d + k);
+            v = make_float4(__uint_as_float(e.x << 16), __uint_as_float(e.x & 0xffff0000u), __uint_as_float(e.y << 16),
+                            __uint_as_float(e.y & 0xffff0000u));
+        }
+        *reinterpret_cast<float4 *>(x + (size_t)m * d + k) = v;
+        store_split4(us, m, k, MT,
+                     make_float4(v.x * bf2f(gain[k]), v.y * bf2f(gain[k + 1]), v.z * bf2f(gain[k + 2]),
+                                 v.w * bf2f(gain[k + 3])));
+        // 16 neighbouring threads hold one 64-column slice
+        float ss = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, v.w * v.w)));
+        ss += __shfl_xor(ss, 1);
+        ss += __shfl_xor(ss, 2);
+        ss += __shfl_xor(ss, 4);
+        ss += __shfl_xor(ss, 8);
+        if ((threadIdx.x & 15) == 0) ssq[(size_t)m * nsq + k / 64] = ss;
+    }
 }
 
-// One token per workgroup: x = (layer 0) the embedding row, or x + D[i] +
-// D[M + i] (a residual projection's two halves); then RMSNorm with gain g into
-// rows i / M + i of xs.  d % 4 == 0, d <= 4 * PF_THREADS * 8.
-__global__ __launch_bounds__(PF_THREADS) void k_pf_norm(const int32_t *tokens, const uint16_t *embed,
-                                                        const float *D, int M, int d, float *x,
-                                                        const uint16_t *gain, float eps, uint16_t *xs)
+// The prefill GEMM.  Workgroup = NWR x NWT waves over 64 NWR rows (4 blocks
+// per wave) x 16 TT NWT tokens (TT token tiles per wave).  Per k-step each
+// wave loads its 4 weight blocks into registers, the workgroup stages the
+// activation slab of its token tiles (hi + lo) in LDS (two buffers), and
+// each wave runs 8 TT MFMAs (16x16x32 bf16, hi and lo into the same
+// accumulator).  A wave's loads return in
+// order, so weights and activations share one lead of PF_LEAD k-steps.
+constexpr int PF_LEAD = 4;
+
+
+template <int EPI, int NWR, int NWT, int TT>
+__global__ __launch_bounds__(64 * NWR * NWT) void k_pf_gemm(PfArgs a)
 {
-    __shared__ float red[PF_THREADS / 64];
-    const int i = blockIdx.x;
-    float4 v[8];
-    float ss = 0.f;
+    constexpr int NW = NWR * NWT, NT = 64 * NW, BW = 4, XT = NWT * TT;
+    constexpr int XL = XT * 2 * 64 / NT;  // activation u32x4 each thread stages per k-step
+    static_assert(XT * 2 * 64 % NT == 0, "activation slab must split evenly");
+    __shared__ u32x4 xsm[2][XT * 2 * 64];
+    __shared__ float rinv_s[16 * XT];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, tid = threadIdx.x;
+    const int wr = wave % NWR, wt = wave / NWR;
+    // 1-D grid, XCD-aware: workgroups are dispatched to the 8 XCDs round
+    // robin, so the token tiles of one row tile get the same blockIdx % 8 and
+    // share that XCD's L2 for the row tile's weights
+    const int n_tt = a.MT / XT, n_rt = (a.NB + NWR * BW - 1) / (NWR * BW);
+    const int xcd = blockIdx.x & 7, qq = blockIdx.x >> 3;
+    const int rtile = (qq / n_tt) * 8 + xcd;
+    if (rtile >= n_rt) return;  // padding of the row tiles to a multiple of 8
+    const int tt0 = (qq % n_tt) * XT;                        // first token tile of the workgroup
+    const int gb0 = (rtile * NWR + wr) * BW;                 // first block of this wave
+    const int S = a.K / 32;
+    if (EPI != EPI_RESID) {
+        for (int m = tid; m < 16 * XT; m += NT) {
+            const float *p = a.ssq_in + (size_t)(tt0 * 16 + m) * a.nsq_in;
+            float sum = 0.f;
+            for (int c = 0; c < a.nsq_in; ++c) sum += p[c];
+            rinv_s[m] = 1.0f / sqrtf(sum / (float)a.d + a.eps);
+        }
+    }
+    // buffer loads: the per-lane byte offsets stay fixed, a scalar offset moves
+    // by one k-step (so no address register is rewritten while a load into a
+    // neighbouring register is in flight); blocks past NB re-read the last
+    // block (their sums are dropped)
+    const __amdgpu_buffer_rsrc_t rw = rsrc_of(a.packed), rx = rsrc_of(a.xs);
+    uint32_t wofs[BW], xofs[XL];
 #pragma unroll
-    for (int c = 0; c < 8; ++c) {
-        const int k = 4 * (threadIdx.x + PF_THREADS * c);
-        v[c] = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (k < d) {
-            if (embed) {
-                const uint2 e = *reinterpret_cast<const uint2 *>(embed + (size_t)tokens[i] * d + k);
-                v[c] = make_float4(__uint_as_float(e.x << 16), __uint_as_float(e.x & 0xffff0000u),
-                                   __uint_as_float(e.y << 16), __uint_as_float(e.y & 0xffff0000u));
-            } else {
-                const float4 a = *reinterpret_cast<const float4 *>(x + (size_t)i * d + k);
-                const float4 hi = *reinterpret_cast<const float4 *>(D + (size_t)i * d + k);
-                const float4 lo = *reinterpret_cast<const float4 *>(D + (size_t)(M + i) * d + k);
-                v[c] = make_float4(a.x + (hi.x + lo.x), a.y + (hi.y + lo.y), a.z + (hi.z + lo.z),
-                                   a.w + (hi.w + lo.w));
+    for (int b = 0; b < BW; ++b) wofs[b] = (uint32_t)(min(gb0 + b, a.NB - 1) * 1024 + lane * 16);
+#pragma unroll
+    for (int i = 0; i < XL; ++i) xofs[i] = (uint32_t)((tt0 * 128 + tid + NT * i) * 16);
+    const uint32_t wstep = (uint32_t)a.NB * 1024u, xstep = (uint32_t)a.MT * 2048u;
+    u32x4 wb[PF_LEAD][BW], stg[PF_LEAD][XL];
+    auto fetch = [&](int j, int st) {
+#pragma unroll
+        for (int b = 0; b < BW; ++b)
+            wb[j][b] = __builtin_amdgcn_raw_buffer_load_b128(rw, wofs[b], (uint32_t)st * wstep, DV_NT);
+#pragma unroll
+        for (int i = 0; i < XL; ++i) stg[j][i] = __builtin_amdgcn_raw_buffer_load_b128(rx, xofs[i], (uint32_t)st * xstep, 0);
+    };
+    auto stash = [&](int j, int buf) {
+#pragma unroll
+        for (int i = 0; i < XL; ++i) xsm[buf][tid + NT * i] = stg[j][i];
+    };
+    f32x4 acc[BW][TT];
+#pragma unroll
+    for (int b = 0; b < BW; ++b)
+#pragma unroll
+        for (int t = 0; t < TT; ++t) acc[b][t] = (f32x4){0.f, 0.f, 0.f, 0.f};
+    auto mfma = [&](int j, int buf) {
+#pragma unroll
+        for (int t = 0; t < TT; ++t) {
+            const bf16x8 hi = __builtin_bit_cast(bf16x8, xsm[buf][((wt * TT + t) * 2 + 0) * 64 + lane]);
+            const bf16x8 lo = __builtin_bit_cast(bf16x8, xsm[buf][((wt * TT + t) * 2 + 1) * 64 + lane]);
+#pragma unroll
+            for (int b = 0; b < BW; ++b) {
+                const bf16x8 w = __builtin_bit_cast(bf16x8, wb[j][b]);
+                acc[b][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, hi, acc[b][t], 0, 0, 0);
+                acc[b][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, lo, acc[b][t], 0, 0, 0);
             }
-            *reinterpret_cast<float4 *>(x + (size_t)i * d + k) = v[c];
-            ss += v[c].x * v[c].x + v[c].y * v[c].y + v[c].z * v[c].z + v[c].w * v[c].w;
         }
-    }
-    const float rinv = 1.f / sqrtf(pf_block_sum(ss, red) / (float)d + eps);
+    };
+    // Loads and stashes are issued unconditionally (k-steps past the end
+    // re-read the last one and are never used), so the number of loads in
+    // flight behind each one is the same on every path and every wait is the
+    // one the pipeline needs.
 #pragma unroll
-    for (int c = 0; c < 8; ++c) {
-        const int k = 4 * (threadIdx.x + PF_THREADS * c);
-        if (k < d) {
-            const float4 u = make_float4(v[c].x * rinv * bf2f(gain[k]), v[c].y * rinv * bf2f(gain[k + 1]),
-                                         v[c].z * rinv * bf2f(gain[k + 2]), v[c].w * rinv * bf2f(gain[k + 3]));
-            store_hilo4(xs, (size_t)i * d + k, (size_t)(M + i) * d + k, u);
+    for (int j = 0; j < PF_LEAD; ++j) fetch(j, min(j, S - 1));
+    stash(0, 0);
+    __syncthreads();
+    // k-step st uses register slot st % PF_LEAD and LDS buffer st % 2
+    for (int s0 = 0; s0 < S; s0 += PF_LEAD) {
+#pragma unroll
+        for (int j = 0; j < PF_LEAD; ++j) {
+            const int st = s0 + j;
+            if (st < S) mfma(j, st & 1);
+            stash((j + 1) % PF_LEAD, (st + 1) & 1);
+            fetch(j, min(st + PF_LEAD, S - 1));
+            __syncthreads();
         }
     }
-}
 
-// silu(gate) * up of the two GEMM results into the down projection's operand
-__global__ __launch_bounds__(PF_THREADS) void k_pf_swiglu(const float *Dg, const float *Du, int M, int F,
-                                                          uint16_t *hs)
-{
-    const size_t e = 4 * ((size_t)blockIdx.x * PF_THREADS + threadIdx.x);
-    if (e >= (size_t)M * F) return;
-    const size_t i = e / F, k = e - i * F;
-    const float4 gh = *reinterpret_cast<const float4 *>(Dg + e);
-    const float4 gl = *reinterpret_cast<const float4 *>(Dg + (size_t)M * F + e);
-    const float4 uh = *reinterpret_cast<const float4 *>(Du + e);
-    const float4 ul = *reinterpret_cast<const float4 *>(Du + (size_t)M * F + e);
-    const float4 h = make_float4(silu(gh.x + gl.x) * (uh.x + ul.x), silu(gh.y + gl.y) * (uh.y + ul.y),
-                                 silu(gh.z + gl.z) * (uh.z + ul.z), silu(gh.w + gl.w) * (uh.w + ul.w));
-    store_hilo4(hs, i * F + k, (size_t)(M + i) * F + k, h);
-}
-
-// Rotary embedding of q and k at positions P0 + i, q stored fp32 [M][d], k
-// and v rounded to bf16 into cache slots P0 + i.  Workgroup = (64 tokens, one
-// head); V goes through LDS so that each cache column is written contiguously.
-template <int HD>
-__global__ __launch_bounds__(PF_THREADS) void k_pf_qkv(const float *Dq, const float *Dk, const float *Dv, int M,
-                                                       int P0, int H, int cap, const float *rc, const float *rs,
-                                                       float *q, uint16_t *kc, uint16_t *vc)
-{
-    constexpr int HALF = HD / 2;
-    __shared__ float vt[HD][64 + 1];
-    const int i0 = blockIdx.x * 64, h = blockIdx.y, d = H * HD;
-    for (int e = threadIdx.x; e < 64 * HALF; e += PF_THREADS) {
-        const int t = e / HALF, j = e - t * HALF, i = i0 + t;
-        if (i >= M) continue;
-        const size_t c1 = (size_t)h * HD + j, c2 = c1 + HALF;
-        const size_t rh = (size_t)i * d, rl = (size_t)(M + i) * d;
-        const float c = rc[(size_t)(P0 + i) * HALF + j], s = rs[(size_t)(P0 + i) * HALF + j];
-        const float q1 = Dq[rh + c1] + Dq[rl + c1], q2 = Dq[rh + c2] + Dq[rl + c2];
-        q[rh + c1] = q1 * c - q2 * s;
-        q[rh + c2] = q2 * c + q1 * s;
-        const float k1 = Dk[rh + c1] + Dk[rl + c1], k2 = Dk[rh + c2] + Dk[rl + c2];
-        uint16_t *kr = kc + ((size_t)h * cap + P0 + i) * HD;
-        kr[j] = f2bf(k1 * c - k2 * s);
-        kr[j + HALF] = f2bf(k2 * c + k1 * s);
-        vt[j][t] = Dv[rh + c1] + Dv[rl + c1];
-        vt[j + HALF][t] = Dv[rh + c2] + Dv[rl + c2];
-    }
-    __syncthreads();
-    const int nt = min(64, M - i0);
-    for (int e = threadIdx.x; e < HD * 64; e += PF_THREADS) {
-        const int j = e / 64, t = e - j * 64;
-        if (t < nt) vc[(size_t)h * HD * cap + v_index(j, P0 + i0 + t, HD)] = f2bf(vt[j][t]);
+    // ---- epilogues: lane l holds rows 4 (l / 16) + jj of block gb0 + b for
+    // token (tt0 + wt TT + t) 16 + l % 16
+    const int n16 = lane & 15, r4 = 4 * (lane >> 4);
+    if (EPI == EPI_QKV) {
+        const int per_seg = a.d / DV_GEMM_TILE, per_head = a.hd / DV_GEMM_TILE, half = a.hd / 2;
+#pragma unroll
+        for (int p = 0; p < BW / 2; ++p) {
+            const int gb = gb0 + 2 * p;
+            if (gb >= a.NB) break;
+            const int tile = gb >> 1, seg = tile / per_seg, tt = tile - seg * per_seg;
+            const int h = tt / per_head, j0 = (tt - h * per_head) * 16 + r4;
+#pragma unroll
+            for (int t = 0; t < TT; ++t) {
+                const int ml = (wt * TT + t) * 16 + n16, m = tt0 * 16 + ml;
+                if (m >= a.M) continue;
+                const float ri = rinv_s[ml];
+                float y1[4], y2[4];
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) {
+                    y1[jj] = acc[2 * p][t][jj] * ri;
+                    y2[jj] = acc[2 * p + 1][t][jj] * ri;
+                }
+                const int pos = a.P0 + m;
+                if (seg < 2) {
+#pragma unroll
+                    for (int jj = 0; jj < 4; ++jj) {
+                        const float c = a.rope_cos[(size_t)pos * half + j0 + jj];
+                        const float sn = a.rope_sin[(size_t)pos * half + j0 + jj];
+                        const float o1 = y1[jj] * c - y2[jj] * sn, o2 = y2[jj] * c + y1[jj] * sn;
+                        y1[jj] = o1;
+                        y2[jj] = o2;
+                    }
+                }
+                if (seg == 0) {
+                    float *qr = a.q + (size_t)m * a.d + h * a.hd + j0;
+                    *reinterpret_cast<float4 *>(qr) = make_float4(y1[0], y1[1], y1[2], y1[3]);
+                    *reinterpret_cast<float4 *>(qr + half) = make_float4(y2[0], y2[1], y2[2], y2[3]);
+                } else if (seg == 1) {  // K: [H][cap][hd]
+                    uint16_t *kr = reinterpret_cast<uint16_t *>(a.kc) + ((size_t)h * a.cap + pos) * a.hd + j0;
+                    *reinterpret_cast<uint2 *>(kr) = make_uint2(f2bf(y1[0]) | (uint32_t)f2bf(y1[1]) << 16,
+                                                                f2bf(y1[2]) | (uint32_t)f2bf(y1[3]) << 16);
+                    *reinterpret_cast<uint2 *>(kr + half) = make_uint2(f2bf(y2[0]) | (uint32_t)f2bf(y2[1]) << 16,
+                                                                       f2bf(y2[2]) | (uint32_t)f2bf(y2[3]) << 16);
+                } else {                // V: [H][cap/32][hd][32]
+                    uint16_t *vh = reinterpret_cast<uint16_t *>(a.vc) + (size_t)h * a.hd * a.cap;
+#pragma unroll
+                    for (int jj = 0; jj < 4; ++jj) {
+                        vh[v_index(j0 + jj, pos, a.hd)] = f2bf(y1[jj]);
+                        vh[v_index(j0 + jj + half, pos, a.hd)] = f2bf(y2[jj]);
+                    }
+                }
+            }
+        }
+    } else if (EPI == EPI_SWIGLU) {
+        // gate block 2p and up block 2p + 1 hold h columns 16 (gb / 2) + ...
+#pragma unroll
+        for (int p = 0; p < BW / 2; ++p) {
+            const int gb = gb0 + 2 * p;
+            if (gb >= a.NB) break;
+            const int f0 = 16 * (gb >> 1) + r4;
+#pragma unroll
+            for (int t = 0; t < TT; ++t) {
+                const int ml = (wt * TT + t) * 16 + n16, m = tt0 * 16 + ml;
+                float hv[4] = {0.f, 0.f, 0.f, 0.f};
+                if (m < a.M) {
+                    const float ri = rinv_s[ml];
+#pragma unroll
+                    for (int jj = 0; jj < 4; ++jj) hv[jj] = silu(acc[2 * p][t][jj] * ri) * (acc[2 * p + 1][t][jj] * ri);
+                }
+                store_split4(a.hs, m, f0, a.MT, make_float4(hv[0], hv[1], hv[2], hv[3]));
+            }
+        }
+    } else {  // EPI_RESID
+        if (gb0 < a.NB) {
+            const int nsq = a.d / 64;
+#pragma unroll
+            for (int t = 0; t < TT; ++t) {
+                const int ml = (wt * TT + t) * 16 + n16, m = tt0 * 16 + ml;
+                float ss = 0.f;
+#pragma unroll
+                for (int b = 0; b < BW; ++b) {
+                    const int r = 16 * (gb0 + b) + r4;
+                    float4 xv = make_float4(0.f, 0.f, 0.f, 0.f);
+                    if (m < a.M) {
+                        float *xp = a.x + (size_t)m * a.d + r;
+                        xv = *reinterpret_cast<const float4 *>(xp);
+                        xv.x += acc[b][t][0];
+                        xv.y += acc[b][t][1];
+                        xv.z += acc[b][t][2];
+                        xv.w += acc[b][t][3];
+                        *reinterpret_cast<float4 *>(xp) = xv;
+                    }
+                    ss = fmaf(xv.x, xv.x, fmaf(xv.y, xv.y, fmaf(xv.z, xv.z, fmaf(xv.w, xv.w, ss))));
+                    store_split4(a.us, m, r, a.MT,
+                                 make_float4(xv.x * bf2f(a.gain[r]), xv.y * bf2f(a.gain[r + 1]),
+                                             xv.z * bf2f(a.gain[r + 2]), xv.w * bf2f(a.gain[r + 3])));
+                }
+                ss += __shfl_xor(ss, 16);
+                ss += __shfl_xor(ss, 32);
+                if (lane < 16) a.ssq_out[(size_t)m * nsq + gb0 / 4] = ss;
+            }
+        }
     }
 }
 
@@ -1736,13 +1852,13 @@ __global__ __launch_bounds__(PF_THREADS) void k_pf_qkv(const float *Dq, const fl
 // global loads are in flight while the current one is used), and each wave
 // uses the tiles up to its own last query.  The scores and the running
 // softmax follow the tree-attention kernel (MFMA with q split in hi + lo,
-// exp2 in log2 units); the output goes to rows i / M + i of the O
-// projection's operand.  Grid (heads, query blocks) with the last query
+// exp2 in log2 units); the output goes to the O projection's operand (split
+// layout of MT token tiles).  Grid (heads, query blocks) with the last query
 // block first: workgroups are dispatched in order, so the longest ones (the
 // most keys) start first and the short ones fill in behind them.
 template <int HD>
 __global__ __launch_bounds__(256) void k_attn_causal(const float *q, const uint16_t *kc_l, const uint16_t *vc_l,
-                                                     int M, int P0, int H, int cap, uint16_t *out)
+                                                     int M, int P0, int H, int cap, int MT, uint16_t *out)
 {
     constexpr int NC = HD / 32, ND = HD / 16;
     constexpr int KROW = HD * 2 + 16;          // bytes per staged key row (padded)
@@ -1898,43 +2014,7 @@ __global__ __launch_bounds__(256) void k_attn_causal(const float *q, const uint1
         const int i = qb + 4 * g + j;
         if (i >= M) continue;
 #pragma unroll
-        for (int dt = 0; dt < ND; ++dt) {
-            const float r = o[dt][j] / lr[j];
-            const float hi = __uint_as_float(__float_as_uint(r) & 0xffff0000u);
-            const size_t col = (size_t)h * HD + dt * 16 + n;
-            out[(size_t)i * D + col] = (uint16_t)(__float_as_uint(r) >> 16);
-            out[(size_t)(M + i) * D + col] = f2bf(r - hi);
-        }
-    }
-}
-
-// argmax (lowest id on ties) of hi + lo rows D[0][v] + D[1][v]
-__global__ __launch_bounds__(1024) void k_pf_argmax(const float *Dz, int V, DevAccept *acc)
-{
-    __shared__ float bv[16];
-    __shared__ int bi[16];
-    float best = -INFINITY;
-    int idx = 0x7fffffff;
-    for (int v = threadIdx.x; v < V; v += 1024) {
-        const float z = Dz[v] + Dz[V + v];
-        if (z > best || (z == best && v < idx)) { best = z; idx = v; }
-    }
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-        const float v2 = __shfl_xor(best, off);
-        const int i2 = __shfl_xor(idx, off);
-        arg_better(best, idx, v2, i2);
-    }
-    if ((threadIdx.x & 63) == 0) {
-        bv[threadIdx.x >> 6] = best;
-        bi[threadIdx.x >> 6] = idx;
-    }
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        best = bv[0];
-        idx = bi[0];
-        for (int w = 1; w < 16; ++w) arg_better(best, idx, bv[w], bi[w]);
-        acc->argmax[0] = idx;
+        for (int dt = 0; dt < ND; ++dt) store_split(out, i, h * HD + dt * 16 + n, MT, o[dt][j] / lr[j]);
     }
 }
 
@@ -2323,49 +2403,43 @@ hipError_t launch_kv_commit(const CommitArgs &a, int kv_bf16, hipStream_t s)
     return hipGetLastError();
 }
 
-hipError_t launch_pf_norm(const int32_t *tokens, const void *embed, const float *D, int M, int d, float *x,
-                          const void *gain, float eps, uint16_t *xs, hipStream_t s)
+hipError_t launch_pf_embed(const int32_t *tokens, const void *embed, int M, int Mp, int d, const void *gain, float *x,
+                           uint16_t *us, float *ssq, hipStream_t s)
 {
-    if (d % 4 || d > 4 * PF_THREADS * 8 || M < 1) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_pf_norm, dim3(M), dim3(PF_THREADS), 0, s, tokens, static_cast<const uint16_t *>(embed), D,
-                       M, d, x, static_cast<const uint16_t *>(gain), eps, xs);
+    if (d % 64 || Mp % 16 || M < 1 || M > Mp) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_pf_embed, dim3(Mp), dim3(PF_THREADS), 0, s, tokens, static_cast<const uint16_t *>(embed), M, d,
+                       Mp / 16, static_cast<const uint16_t *>(gain), x, us, ssq);
     return hipGetLastError();
 }
 
-hipError_t launch_pf_swiglu(const float *Dg, const float *Du, int M, int F, uint16_t *hs, hipStream_t s)
+hipError_t launch_pf_gemm(const PfArgs &a, int epi, hipStream_t s)
 {
-    if (F % 4 || M < 1) return hipErrorInvalidValue;
-    const size_t n4 = (size_t)M * F / 4;
-    hipLaunchKernelGGL(k_pf_swiglu, dim3((unsigned)((n4 + PF_THREADS - 1) / PF_THREADS)), dim3(PF_THREADS), 0, s,
-                       Dg, Du, M, F, hs);
-    return hipGetLastError();
-}
-
-hipError_t launch_pf_qkv(const float *Dq, const float *Dk, const float *Dv, int M, int P0, int H, int hd, int cap,
-                         const float *rc, const float *rs, float *q, void *kc, void *vc, hipStream_t s)
-{
-    const dim3 grid((M + 63) / 64, H);
-    uint16_t *k16 = static_cast<uint16_t *>(kc), *v16 = static_cast<uint16_t *>(vc);
-    if (hd == 128) hipLaunchKernelGGL(k_pf_qkv<128>, grid, dim3(PF_THREADS), 0, s, Dq, Dk, Dv, M, P0, H, cap, rc, rs, q, k16, v16);
-    else if (hd == 64) hipLaunchKernelGGL(k_pf_qkv<64>, grid, dim3(PF_THREADS), 0, s, Dq, Dk, Dv, M, P0, H, cap, rc, rs, q, k16, v16);
-    else return hipErrorInvalidValue;
+    if (a.K % 32 || a.NB < 1 || a.MT % 8 || a.d % 64 || a.M < 1 || a.M > 16 * a.MT) return hipErrorInvalidValue;
+    // 8 waves of 64 rows x 64 tokens: 256 rows x 128 tokens per workgroup;
+    // 1-D grid of (token tiles) x (row tiles rounded up to a multiple of 8)
+    const int n_rt = (a.NB + 15) / 16;
+    const dim3 grid((a.MT / 8) * ((n_rt + 7) / 8 * 8));
+    if (epi == EPI_RESID) {
+        hipLaunchKernelGGL((k_pf_gemm<EPI_RESID, 4, 2, 4>), grid, dim3(512), 0, s, a);
+    } else if (epi == EPI_QKV) {
+        if (a.hd != 64 && a.hd != 128) return hipErrorInvalidValue;
+        hipLaunchKernelGGL((k_pf_gemm<EPI_QKV, 4, 2, 4>), grid, dim3(512), 0, s, a);
+    } else if (epi == EPI_SWIGLU) {
+        hipLaunchKernelGGL((k_pf_gemm<EPI_SWIGLU, 4, 2, 4>), grid, dim3(512), 0, s, a);
+    } else {
+        return hipErrorInvalidValue;
+    }
     return hipGetLastError();
 }
 
 hipError_t launch_attn_causal(const float *q, const void *kc, const void *vc, int M, int P0, int H, int hd, int cap,
-                              uint16_t *out, hipStream_t s)
+                              int MT, uint16_t *out, hipStream_t s)
 {
     const dim3 grid(H, (M + 63) / 64);
     const uint16_t *k16 = static_cast<const uint16_t *>(kc), *v16 = static_cast<const uint16_t *>(vc);
-    if (hd == 128) hipLaunchKernelGGL(k_attn_causal<128>, grid, dim3(256), 0, s, q, k16, v16, M, P0, H, cap, out);
-    else if (hd == 64) hipLaunchKernelGGL(k_attn_causal<64>, grid, dim3(256), 0, s, q, k16, v16, M, P0, H, cap, out);
+    if (hd == 128) hipLaunchKernelGGL(k_attn_causal<128>, grid, dim3(256), 0, s, q, k16, v16, M, P0, H, cap, MT, out);
+    else if (hd == 64) hipLaunchKernelGGL(k_attn_causal<64>, grid, dim3(256), 0, s, q, k16, v16, M, P0, H, cap, MT, out);
     else return hipErrorInvalidValue;
-    return hipGetLastError();
-}
-
-hipError_t launch_pf_argmax(const float *Dz, int V, DevAccept *acc, hipStream_t s)
-{
-    hipLaunchKernelGGL(k_pf_argmax, dim3(1), dim3(1024), 0, s, Dz, V, acc);
     return hipGetLastError();
 }
 

@@ -1,7 +1,7 @@
-"""Large-M prefill on the GPU (bf16 weights, prompts longer than max_tree: plain
-GEMMs for the projections, fused norm / rotary / SwiGLU kernels, causal
-attention) vs the oracle's prefill (the prompt as one chain through the stack,
-float64), through the C ABI.
+"""Large-M prefill on the GPU (bf16 weights, prompts longer than max_tree: the
+prefill GEMM with fused rotary + KV write / SwiGLU / residual + norm
+epilogues, causal attention) vs the oracle's prefill (the prompt as one chain
+through the stack, float64), through the C ABI.
 
 Bars: every new cache row within one bf16 rounding step (2^-7 relative) plus
 the accumulated error: 1e-4 of the rows' RMS in layer 0, 1e-2 in later layers.
@@ -12,9 +12,11 @@ the 280 000 layer-0 entries of a 1100-token prompt) the cached entries differ by
 one bf16 step, and every later layer inherits that through attention over
 all earlier tokens (measured: median 2.5e-4, largest 7.3e-3 of the RMS).  The
 next token equal to the oracle's argmax of the last logits unless its top-2 gap
-is within 4e-2 (then a maximiser within that margin); a verify step on each
-side's own prefilled cache within 4e-2 (twice the step bar: the caches differ
-by the rounding ties above); two prefills write identical bytes.
+is within 4e-2 (then a maximiser within that margin); a verify step on the
+prefilled cache within the step bar 2e-2, both against the oracle on the
+same cache bytes and against the oracle on its own prefilled cache (the
+caches differ by the rounding ties above); two prefills write identical
+bytes.
 """
 import numpy as np
 import pytest
@@ -71,16 +73,24 @@ def test_prefill_matches_oracle(case, n, p0):
     kv_ref, logits = ov.prefill(om, prompt, kv=kv_o)
     _check_rows(case, kv, kv_ref, p0, n)
     _check_next(nxt, logits[-1])
-    # a verify step on the prefilled cache, each side from its own cache
+    # a verify step on the prefilled cache at the step bar: against the
+    # oracle on the same cache bytes (the GPU's, downloaded), and against the
+    # oracle on its own prefilled cache, which differs from the GPU's by the
+    # propagated bf16 rounding ties above (observed: 1.4e-4 to 1.7e-4 on the
+    # same bytes, 1.8e-3 to 3.2e-3 on each side's own cache, 65 to 1100 tokens)
     root = int(ov.argmax_lowest(logits[-1:])[0])
     toks, par = synth.random_tree(204 + n, 12, 4, case.cfg.vocab)
     toks[0] = root
+    acc, lg = case.step(kv, toks, par)
+    kv_gpu = ov.kv_from_raw([kv.layer_host(l, p0 + n) for l in range(case.cfg.n_layers)])
+    same = ov.verify_step(om, kv_gpu, toks, par)
+    same["tokens"], same["parents"] = toks, par
+    err_same, _ = compare_step(acc, lg, same, 2e-2)
     ref = ov.verify_step(om, kv_ref, toks, par)
     ref["tokens"], ref["parents"] = toks, par
-    acc, lg = case.step(kv, toks, par)
-    # the two caches differ by the propagated bf16 rounding ties above, so
-    # this step gets twice the step bar (observed up to 2.4e-2 at 1100 tokens)
-    compare_step(acc, lg, ref, 4e-2)
+    err_own, _ = compare_step(acc, lg, ref, 2e-2)
+    print("[prefill] n=%d p0=%d: verify step on the same cache %.3g, on each side's own cache %.3g"
+          % (n, p0, err_same, err_own), flush=True)
 
 
 def test_prefill_is_deterministic(case):
