@@ -244,9 +244,10 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
 {
     const dv_config &c = h->cfg;
     StepDesc *sd = h->h_sd;
-    const int M = sd->M, Mpad = sd->Mpad, P = sd->P;
+    const int M = sd->M, Mpad = sd->Mpad, P = sd->P, half = sd->half;
     const int d = c.d_model, hd = c.head_dim, H = c.n_heads, F = c.d_ffn;
     hipStream_t s = h->stream;
+    const int mt = half ? 0 : Mpad / 16;  // token tiles of the split activations (0: half layout)
 
     const size_t layer_kv = (size_t)H * kv->capacity * hd * h->esz;
     // attention: the P + M keys of each head are split evenly into
@@ -268,6 +269,7 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
     GemmArgs g{};
     g.M = M;
     g.Mpad = Mpad;
+    g.half = half;
     g.cap = kv->capacity;
     g.P = P;
     g.hd = hd;
@@ -296,6 +298,7 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
     aa.tm.M = M;
     aa.tm.P = P;
     aa.tm.Mpad = Mpad;
+    aa.tm.half = half;
     std::memcpy(aa.tm.anc, sd->anc, sizeof aa.tm.anc);
     aa.part_o = h->part_o;
     aa.part_m = h->part_m;
@@ -324,7 +327,7 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
         a.x = x;
         a.out = out;
         a.gain = gain;
-        const int grid = gemm_grid(p, epi, h->wkind, Mpad / 16, h->n_cu);
+        const int grid = gemm_grid(p, epi, h->wkind, mt, h->n_cu);
         ProfEv *ev = prof_pair(h, DV_K_GEMM);
         hipError_t e = launch_gemm(a, grid, epi, h->wkind, p.mfma, s, ev ? ev->a : nullptr, ev ? ev->b : nullptr);
         if (e != hipSuccess) return hip_fail(h, e, "gemm launch");
@@ -343,6 +346,7 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
         na.ssq = h->ssq;
         na.d = d;
         na.M = M;
+        na.half = half;
         na.x_in = h->x_in;
         std::memcpy(na.tokens, sd->tokens, sizeof na.tokens);
         prof_begin(h, DV_K_NORM);
@@ -414,6 +418,8 @@ void fill_desc(StepDesc *sd, const int32_t *tokens, const int32_t *parents, int 
     sd->M = n;
     sd->P = base;
     sd->Mpad = round_up(n, 16);
+    // up to 8 nodes: hi and lo of the split activations share one MFMA operand
+    sd->half = n <= 8 ? 1 : 0;
     for (int i = 0; i < n; ++i) {
         sd->tokens[i] = tokens[i];
         sd->parents[i] = parents[i];
@@ -570,6 +576,7 @@ int prefill_large(dv_handle *h, const int32_t *tokens, int n, dv_kv *kv, int32_t
             na.ssq = h->ssq;
             na.d = d;
             na.M = 1;
+            na.half = 1;
             prof_begin(h, DV_K_NORM);
             rc = ck(launch_embed_norm(na, 16, 1, s), "prefill final norm");
             prof_end(h);
@@ -586,6 +593,7 @@ int prefill_large(dv_handle *h, const int32_t *tokens, int n, dv_kv *kv, int32_t
             g.xs = h->u_s;
             g.M = 1;
             g.Mpad = 16;
+            g.half = 1;
             g.ssq_in = h->ssq;
             g.n_ssq_in = DV_NORM_SLICES;
             g.eps = c.rms_eps;
@@ -593,7 +601,7 @@ int prefill_large(dv_handle *h, const int32_t *tokens, int n, dv_kv *kv, int32_t
             g.arg_val = h->arg_val;
             g.arg_idx = h->arg_idx;
             ProfEv *ev = prof_pair(h, DV_K_GEMM);
-            rc = ck(launch_gemm(g, gemm_grid(h->p_lm, EPI_LOGITS, h->wkind, 1, h->n_cu), EPI_LOGITS, h->wkind, 1, s,
+            rc = ck(launch_gemm(g, gemm_grid(h->p_lm, EPI_LOGITS, h->wkind, 0, h->n_cu), EPI_LOGITS, h->wkind, 1, s,
                                 ev ? ev->a : nullptr, ev ? ev->b : nullptr),
                     "prefill lm_head");
             if (rc) return rc;

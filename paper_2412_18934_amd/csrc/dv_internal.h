@@ -18,7 +18,7 @@ struct StepDesc {
     int32_t M;        // tree nodes
     int32_t P;        // committed length before the step
     int32_t Mpad;     // M rounded up to 16
-    int32_t pad0;
+    int32_t half;     // activations in the half split layout (M <= 8)
     int32_t tokens[DV_TREE_MAX];
     int32_t parents[DV_TREE_MAX];
     int32_t pos[DV_TREE_MAX];
@@ -28,7 +28,7 @@ struct StepDesc {
 
 // The tree as attention needs it (by value).
 struct TreeMask {
-    int32_t M, P, Mpad, pad0;
+    int32_t M, P, Mpad, half;  // half: outputs in the half split layout
     uint64_t anc[DV_TREE_MAX];
 };
 
@@ -52,6 +52,12 @@ enum GemmEpi { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LOGITS = 3, EPI_P
 // 16 (k%32)/8 + m%16 holding columns 32 s + 8 ((k%32)/8) .. +8 of token m.
 // Block (s, mt, p) starts at element ((s MT + mt) 2 + p) 512.
 // Size: K/32 * MT * 2 * 512 bf16 = 64 K MT bytes.
+// Half layout (steps of at most 8 nodes, flag `half`, written as MT = 0):
+// one 1 KB block per k-step, B-operand columns 0-7 holding the hi parts of
+// tokens 0-7 and columns 8-15 their lo parts, so one MFMA covers both and
+// the sums of columns n and n + 8 give token n.  Block s starts at element
+// 512 s; a token's lo values sit 64 elements after its hi values.  Size:
+// K/32 * 512 bf16 = 32 K bytes.
 
 // Projection weights, MFMA path.  The output rows are cut into 16-row
 // blocks; rb consecutive blocks form a row group (one work unit, or ks units
@@ -86,6 +92,7 @@ struct GemmArgs {
     const float *x;            // VALU path: activations [Mpad][K], fp32
     const uint16_t *xs;        // MFMA path: the same activations in split layout
     int32_t M, Mpad;
+    int32_t half;              // xs, us and out_split in the half split layout
     float *out;                // QKV: q [Mpad][d]; SWIGLU: h [Mpad][N] (VALU
                                // consumer); LOGITS: logits [M][N] or null
     uint16_t *out_split;       // SWIGLU: h in split layout (MFMA consumer)
@@ -137,6 +144,7 @@ struct NormArgs {
     float *ssq;                // [Mpad][DV_NORM_SLICES] sums of squares of x
     int32_t d;
     int32_t M;
+    int32_t half;              // us in the half split layout
     int32_t tokens[DV_TREE_MAX];  // token ids of the nodes
 };
 

@@ -78,18 +78,27 @@ __device__ __forceinline__ size_t v_index(int j, int s, int hd)
 // ---------------------------------------------------------------------------
 // split layout of activations (see dv_internal.h)
 
+// MT = 0 selects the half layout (tokens 0-7 only; lo in columns 8-15).
 __device__ __forceinline__ size_t split_index(int m, int k, int MT)
 {
     const int s = k >> 5, g = (k >> 3) & 3, j = k & 7, mt = m >> 4, n = m & 15;
-    return (((size_t)s * MT + mt) * 2 * 64 + g * 16 + n) * 8 + j;  // hi; lo is +512
+    const size_t blk = MT ? ((size_t)s * MT + mt) * 2 : (size_t)s;
+    return (blk * 64 + g * 16 + n) * 8 + j;  // hi; lo is + split_lo(MT)
 }
+
+__device__ __forceinline__ int split_lo(int MT) { return MT ? 512 : 64; }
+
+// token tiles of a split-layout operand (0: half layout) and the tokens it
+// holds
+__device__ __forceinline__ int split_mt(int Mpad, int half) { return half ? 0 : Mpad >> 4; }
+__device__ __forceinline__ int split_rows(int Mpad, int half) { return half ? 8 : Mpad; }
 
 __device__ __forceinline__ void store_split(uint16_t *xs, int m, int k, int MT, float v)
 {
     const size_t i = split_index(m, k, MT);
     const float hi = __uint_as_float(__float_as_uint(v) & 0xffff0000u);
     xs[i] = (uint16_t)(__float_as_uint(v) >> 16);
-    xs[i + 512] = f2bf(v - hi);
+    xs[i + split_lo(MT)] = f2bf(v - hi);
 }
 
 // fp32 -> bf16 hi (truncation) + lo (RNE of the remainder), 8 values
@@ -124,7 +133,7 @@ __device__ __forceinline__ void store_split4(uint16_t *xs, int m, int k, int MT,
         lo[p] = l2;
     }
     *reinterpret_cast<uint2 *>(xs + i) = make_uint2(hi[0], hi[1]);
-    *reinterpret_cast<uint2 *>(xs + i + 512) = make_uint2(lo[0], lo[1]);
+    *reinterpret_cast<uint2 *>(xs + i + split_lo(MT)) = make_uint2(lo[0], lo[1]);
 }
 
 // ---------------------------------------------------------------------------
@@ -225,8 +234,8 @@ __device__ void resid_epilogue(const GemmArgs &a, float *Y, int ld, int row0, in
     auto gain = [&](int r) -> float { return gain_s ? gain_s[r] : Elem<W>::load(gp, row0 + r); };
     if (a.us) {
         // 8 consecutive rows of one token per thread: one 16-byte hi and lo store
-        const int MT = a.Mpad >> 4, nc = nrows >> 3;
-        for (int e = tid; e < a.Mpad * nc; e += nt) {
+        const int MT = split_mt(a.Mpad, a.half), nc = nrows >> 3;
+        for (int e = tid; e < split_rows(a.Mpad, a.half) * nc; e += nt) {
             const int m = e / nc, c = e - m * nc;
             const float *y = Y + m * ld + 8 * c;
             const int r = 8 * c;
@@ -236,7 +245,7 @@ __device__ void resid_epilogue(const GemmArgs &a, float *Y, int ld, int row0, in
             split_hi_lo(v0, v1, hi, lo);
             const size_t i = split_index(m, row0 + r, MT);
             *reinterpret_cast<bf16x8 *>(a.us + i) = hi;
-            *reinterpret_cast<bf16x8 *>(a.us + i + 512) = lo;
+            *reinterpret_cast<bf16x8 *>(a.us + i + split_lo(MT)) = lo;
         }
     } else {
         for (int e = tid; e < a.Mpad * nrows; e += nt) {
@@ -263,8 +272,8 @@ __device__ void swiglu_epilogue(const GemmArgs &a, const float *Y, int ld, int t
 {
     const int tid = threadIdx.x, nt = blockDim.x;
     if (a.out_split) {
-        const int MT = a.Mpad >> 4, nc = 2 * ntile;
-        for (int e = tid; e < a.Mpad * nc; e += nt) {
+        const int MT = split_mt(a.Mpad, a.half), nc = 2 * ntile;
+        for (int e = tid; e < split_rows(a.Mpad, a.half) * nc; e += nt) {
             const int m = e / nc, c = e - m * nc, p = c >> 1, r0 = 8 * (c & 1);
             const float *g = Y + m * ld + 32 * p + r0, *u = g + 16;
             float hv[8];
@@ -274,7 +283,7 @@ __device__ void swiglu_epilogue(const GemmArgs &a, const float *Y, int ld, int t
             split_hi_lo(make_float4(hv[0], hv[1], hv[2], hv[3]), make_float4(hv[4], hv[5], hv[6], hv[7]), hi, lo);
             const size_t i = split_index(m, 16 * t0 + 8 * c, MT);
             *reinterpret_cast<bf16x8 *>(a.out_split + i) = hi;
-            *reinterpret_cast<bf16x8 *>(a.out_split + i + 512) = lo;
+            *reinterpret_cast<bf16x8 *>(a.out_split + i + split_lo(MT)) = lo;
         }
     } else {
         for (int e = tid; e < a.Mpad * 16 * ntile; e += nt) {
@@ -398,6 +407,12 @@ __device__ void plain_epilogue(const GemmArgs &a, const float *Y, int ld, int ro
 // Loads: weights are read once per step (non-temporal hint), activations
 // (MT KB hi + MT KB lo per k-step) are shared by every workgroup and stay in
 // the caches.
+//
+// MT = 0: activations in the half split layout (at most 8 tokens): one 1 KB
+// block per k-step carries hi in B columns 0-7 and lo in columns 8-15, so
+// each weight block takes one MFMA and half the activation bytes; column n
+// and column n + 8 are summed (a lane shuffle) once the unit's sums are
+// complete, leaving columns 8-15 zero.
 
 #ifndef DV_WEIGHT_NT
 #define DV_WEIGHT_NT 1
@@ -465,14 +480,17 @@ __device__ __forceinline__ uint2 i8x4_to_bf16(uint32_t d)
     return make_uint2(__builtin_amdgcn_perm(f1, f0, 0x07060302u), __builtin_amdgcn_perm(f3, f2, 0x07060302u));
 }
 
-template <int MT, int EPI, typename KV, int NW, int U, int RB, bool Q8 = false>
+template <int MT_, int EPI, typename KV, int NW, int U, int RB, bool Q8 = false>
 __global__ __launch_bounds__(64 * NW) void k_proj(GemmArgs a)
 {
+    constexpr bool HALF = MT_ == 0;
+    constexpr int MT = HALF ? 1 : MT_;  // token tiles of the MFMA outputs
     constexpr int ROWS = RB * 16, LD = ROWS + 1, NE = RB * MT * 64;
     static_assert(64 * NW >= 4 * 16 * MT, "input_rinv needs 4 threads per token");
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, tid = threadIdx.x;
-    // a step is one k-step of 32 (bf16 weights) or a pair of them (int8)
-    constexpr int XP = Q8 ? 4 : 2;
+    // a step is one k-step of 32 (bf16 weights) or a pair of them (int8);
+    // XP activation blocks per step and token tile (PP parts per k-step)
+    constexpr int PP = HALF ? 1 : 2, XP = (Q8 ? 2 : 1) * PP;
     const int S = a.K / (Q8 ? 64 : 32), G = a.n_groups, KS = a.ks;
     __shared__ f32x4 red[NW][NE / 64][64];
     __shared__ float Y[16 * MT * LD];
@@ -509,7 +527,7 @@ __global__ __launch_bounds__(64 * NW) void k_proj(GemmArgs a)
         // activation block of step i, half hf (int8: k-step 2 step + hf), part q
         auto xp = [&](int i, int hf, int mt, int q) -> const u32x4 * {
             const size_t k32 = Q8 ? 2 * (size_t)(s0 + NW * i) + hf : (size_t)(s0 + NW * i);
-            return Xb + ((k32 * MT + mt) * 2 + q) * 64 + lane;
+            return Xb + ((k32 * MT + mt) * PP + q) * 64 + lane;
         };
         f32x4 acc[RB][MT];
 #pragma unroll
@@ -525,15 +543,15 @@ __global__ __launch_bounds__(64 * NW) void k_proj(GemmArgs a)
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-                    for (int q = 0; q < XP; ++q) xb[j][mt][q] = *xp(i, q >> 1, mt, q & 1);
+                    for (int q = 0; q < XP; ++q) xb[j][mt][q] = *xp(i, q / PP, mt, q % PP);
             };
             auto mfma = [&](int j) {
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
-                    for (int hf = 0; hf < XP / 2; ++hf) {
-                        const bf16x8 hi = __builtin_bit_cast(bf16x8, xb[j][mt][2 * hf]);
-                        const bf16x8 lo = __builtin_bit_cast(bf16x8, xb[j][mt][2 * hf + 1]);
+                    for (int hf = 0; hf < XP / PP; ++hf) {
+                        const bf16x8 hi = __builtin_bit_cast(bf16x8, xb[j][mt][PP * hf]);
+                        const bf16x8 lo = __builtin_bit_cast(bf16x8, xb[j][mt][PP * hf + PP - 1]);
 #pragma unroll
                         for (int b = 0; b < RB; ++b) {
                             bf16x8 w;
@@ -545,7 +563,8 @@ __global__ __launch_bounds__(64 * NW) void k_proj(GemmArgs a)
                                 w = __builtin_bit_cast(bf16x8, wb[j][b]);
                             }
                             acc[b][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, hi, acc[b][mt], 0, 0, 0);
-                            acc[b][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, lo, acc[b][mt], 0, 0, 0);
+                            if (!HALF)
+                                acc[b][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, lo, acc[b][mt], 0, 0, 0);
                         }
                     }
                 }
@@ -648,6 +667,17 @@ __global__ __launch_bounds__(64 * NW) void k_proj(GemmArgs a)
             }
         }
         if (mine) {
+            if (HALF) {
+                // token n = hi column n + lo column n + 8; columns 8-15 -> 0
+                // (every lane of a wave holds the same e >> 6)
+#pragma unroll
+                for (int c = 0; c < (NE + 64 * NW - 1) / (64 * NW); ++c)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const float o = __shfl_xor(v[c][j], 8);
+                        v[c][j] = (lane & 8) ? 0.f : v[c][j] + o;
+                    }
+            }
             // D layout -> Y[token][row]
 #pragma unroll
             for (int c = 0; c < (NE + 64 * NW - 1) / (64 * NW); ++c) {
@@ -772,12 +802,15 @@ __global__ __launch_bounds__(DV_NORM_THREADS) void k_embed_norm(NormArgs a)
     const int c0 = sl * (d / DV_NORM_SLICES), c1 = c0 + d / DV_NORM_SLICES;
     float *urow = a.u + (size_t)m * d;
     float *xrow = a.x + (size_t)m * d;
-    const int MT = gridDim.x >> 4;  // grid.x = Mpad rows
+    const int MT = split_mt(gridDim.x, a.half);  // grid.x = Mpad rows
     if (m >= a.M) {
         for (int i = c0 + 4 * tid; i < c1; i += SPAN) {
             const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (a.us) store_split4(a.us, m, i, MT, z);
-            else *reinterpret_cast<float4 *>(urow + i) = z;
+            if (a.us) {
+                if (m < split_rows(gridDim.x, a.half)) store_split4(a.us, m, i, MT, z);
+            } else {
+                *reinterpret_cast<float4 *>(urow + i) = z;
+            }
             *reinterpret_cast<float4 *>(xrow + i) = z;
         }
         if (tid == 0) a.ssq[m * DV_NORM_SLICES + sl] = 0.f;
@@ -1069,11 +1102,12 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mfma(AttnArgs a)
                 for (int j = 0; j < 4; ++j) ov[j] = fmaf(wgt, o4[j], ov[j]);
             }
             if (a.n_split == 1) {
-                if (ti < a.tm.Mpad) {
+                if (ti < (a.out_split ? split_rows(a.tm.Mpad, a.tm.half) : a.tm.Mpad)) {
 #pragma unroll
                     for (int j = 0; j < 4; ++j) {
                         const float r = ti < M ? ov[j] / l : 0.f;
-                        if (a.out_split) store_split(a.out_split, ti, h * HD + d0 + j, a.tm.Mpad >> 4, r);
+                        if (a.out_split)
+                            store_split(a.out_split, ti, h * HD + d0 + j, split_mt(a.tm.Mpad, a.tm.half), r);
                         else a.out[(size_t)ti * D + h * HD + d0 + j] = r;
                     }
                 }
@@ -1105,9 +1139,10 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mfma(AttnArgs a)
     }
     __syncthreads();
     if (!last_s) return;
-    const int Mpad = a.tm.Mpad, MT = Mpad >> 4;
+    const int MT = split_mt(a.tm.Mpad, a.tm.half);
+    const int rows = a.out_split ? split_rows(a.tm.Mpad, a.tm.half) : a.tm.Mpad;
     constexpr int CH = 8;  // splits whose loads are in flight together
-    for (int e2 = threadIdx.x; e2 < Mpad * (HD / 8); e2 += 64 * NW) {
+    for (int e2 = threadIdx.x; e2 < rows * (HD / 8); e2 += 64 * NW) {
         const int i = e2 / (HD / 8), d0 = 8 * (e2 % (HD / 8));
         float ov[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
         float run_m = -INFINITY, l = 0.f;
@@ -1147,7 +1182,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mfma(AttnArgs a)
             split_hi_lo(make_float4(ov[0], ov[1], ov[2], ov[3]), make_float4(ov[4], ov[5], ov[6], ov[7]), hi, lo);
             const size_t si = split_index(i, h * HD + d0, MT);
             *reinterpret_cast<bf16x8 *>(a.out_split + si) = hi;
-            *reinterpret_cast<bf16x8 *>(a.out_split + si + 512) = lo;
+            *reinterpret_cast<bf16x8 *>(a.out_split + si + split_lo(MT)) = lo;
         } else {
 #pragma unroll
             for (int j = 0; j < 8; ++j) a.out[(size_t)i * D + h * HD + d0 + j] = ov[j];
@@ -1249,11 +1284,12 @@ __global__ __launch_bounds__(256) void k_attn_f32(AttnArgs a)
             __syncthreads();
         }
         if (a.n_split == 1) {
-            if (q0 + qi < a.tm.Mpad) {
+            if (q0 + qi < (a.out_split ? split_rows(a.tm.Mpad, a.tm.half) : a.tm.Mpad)) {
 #pragma unroll
                 for (int c = 0; c < DPT; ++c) {
                     const float r = qi < nq ? o[c] / lrun[qi] : 0.f;
-                    if (a.out_split) store_split(a.out_split, q0 + qi, h * HD + dd + c, a.tm.Mpad >> 4, r);
+                    if (a.out_split)
+                        store_split(a.out_split, q0 + qi, h * HD + dd + c, split_mt(a.tm.Mpad, a.tm.half), r);
                     else a.out[(size_t)(q0 + qi) * D + h * HD + dd + c] = r;
                 }
             }
@@ -1280,10 +1316,14 @@ __global__ __launch_bounds__(128) void k_attn_merge(AttnArgs a)
 {
     constexpr int CH = 16;
     const int i = blockIdx.x, h = blockIdx.y, d = threadIdx.x, HD = a.hd;
-    const int M = a.tm.M, MT = gridDim.x >> 4;
+    const int M = a.tm.M, MT = split_mt(gridDim.x, a.tm.half);
     if (i >= M) {
-        if (a.out_split) store_split(a.out_split, i, h * HD + d, MT, 0.f);
-        else a.out[(size_t)i * a.H * HD + h * HD + d] = 0.f;
+        if (a.out_split) {
+            if (i < split_rows(gridDim.x, a.tm.half)) store_split(a.out_split, i, h * HD + d, MT, 0.f);
+        }
+        else {
+            a.out[(size_t)i * a.H * HD + h * HD + d] = 0.f;
+        }
         return;
     }
     const size_t base = (size_t)h * a.n_split * DV_TREE_MAX + i;
@@ -2195,6 +2235,7 @@ static const void *proj_kernel_mt(int mt)
 {
     constexpr int U1 = RB == 4 ? 2 : 4, NWM = Q8 ? 4 : 8;
     switch (mt) {
+    case 0: return (const void *)k_proj<0, EPI, KV, 4, U1, RB, Q8>;  // half split layout
     case 1: return (const void *)k_proj<1, EPI, KV, 4, U1, RB, Q8>;
     case 2: return (const void *)k_proj<2, EPI, KV, NWM, 2, RB, Q8>;
     case 3: return (const void *)k_proj<3, EPI, KV, NWM, 2, RB, Q8>;
@@ -2245,7 +2286,8 @@ int gemm_blocks_per_cu(int epi, int wkind, int use_mfma, int mt, int rb)
 {
     static int cache[5][3][2][5][2];
     if (wkind < 0 || wkind > 2 || epi < 0 || epi > 4) return 1;
-    int &c = cache[epi][wkind][use_mfma ? 1 : 0][(mt >= 1 && mt <= 4) ? mt : 0][rb == 4];
+    if (mt < 0 || mt > 4) return 1;
+    int &c = cache[epi][wkind][use_mfma ? 1 : 0][mt][rb == 4];
     if (c == 0) {
         const void *k = gemm_kernel_any(epi, wkind, use_mfma, mt, rb);
         int n = 0;
@@ -2260,12 +2302,14 @@ int gemm_blocks_per_cu(int epi, int wkind, int use_mfma, int mt, int rb)
 hipError_t launch_gemm(const GemmArgs &a, int grid, int epi, int wkind, int use_mfma, hipStream_t s,
                        hipEvent_t ev_start, hipEvent_t ev_stop)
 {
-    const void *k = gemm_kernel_any(epi, wkind, use_mfma, a.Mpad / 16, a.rb);
+    const int mt = a.half ? 0 : a.Mpad / 16;
+    if (a.half && a.M > 8) return hipErrorInvalidValue;
+    const void *k = gemm_kernel_any(epi, wkind, use_mfma, mt, a.rb);
     if (!k || grid < 1) return hipErrorInvalidValue;
     if (wkind == W_I8 && (!a.scale || a.K % 64)) return hipErrorInvalidValue;
     GemmArgs arg = a;
     void *params[] = {&arg};
-    const dim3 block(gemm_threads(wkind, use_mfma, a.Mpad / 16, a.rb));
+    const dim3 block(gemm_threads(wkind, use_mfma, mt, a.rb));
     // with events: timestamps taken by the dispatch itself (no extra packets)
     if (ev_start && ev_stop) return hipExtLaunchKernel(k, dim3(grid), block, params, 0, s, ev_start, ev_stop, 0);
     return hipLaunchKernel(k, dim3(grid), block, params, 0, s);
