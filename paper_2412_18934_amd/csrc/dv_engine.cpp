@@ -169,6 +169,22 @@ GemmPlan make_plan(int n_tiles, int K, int mfma, bool resid, int n_cu)
 
 int gemm_units(const GemmPlan &p) { return p.n_groups * p.ks; }
 
+// A projection without K splits whose 4-block groups outnumber the CUs runs
+// its steps of at most one token tile as 8-block groups when those fit on the
+// CUs once: every CU then streams one group (half the activation bytes per
+// weight byte) instead of some CUs streaming two and the rest one.  The
+// k-major block order is the same for both group sizes, so the packed weights
+// serve either.
+GemmPlan step_plan(const GemmPlan &p, int epi, int wkind, int mt, int n_cu)
+{
+    if (!p.mfma || p.rb != 4 || p.ks != 1 || mt > 1 || p.n_groups % 2) return p;
+    if (p.n_groups <= n_cu || p.n_groups / 2 > n_cu || !gemm_has_rb8(epi, wkind, mt)) return p;
+    GemmPlan q = p;
+    q.rb = 8;
+    q.n_groups = p.n_groups / 2;
+    return q;
+}
+
 // Grid of a launch: every unit its own workgroup, capped at what the CUs hold
 // at once (the workgroups then loop over the units).
 int gemm_grid(const GemmPlan &p, int epi, int wkind, int mt, int n_cu)
@@ -307,9 +323,10 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
     aa.out = h->attn;
     aa.out_split = h->p_o.mfma ? h->attn_s : nullptr;
 
-    auto gemm = [&](const GemmPlan &p, int epi, const void *w0, const void *w1, const void *w2,
+    auto gemm = [&](const GemmPlan &p0, int epi, const void *w0, const void *w1, const void *w2,
                     const uint16_t *packed, const float *scale, int N, int K, const float *x, const uint16_t *xs,
                     float *out, const void *gain) -> int {
+        const GemmPlan p = step_plan(p0, epi, h->wkind, mt, h->n_cu);
         GemmArgs a = g;
         a.packed = packed;
         a.scale = scale;

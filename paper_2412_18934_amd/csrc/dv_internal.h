@@ -197,6 +197,9 @@ hipError_t launch_pack_scales(const GemmArgs &a, int epi, float *dst, hipStream_
 GemmShape gemm_shape(int rb);
 // workgroups one CU can hold for a GEMM variant (cached)
 int gemm_blocks_per_cu(int epi, int wkind, int use_mfma, int mt, int rb);
+// whether an MFMA projection variant with 8-block row groups exists for this
+// epilogue, weight kind and token-tile count
+bool gemm_has_rb8(int epi, int wkind, int mt);
 // ev_start/ev_stop (optional, both or neither): timestamps of this launch
 hipError_t launch_gemm(const GemmArgs &a, int grid, int epi, int wkind, int use_mfma,
                        hipStream_t s, hipEvent_t ev_start, hipEvent_t ev_stop);

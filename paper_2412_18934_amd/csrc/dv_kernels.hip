@@ -208,6 +208,39 @@ __device__ __forceinline__ void input_rinv(const GemmArgs &a, float *rinv)
     if (m < a.Mpad && c == 0) rinv[m] = m < a.M ? 1.0f / sqrtf(s / (float)a.dn + a.eps) : 0.f;
 }
 
+// The same 1/rms in two parts, for the projections: rinv_load issues the
+// first NJ partials of each thread before the weight stream starts (loads
+// return in order, so they arrive first and no later wait on them drains the
+// stream); rinv_finish, after the stream, adds the remaining partials in the
+// same order and writes rinv (bit-identical to input_rinv).
+template <int NJ>
+__device__ __forceinline__ void rinv_load(const GemmArgs &a, float (&v)[NJ])
+{
+    const int tid = threadIdx.x, m = tid >> 2, c = tid & 3;
+    const float *p = a.ssq_in + (size_t)m * a.n_ssq_in;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+        const int i = c + 4 * j;
+        v[j] = (m < a.Mpad && i < a.n_ssq_in) ? p[i] : 0.f;
+    }
+}
+
+template <int NJ>
+__device__ __forceinline__ void rinv_finish(const GemmArgs &a, const float (&v)[NJ], float *rinv)
+{
+    const int tid = threadIdx.x, m = tid >> 2, c = tid & 3;
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) s += v[j];
+    if (m < a.Mpad) {
+        const float *p = a.ssq_in + (size_t)m * a.n_ssq_in;
+        for (int i = c + 4 * NJ; i < a.n_ssq_in; i += 4) s += p[i];
+    }
+    s += __shfl_xor(s, 1);
+    s += __shfl_xor(s, 2);
+    if (m < a.Mpad && c == 0) rinv[m] = m < a.M ? 1.0f / sqrtf(s / (float)a.dn + a.eps) : 0.f;
+}
+
 // Residual projections: x += sums, then the next RMSNorm's numerator
 // u = x * gain (split layout or fp32) and the group's sums of squares.
 // Rows [row0, row0 + nrows) of the stream.  With y_is_x, Y already holds the
@@ -297,8 +330,11 @@ __device__ void swiglu_epilogue(const GemmArgs &a, const float *Y, int ld, int t
 // QKV on the 32-row tile t held in Y[m * ld + 0..32): rotary embedding of q
 // and k at each token's position, q to the query buffer, k and v (rounded to
 // the cache type) to cache slots P + m.
-template <typename KV>
-__device__ void qkv_epilogue(const GemmArgs &a, const float *Y, int ld, int t, const float *rinv)
+// EPT > 0: the rotary factors of this thread's entries (iteration c of the
+// loop below) were loaded beforehand into cs[c], sn[c].
+template <typename KV, int EPT = 0>
+__device__ void qkv_epilogue(const GemmArgs &a, const float *Y, int ld, int t, const float *rinv,
+                             const float *cs = nullptr, const float *sn = nullptr)
 {
     const int tid = threadIdx.x, nt = blockDim.x;
     {
@@ -307,14 +343,14 @@ __device__ void qkv_epilogue(const GemmArgs &a, const float *Y, int ld, int t, c
         const int per_head = a.hd / DV_GEMM_TILE;
         const int h = tt / per_head, j0 = (tt - h * per_head) * 16;
         const int half = a.hd / 2;
-        for (int e = tid; e < a.M * 16; e += nt) {
+        for (int e = tid, it = 0; e < a.M * 16; e += nt, ++it) {
             const int m = e / 16, r = e % 16;
             const int j = j0 + r;
             float y1 = Y[m * ld + r] * rinv[m], y2 = Y[m * ld + 16 + r] * rinv[m];
             if (seg < 2) {
                 const int pos = a.pos[m];  // P + depth(m) - 1
-                const float c = a.rope_cos[(size_t)pos * half + j];
-                const float s = a.rope_sin[(size_t)pos * half + j];
+                const float c = EPT > 0 ? cs[it] : a.rope_cos[(size_t)pos * half + j];
+                const float s = EPT > 0 ? sn[it] : a.rope_sin[(size_t)pos * half + j];
                 const float o1 = y1 * c - y2 * s, o2 = y2 * c + y1 * s;
                 y1 = o1;
                 y2 = o2;
@@ -502,19 +538,16 @@ __global__ __launch_bounds__(64 * NW) void k_proj(GemmArgs a)
     const u32x4 *Wb = reinterpret_cast<const u32x4 *>(a.packed);
     const u32x4 *Xb = reinterpret_cast<const u32x4 *>(a.xs);
     bool have_rinv = false;
-
-    // epilogue operands of unit (g), RESID: x rows into Y and the gains;
-    // issued after the unit's first weight loads
-    auto stage = [&](int g) {
-        if (EPI == EPI_RESID) {
-            for (int e = tid; e < 16 * MT * ROWS; e += 64 * NW) {
-                const int m = e / ROWS, r = e - m * ROWS;
-                Y[m * LD + r] = m < a.M ? a.resid[(size_t)m * a.N + g * ROWS + r] : 0.f;
-            }
-            for (int r = tid; r < ROWS; r += 64 * NW)
-                stage_s[r] = Elem<uint16_t>::load(reinterpret_cast<const uint16_t *>(a.gain), g * ROWS + r);
-        }
-    };
+    // Small epilogue operands (the input's norm partials, RESID: the unit's
+    // rows of x and their gains, QKV: the rotary factors) are loaded into
+    // registers before the unit's weight stream starts and consumed after it:
+    // loads return in order, so they are back before the first weights and no
+    // wait for them empties the stream.
+    constexpr bool NEED_RINV = EPI != EPI_RESID && EPI != EPI_PLAIN;
+    constexpr int NJP = MT >= 2 ? 8 : 24;                            // norm partials per thread
+    constexpr int SXN = (16 * MT * ROWS + 64 * NW - 1) / (64 * NW);  // RESID: x values per thread
+    constexpr int EPT = (16 * 16 * MT + 64 * NW - 1) / (64 * NW);    // QKV: rotary entries per thread and tile
+    static_assert(ROWS <= 64 * NW, "one gain per thread");
 
     for (int unit = blockIdx.x; unit < a.n_units; unit += gridDim.x) {
         const int g = unit / KS, ks = unit - g * KS;
@@ -535,6 +568,39 @@ __global__ __launch_bounds__(64 * NW) void k_proj(GemmArgs a)
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) acc[b][mt] = (f32x4){0.f, 0.f, 0.f, 0.f};
         f32x4 rs[Q8 ? RB : 1];  // int8: this lane's four row scales per block
+        float sx[EPI == EPI_RESID ? SXN : 1], sgain = 0.f;
+        float sv[NEED_RINV ? NJP : 1];
+        float rcs[EPI == EPI_QKV ? RB / 2 : 1][EPI == EPI_QKV ? EPT : 1];
+        float rsn[EPI == EPI_QKV ? RB / 2 : 1][EPI == EPI_QKV ? EPT : 1];
+        const bool load_rinv = NEED_RINV && !have_rinv;
+        if constexpr (EPI == EPI_RESID) {
+#pragma unroll
+            for (int c = 0; c < SXN; ++c) {
+                const int e = tid + 64 * NW * c, m = e / ROWS, r = e - m * ROWS;
+                sx[c] = (e < 16 * MT * ROWS && m < a.M) ? a.resid[(size_t)m * a.N + g * ROWS + r] : 0.f;
+            }
+            if (tid < ROWS) sgain = Elem<uint16_t>::load(reinterpret_cast<const uint16_t *>(a.gain), g * ROWS + tid);
+        }
+        if constexpr (NEED_RINV) {
+            if (load_rinv) rinv_load<NJP>(a, sv);
+        }
+        if constexpr (EPI == EPI_QKV) {
+            // the (m, r) entries qkv_epilogue gives this thread, per 32-row tile
+            const int per_seg = a.N / DV_GEMM_TILE, per_head = a.hd / DV_GEMM_TILE, half = a.hd / 2;
+#pragma unroll
+            for (int p = 0; p < RB / 2; ++p) {
+                const int t = g * (RB / 2) + p, seg = t / per_seg, tt = t - seg * per_seg;
+                const int j0 = (tt - (tt / per_head) * per_head) * 16;
+#pragma unroll
+                for (int c = 0; c < EPT; ++c) {
+                    const int e = tid + 64 * NW * c, m = e / 16, j = j0 + (e % 16);
+                    const bool ok = seg < 2 && e < a.M * 16;
+                    const size_t ti = ok ? (size_t)a.pos[m] * half + j : 0;
+                    rcs[p][c] = ok ? a.rope_cos[ti] : 0.f;
+                    rsn[p][c] = ok ? a.rope_sin[ti] : 0.f;
+                }
+            }
+        }
         if (n > 0) {
             u32x4 wb[U][RB], xb[U][MT][XP];
             auto fetch = [&](int j, int i) {
@@ -578,13 +644,6 @@ __global__ __launch_bounds__(64 * NW) void k_proj(GemmArgs a)
                 for (int b = 0; b < RB; ++b)
                     rs[b] = *reinterpret_cast<const f32x4 *>(a.scale + (g * RB + b) * 16 + 4 * (lane >> 4));
             }
-            stage(g);
-            if (EPI != EPI_RESID && EPI != EPI_PLAIN && !have_rinv) {
-                // the first unit's loads are in flight; the norm scalars of
-                // the input arrive meanwhile
-                input_rinv(a, rinv);
-                have_rinv = true;
-            }
             int i = 0;
             for (; i + U < n; i += U) {
 #pragma unroll
@@ -603,10 +662,19 @@ __global__ __launch_bounds__(64 * NW) void k_proj(GemmArgs a)
 #pragma unroll
                     for (int mt = 0; mt < MT; ++mt) acc[b][mt] *= rs[b];
             }
-        } else {
-            stage(g);
-            if (EPI != EPI_RESID && EPI != EPI_PLAIN && !have_rinv) {
-                input_rinv(a, rinv);
+        }
+        // the epilogue operands loaded before the stream, into LDS
+        if constexpr (EPI == EPI_RESID) {
+#pragma unroll
+            for (int c = 0; c < SXN; ++c) {
+                const int e = tid + 64 * NW * c, m = e / ROWS, r = e - m * ROWS;
+                if (e < 16 * MT * ROWS) Y[m * LD + r] = sx[c];
+            }
+            if (tid < ROWS) stage_s[tid] = sgain;
+        }
+        if constexpr (NEED_RINV) {
+            if (load_rinv) {
+                rinv_finish<NJP>(a, sv, rinv);
                 have_rinv = true;
             }
         }
@@ -702,7 +770,8 @@ __global__ __launch_bounds__(64 * NW) void k_proj(GemmArgs a)
                 swiglu_epilogue(a, Y, LD, g * (RB / 2), RB / 2, rinv);
             } else {
 #pragma unroll
-                for (int p = 0; p < RB / 2; ++p) qkv_epilogue<KV>(a, Y + 32 * p, LD, g * (RB / 2) + p, rinv);
+                for (int p = 0; p < RB / 2; ++p)
+                    qkv_epilogue<KV, EPT>(a, Y + 32 * p, LD, g * (RB / 2) + p, rinv, rcs[p], rsn[p]);
             }
         }
         __syncthreads();
@@ -2222,7 +2291,7 @@ __global__ __launch_bounds__(256) void k_kv_commit(CommitArgs a)
 // ---------------------------------------------------------------------------
 // launchers
 
-GemmShape gemm_shape(int rb) { return rb == 4 ? GemmShape{4, 2} : GemmShape{4, 4}; }
+GemmShape gemm_shape(int rb) { return rb >= 4 ? GemmShape{4, 2} : GemmShape{4, 4}; }
 
 // Waves per workgroup of the MFMA projection.  More than one token tile
 // holds more accumulators and operands per wave, so each wave keeps fewer
@@ -2233,14 +2302,21 @@ static int proj_waves(int wkind, int mt, int rb) { return mt >= 2 && wkind == W_
 template <int EPI, typename KV, int RB, bool Q8>
 static const void *proj_kernel_mt(int mt)
 {
-    constexpr int U1 = RB == 4 ? 2 : 4, NWM = Q8 ? 4 : 8;
-    switch (mt) {
-    case 0: return (const void *)k_proj<0, EPI, KV, 4, U1, RB, Q8>;  // half split layout
-    case 1: return (const void *)k_proj<1, EPI, KV, 4, U1, RB, Q8>;
-    case 2: return (const void *)k_proj<2, EPI, KV, NWM, 2, RB, Q8>;
-    case 3: return (const void *)k_proj<3, EPI, KV, NWM, 2, RB, Q8>;
-    case 4: return (const void *)k_proj<4, EPI, KV, NWM, 2, RB, Q8>;
-    default: return nullptr;
+    constexpr int U1 = RB >= 4 ? 2 : 4, NWM = Q8 ? 4 : 8;
+    if constexpr (RB == 8) {
+        // 8-block groups: one token tile at most (see gemm_rb8)
+        if (mt == 0) return (const void *)k_proj<0, EPI, KV, 4, U1, RB, Q8>;
+        if (mt == 1) return (const void *)k_proj<1, EPI, KV, 4, U1, RB, Q8>;
+        return nullptr;
+    } else {
+        switch (mt) {
+        case 0: return (const void *)k_proj<0, EPI, KV, 4, U1, RB, Q8>;  // half split layout
+        case 1: return (const void *)k_proj<1, EPI, KV, 4, U1, RB, Q8>;
+        case 2: return (const void *)k_proj<2, EPI, KV, NWM, 2, RB, Q8>;
+        case 3: return (const void *)k_proj<3, EPI, KV, NWM, 2, RB, Q8>;
+        case 4: return (const void *)k_proj<4, EPI, KV, NWM, 2, RB, Q8>;
+        default: return nullptr;
+        }
     }
 }
 
@@ -2255,6 +2331,10 @@ static const void *gemm_kernel(int wkind, int use_mfma, int mt, int rb)
     } else {
         if (wkind != W_F32 && use_mfma) {
             const bool q8 = wkind == W_I8;
+            if constexpr (EPI == EPI_SWIGLU) {
+                if (rb == 8 && !q8) return proj_kernel_mt<EPI, uint16_t, 8, false>(mt);
+            }
+            if (rb == 8) return nullptr;
             if (rb == 4) return q8 ? proj_kernel_mt<EPI, uint16_t, 4, true>(mt) : proj_kernel_mt<EPI, uint16_t, 4, false>(mt);
             if (rb == 2) return q8 ? proj_kernel_mt<EPI, uint16_t, 2, true>(mt) : proj_kernel_mt<EPI, uint16_t, 2, false>(mt);
             return nullptr;
@@ -2284,10 +2364,10 @@ static int gemm_threads(int wkind, int use_mfma, int mt, int rb)
 
 int gemm_blocks_per_cu(int epi, int wkind, int use_mfma, int mt, int rb)
 {
-    static int cache[5][3][2][5][2];
+    static int cache[5][3][2][5][3];
     if (wkind < 0 || wkind > 2 || epi < 0 || epi > 4) return 1;
     if (mt < 0 || mt > 4) return 1;
-    int &c = cache[epi][wkind][use_mfma ? 1 : 0][mt][rb == 4];
+    int &c = cache[epi][wkind][use_mfma ? 1 : 0][mt][rb == 8 ? 2 : (rb == 4 ? 1 : 0)];
     if (c == 0) {
         const void *k = gemm_kernel_any(epi, wkind, use_mfma, mt, rb);
         int n = 0;
@@ -2298,6 +2378,8 @@ int gemm_blocks_per_cu(int epi, int wkind, int use_mfma, int mt, int rb)
     }
     return c;
 }
+
+bool gemm_has_rb8(int epi, int wkind, int mt) { return gemm_kernel_any(epi, wkind, 1, mt, 8) != nullptr; }
 
 hipError_t launch_gemm(const GemmArgs &a, int grid, int epi, int wkind, int use_mfma, hipStream_t s,
                        hipEvent_t ev_start, hipEvent_t ev_stop)
