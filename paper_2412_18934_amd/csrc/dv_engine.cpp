@@ -873,6 +873,7 @@ int dv_verify_init(const dv_config *cfg, const dv_weights *w, void *stream, dv_h
               dalloc((void **)&h->part_l, (size_t)H * h->attn_split_max * rows * 4) &&
               dalloc((void **)&h->attn_cnt, (size_t)H * 4) &&
               dalloc((void **)&h->part_gemm, part_elems * 4) &&
+              hipMemset(h->part_gemm, 0xff, part_elems * 4) == hipSuccess &&  // empty split-K slots
               dalloc((void **)&h->arg_val, (size_t)h->p_lm.n_groups * rows * 4) &&
               dalloc((void **)&h->arg_idx, (size_t)h->p_lm.n_groups * rows * 4) &&
               dalloc((void **)&h->rope_cos, (size_t)c.max_ctx * (hd / 2) * 4) &&
@@ -1152,7 +1153,7 @@ int dv_draft_init(const dv_config *cfg, const dv_weights *w, const dv_dgf_weight
     if (need > h->part_elems) {
         (void)hipFree(h->part_gemm);
         h->part_gemm = nullptr;
-        okd = zalloc((void **)&h->part_gemm, need * 4);
+        okd = zalloc((void **)&h->part_gemm, need * 4) && hipMemset(h->part_gemm, 0xff, need * 4) == hipSuccess;
         h->part_elems = okd ? need : 0;
     }
     if (okd && need_cnt > h->cnt_n) {

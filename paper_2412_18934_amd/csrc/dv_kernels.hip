@@ -297,6 +297,50 @@ __device__ void resid_epilogue(const GemmArgs &a, float *Y, int ld, int row0, in
     }
 }
 
+// The same for the MFMA projections' split-layout output, in one pass: each
+// thread takes 8 consecutive rows of one token (Y already holds x + sums and
+// gain_s the rows' gains), writes them to the stream, writes x * gain as one
+// 16-byte hi and one lo store, and the 8 threads of a token sum their squares
+// (each over its 8 rows in order, then combined by lane shuffles).
+__device__ void resid_epilogue_split(const GemmArgs &a, const float *Y, int ld, int row0, int nrows, int group,
+                                     const float *gain_s)
+{
+    const int tid = threadIdx.x, nt = blockDim.x;
+    const int MT = split_mt(a.Mpad, a.half), nc = nrows >> 3;  // nc = 8 chunks per token (64 rows)
+    const int total = split_rows(a.Mpad, a.half) * nc;
+    for (int e0 = 0; e0 < total; e0 += nt) {
+        const int e = e0 + tid;
+        float s = 0.f;
+        if (e < total) {
+            const int m = e / nc, c = e - m * nc, r = 8 * c;
+            const float *y = Y + m * ld + r;
+            float4 v0 = make_float4(y[0], y[1], y[2], y[3]), v1 = make_float4(y[4], y[5], y[6], y[7]);
+            if (m < a.M) {
+                float *xp = a.resid + (size_t)m * a.N + row0 + r;
+                *reinterpret_cast<float4 *>(xp) = v0;
+                *reinterpret_cast<float4 *>(xp + 4) = v1;
+            } else {
+                v0 = v1 = make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+            s = fmaf(v0.x, v0.x, s); s = fmaf(v0.y, v0.y, s); s = fmaf(v0.z, v0.z, s); s = fmaf(v0.w, v0.w, s);
+            s = fmaf(v1.x, v1.x, s); s = fmaf(v1.y, v1.y, s); s = fmaf(v1.z, v1.z, s); s = fmaf(v1.w, v1.w, s);
+            const float4 u0 = make_float4(v0.x * gain_s[r], v0.y * gain_s[r + 1], v0.z * gain_s[r + 2], v0.w * gain_s[r + 3]);
+            const float4 u1 = make_float4(v1.x * gain_s[r + 4], v1.y * gain_s[r + 5], v1.z * gain_s[r + 6],
+                                          v1.w * gain_s[r + 7]);
+            bf16x8 hi, lo;
+            split_hi_lo(u0, u1, hi, lo);
+            const size_t i = split_index(m, row0 + r, MT);
+            *reinterpret_cast<bf16x8 *>(a.us + i) = hi;
+            *reinterpret_cast<bf16x8 *>(a.us + i + split_lo(MT)) = lo;
+        }
+        // the nc = 8 threads of a token are 8 aligned consecutive lanes
+        s += __shfl_xor(s, 1);
+        s += __shfl_xor(s, 2);
+        s += __shfl_xor(s, 4);
+        if (e < total && (e & 7) == 0) a.ssq_out[(size_t)(e >> 3) * a.n_groups + group] = s;
+    }
+}
+
 // SWIGLU on ntile consecutive tiles t0.. held in Y (tile p: gate rows at
 // columns 32 p + [0,16), up rows at 32 p + 16 + [0,16)): h columns
 // [16 t0, 16 (t0 + ntile)) of every token; in split layout 8 columns per
@@ -449,6 +493,25 @@ __device__ void plain_epilogue(const GemmArgs &a, const float *Y, int ld, int ro
 // each weight block takes one MFMA and half the activation bytes; column n
 // and column n + 8 are summed (a lane shuffle) once the unit's sums are
 // complete, leaving columns 8-15 zero.
+
+// Split-K partial slots hold this bit pattern (a NaN no arithmetic produces
+// from finite inputs) while empty.  A folder reloads a chunk that still holds
+// it: the arrival counter is bumped without waiting for the partial's stores,
+// which are then still on their way.  The reload count is bounded so that a
+// partial that really holds the pattern (NaN inputs) cannot stall the kernel.
+#define DV_EMPTY_BITS 0xffffffffu
+#define DV_EMPTY_SLOT ((u32x4){DV_EMPTY_BITS, DV_EMPTY_BITS, DV_EMPTY_BITS, DV_EMPTY_BITS})
+#define DV_POLL_MAX 100000
+
+__device__ __forceinline__ f32x4 wait_partial(u32x4 r, __amdgpu_buffer_rsrc_t pr, uint32_t off)
+{
+    for (int it = 0; it < DV_POLL_MAX; ++it) {
+        if (r[0] != DV_EMPTY_BITS && r[1] != DV_EMPTY_BITS && r[2] != DV_EMPTY_BITS && r[3] != DV_EMPTY_BITS) break;
+        __builtin_amdgcn_s_sleep(1);
+        r = __builtin_amdgcn_raw_buffer_load_b128(pr, off, 0, 16);
+    }
+    return __builtin_bit_cast(f32x4, r);
+}
 
 #ifndef DV_WEIGHT_NT
 #define DV_WEIGHT_NT 1
@@ -698,41 +761,58 @@ __global__ __launch_bounds__(64 * NW) void k_proj(GemmArgs a)
         }
         bool mine = true;
         if (KS > 1) {
-            // publish this split's partial (16-byte stores written through to
-            // the device-coherent level, cache policy sc1); the last arriver
-            // folds them
+            // Count this split's arrival first; the last split to arrive
+            // folds, the others publish their partials (16-byte stores
+            // written through to the device-coherent level, cache policy
+            // sc1).  The folder takes its own partial from registers and
+            // loads the others, reloading a chunk while it still holds the
+            // empty-slot pattern (every slot holds it between launches: the
+            // folder puts it back after reading), so no split ever waits for
+            // its own stores.
             const __amdgpu_buffer_rsrc_t pr =
                 __builtin_amdgcn_make_buffer_rsrc(a.part, (short)0, 0x7fffffff, 0x00020000);
-#pragma unroll
-            for (int c = 0; c < (NE + 64 * NW - 1) / (64 * NW); ++c) {
-                const int e = tid + 64 * NW * c;
-                if (e < NE)
-                    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v[c]), pr,
-                                                           (uint32_t)(((size_t)unit * NE + e) * 16), 0, 16);
-            }
-            // the partial is globally visible once the stores completed
-            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-            __syncthreads();
             if (tid == 0) {
                 const uint32_t old = __hip_atomic_fetch_add(a.cnt + g, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 last_s = old == (uint32_t)(KS - 1);
             }
             __syncthreads();
             mine = last_s != 0;
-            if (mine) {
 #pragma unroll
-                for (int c = 0; c < (NE + 64 * NW - 1) / (64 * NW); ++c) {
-                    const int e = tid + 64 * NW * c;
-                    v[c] = (f32x4){0.f, 0.f, 0.f, 0.f};
-                    if (e < NE) {
-                        for (int k = 0; k < KS; ++k)
-                            v[c] += __builtin_bit_cast(
-                                f32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                                           pr, (uint32_t)(((size_t)(g * KS + k) * NE + e) * 16), 0, 16));
+            for (int c = 0; c < (NE + 64 * NW - 1) / (64 * NW); ++c) {
+                const int e = tid + 64 * NW * c;
+                if (e >= NE) continue;
+                if (!mine) {
+                    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v[c]), pr,
+                                                           (uint32_t)(((size_t)unit * NE + e) * 16), 0, 16);
+                    continue;
+                }
+                // fold in split order, loads of 4 splits in flight together
+                f32x4 sum = (f32x4){0.f, 0.f, 0.f, 0.f};
+                for (int k0 = 0; k0 < KS; k0 += 4) {
+                    u32x4 raw[4];
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const int k = k0 + j;
+                        if (k < KS && k != ks)
+                            raw[j] = __builtin_amdgcn_raw_buffer_load_b128(
+                                pr, (uint32_t)(((size_t)(g * KS + k) * NE + e) * 16), 0, 16);
+                    }
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const int k = k0 + j;
+                        if (k >= KS) break;
+                        if (k == ks) {
+                            sum += v[c];
+                        } else {
+                            const uint32_t off = (uint32_t)(((size_t)(g * KS + k) * NE + e) * 16);
+                            sum += wait_partial(raw[j], pr, off);
+                            __builtin_amdgcn_raw_buffer_store_b128(DV_EMPTY_SLOT, pr, off, 0, 16);
+                        }
                     }
                 }
-                if (tid == 0) __hip_atomic_store(a.cnt + g, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                v[c] = sum;
             }
+            if (mine && tid == 0) __hip_atomic_store(a.cnt + g, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
         if (mine) {
             if (HALF) {
@@ -761,7 +841,8 @@ __global__ __launch_bounds__(64 * NW) void k_proj(GemmArgs a)
             }
             __syncthreads();
             if (EPI == EPI_RESID) {
-                resid_epilogue<uint16_t>(a, Y, LD, g * ROWS, ROWS, g, true, stage_s);
+                if (a.us) resid_epilogue_split(a, Y, LD, g * ROWS, ROWS, g, stage_s);
+                else resid_epilogue<uint16_t>(a, Y, LD, g * ROWS, ROWS, g, true, stage_s);
             } else if (EPI == EPI_LOGITS) {
                 logits_epilogue(a, Y, LD, g * ROWS, ROWS, g, rinv);
             } else if (EPI == EPI_PLAIN) {
