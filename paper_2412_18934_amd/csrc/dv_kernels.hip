@@ -497,20 +497,16 @@ __device__ void plain_epilogue(const GemmArgs &a, const float *Y, int ld, int ro
 // Split-K partial slots hold this bit pattern (a NaN no arithmetic produces
 // from finite inputs) while empty.  A folder reloads a chunk that still holds
 // it: the arrival counter is bumped without waiting for the partial's stores,
-// which are then still on their way.  The reload count is bounded so that a
-// partial that really holds the pattern (NaN inputs) cannot stall the kernel.
+// which are then still on their way; all empty chunks of a round are reloaded
+// together.  The reload count is bounded so that a partial that really holds
+// the pattern (NaN inputs) cannot stall the kernel.
 #define DV_EMPTY_BITS 0xffffffffu
 #define DV_EMPTY_SLOT ((u32x4){DV_EMPTY_BITS, DV_EMPTY_BITS, DV_EMPTY_BITS, DV_EMPTY_BITS})
 #define DV_POLL_MAX 100000
 
-__device__ __forceinline__ f32x4 wait_partial(u32x4 r, __amdgpu_buffer_rsrc_t pr, uint32_t off)
+__device__ __forceinline__ bool slot_empty(const u32x4 &r)
 {
-    for (int it = 0; it < DV_POLL_MAX; ++it) {
-        if (r[0] != DV_EMPTY_BITS && r[1] != DV_EMPTY_BITS && r[2] != DV_EMPTY_BITS && r[3] != DV_EMPTY_BITS) break;
-        __builtin_amdgcn_s_sleep(1);
-        r = __builtin_amdgcn_raw_buffer_load_b128(pr, off, 0, 16);
-    }
-    return __builtin_bit_cast(f32x4, r);
+    return r[0] == DV_EMPTY_BITS || r[1] == DV_EMPTY_BITS || r[2] == DV_EMPTY_BITS || r[3] == DV_EMPTY_BITS;
 }
 
 #ifndef DV_WEIGHT_NT
@@ -647,23 +643,36 @@ __global__ __launch_bounds__(64 * NW) void k_proj(GemmArgs a)
         if constexpr (NEED_RINV) {
             if (load_rinv) rinv_load<NJP>(a, sv);
         }
+        // QKV: the positions of the (m, r) entries qkv_epilogue gives this
+        // thread; the rotary factors themselves are loaded once the first
+        // weight steps are requested (their addresses wait for the positions)
+        int posv[EPI == EPI_QKV ? EPT : 1];
         if constexpr (EPI == EPI_QKV) {
-            // the (m, r) entries qkv_epilogue gives this thread, per 32-row tile
-            const int per_seg = a.N / DV_GEMM_TILE, per_head = a.hd / DV_GEMM_TILE, half = a.hd / 2;
 #pragma unroll
-            for (int p = 0; p < RB / 2; ++p) {
-                const int t = g * (RB / 2) + p, seg = t / per_seg, tt = t - seg * per_seg;
-                const int j0 = (tt - (tt / per_head) * per_head) * 16;
-#pragma unroll
-                for (int c = 0; c < EPT; ++c) {
-                    const int e = tid + 64 * NW * c, m = e / 16, j = j0 + (e % 16);
-                    const bool ok = seg < 2 && e < a.M * 16;
-                    const size_t ti = ok ? (size_t)a.pos[m] * half + j : 0;
-                    rcs[p][c] = ok ? a.rope_cos[ti] : 0.f;
-                    rsn[p][c] = ok ? a.rope_sin[ti] : 0.f;
-                }
+            for (int c = 0; c < EPT; ++c) {
+                const int e = tid + 64 * NW * c;
+                posv[c] = e < a.M * 16 ? a.pos[e / 16] : 0;
             }
         }
+        auto load_rotary = [&]() {
+            if constexpr (EPI == EPI_QKV) {
+                const int per_seg = a.N / DV_GEMM_TILE, per_head = a.hd / DV_GEMM_TILE, half = a.hd / 2;
+#pragma unroll
+                for (int p = 0; p < RB / 2; ++p) {
+                    const int t = g * (RB / 2) + p, seg = t / per_seg, tt = t - seg * per_seg;
+                    const int j0 = (tt - (tt / per_head) * per_head) * 16;
+#pragma unroll
+                    for (int c = 0; c < EPT; ++c) {
+                        const int e = tid + 64 * NW * c, j = j0 + (e % 16);
+                        const bool ok = seg < 2 && e < a.M * 16;
+                        const size_t ti = ok ? (size_t)posv[c] * half + j : 0;
+                        rcs[p][c] = ok ? a.rope_cos[ti] : 0.f;
+                        rsn[p][c] = ok ? a.rope_sin[ti] : 0.f;
+                    }
+                }
+            }
+        };
+        if (n <= 0) load_rotary();
         if (n > 0) {
             u32x4 wb[U][RB], xb[U][MT][XP];
             auto fetch = [&](int j, int i) {
@@ -708,6 +717,19 @@ __global__ __launch_bounds__(64 * NW) void k_proj(GemmArgs a)
                     rs[b] = *reinterpret_cast<const f32x4 *>(a.scale + (g * RB + b) * 16 + 4 * (lane >> 4));
             }
             int i = 0;
+            if (U < n) {
+                // first round; the rotary loads go out once step 0 is in,
+                // when the positions (loaded before it) are in as well
+#pragma unroll
+                for (int j = 0; j < U; ++j) {
+                    mfma(j);
+                    if (j == 0) load_rotary();
+                    fetch(j, min(j + U, n - 1));
+                }
+                i = U;
+            } else {
+                load_rotary();
+            }
             for (; i + U < n; i += U) {
 #pragma unroll
                 for (int j = 0; j < U; ++j) {
@@ -797,6 +819,22 @@ __global__ __launch_bounds__(64 * NW) void k_proj(GemmArgs a)
                             raw[j] = __builtin_amdgcn_raw_buffer_load_b128(
                                 pr, (uint32_t)(((size_t)(g * KS + k) * NE + e) * 16), 0, 16);
                     }
+                    // reload every chunk still empty, all together, until none is
+                    for (int it = 0; it < DV_POLL_MAX; ++it) {
+                        bool any = false;
+#pragma unroll
+                        for (int j = 0; j < 4; ++j)
+                            any |= k0 + j < KS && k0 + j != ks && slot_empty(raw[j]);
+                        if (!any) break;
+                        __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) {
+                            const int k = k0 + j;
+                            if (k < KS && k != ks && slot_empty(raw[j]))
+                                raw[j] = __builtin_amdgcn_raw_buffer_load_b128(
+                                    pr, (uint32_t)(((size_t)(g * KS + k) * NE + e) * 16), 0, 16);
+                        }
+                    }
 #pragma unroll
                     for (int j = 0; j < 4; ++j) {
                         const int k = k0 + j;
@@ -804,9 +842,9 @@ __global__ __launch_bounds__(64 * NW) void k_proj(GemmArgs a)
                         if (k == ks) {
                             sum += v[c];
                         } else {
-                            const uint32_t off = (uint32_t)(((size_t)(g * KS + k) * NE + e) * 16);
-                            sum += wait_partial(raw[j], pr, off);
-                            __builtin_amdgcn_raw_buffer_store_b128(DV_EMPTY_SLOT, pr, off, 0, 16);
+                            sum += __builtin_bit_cast(f32x4, raw[j]);
+                            __builtin_amdgcn_raw_buffer_store_b128(
+                                DV_EMPTY_SLOT, pr, (uint32_t)(((size_t)(g * KS + k) * NE + e) * 16), 0, 16);
                         }
                     }
                 }
@@ -1280,6 +1318,9 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mfma(AttnArgs a)
     // waits) merges the splits of every node in split order: a softmax-
     // weighted sum with a running maximum (base-2 units), then the output in
     // split layout, 8 dims of one node per thread.
+    // (the partials were published without waiting for the stores: the
+    // merging split reloads any value that still holds the empty-slot
+    // pattern, and empties every slot it read for the next launch)
     __shared__ int last_s;
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
