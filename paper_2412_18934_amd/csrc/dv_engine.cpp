@@ -414,7 +414,7 @@ int enqueue_forward(dv_handle *h, const dv_kv *kv, float *out_logits, bool with_
     AcceptArgs ac{};
     ac.arg_val = h->arg_val;
     ac.arg_idx = h->arg_idx;
-    ac.n_parts = h->p_lm.n_groups;
+    ac.n_parts = step_plan(h->p_lm, EPI_LOGITS, h->wkind, mt, h->n_cu).n_groups;  // the lm_head launch's groups
     ac.M = M;
     ac.Mpad = Mpad;
     std::memcpy(ac.tokens, sd->tokens, sizeof ac.tokens);

@@ -2453,8 +2453,8 @@ static const void *gemm_kernel(int wkind, int use_mfma, int mt, int rb)
     } else {
         if (wkind != W_F32 && use_mfma) {
             const bool q8 = wkind == W_I8;
-            if constexpr (EPI == EPI_SWIGLU) {
-                if (rb == 8 && !q8) return proj_kernel_mt<EPI, uint16_t, 8, false>(mt);
+            if constexpr (EPI == EPI_SWIGLU || EPI == EPI_LOGITS) {
+                if (rb == 8) return q8 ? proj_kernel_mt<EPI, uint16_t, 8, true>(mt) : proj_kernel_mt<EPI, uint16_t, 8, false>(mt);
             }
             if (rb == 8) return nullptr;
             if (rb == 4) return q8 ? proj_kernel_mt<EPI, uint16_t, 4, true>(mt) : proj_kernel_mt<EPI, uint16_t, 4, false>(mt);
