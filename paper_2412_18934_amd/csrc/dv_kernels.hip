@@ -374,11 +374,8 @@ __device__ void swiglu_epilogue(const GemmArgs &a, const float *Y, int ld, int t
 // QKV on the 32-row tile t held in Y[m * ld + 0..32): rotary embedding of q
 // and k at each token's position, q to the query buffer, k and v (rounded to
 // the cache type) to cache slots P + m.
-// EPT > 0: the rotary factors of this thread's entries (iteration c of the
-// loop below) were loaded beforehand into cs[c], sn[c].
-template <typename KV, int EPT = 0>
-__device__ void qkv_epilogue(const GemmArgs &a, const float *Y, int ld, int t, const float *rinv,
-                             const float *cs = nullptr, const float *sn = nullptr)
+template <typename KV>
+__device__ void qkv_epilogue(const GemmArgs &a, const float *Y, int ld, int t, const float *rinv)
 {
     const int tid = threadIdx.x, nt = blockDim.x;
     {
@@ -387,14 +384,14 @@ __device__ void qkv_epilogue(const GemmArgs &a, const float *Y, int ld, int t, c
         const int per_head = a.hd / DV_GEMM_TILE;
         const int h = tt / per_head, j0 = (tt - h * per_head) * 16;
         const int half = a.hd / 2;
-        for (int e = tid, it = 0; e < a.M * 16; e += nt, ++it) {
+        for (int e = tid; e < a.M * 16; e += nt) {
             const int m = e / 16, r = e % 16;
             const int j = j0 + r;
             float y1 = Y[m * ld + r] * rinv[m], y2 = Y[m * ld + 16 + r] * rinv[m];
             if (seg < 2) {
                 const int pos = a.pos[m];  // P + depth(m) - 1
-                const float c = EPT > 0 ? cs[it] : a.rope_cos[(size_t)pos * half + j];
-                const float s = EPT > 0 ? sn[it] : a.rope_sin[(size_t)pos * half + j];
+                const float c = a.rope_cos[(size_t)pos * half + j];
+                const float s = a.rope_sin[(size_t)pos * half + j];
                 const float o1 = y1 * c - y2 * s, o2 = y2 * c + y1 * s;
                 y1 = o1;
                 y2 = o2;
@@ -605,7 +602,12 @@ __global__ __launch_bounds__(64 * NW) void k_proj(GemmArgs a)
     constexpr bool NEED_RINV = EPI != EPI_RESID && EPI != EPI_PLAIN;
     constexpr int NJP = MT >= 2 ? 8 : 24;                            // norm partials per thread
     constexpr int SXN = (16 * MT * ROWS + 64 * NW - 1) / (64 * NW);  // RESID: x values per thread
-    constexpr int EPT = (16 * 16 * MT + 64 * NW - 1) / (64 * NW);    // QKV: rotary entries per thread and tile
+    // QKV and gate/up compute the input's 1/rms right after requesting their
+    // first weight steps, so every wave waits for those steps before
+    // streaming on; measured faster than preloading the partials (13B: QKV
+    // 28.0 -> 26.9 us, gate/up 44.5 -> 43.6 us), while lm_head is faster
+    // with the preload (51.4 against 53.2 us)
+    constexpr bool RINV_FIRST = EPI == EPI_QKV || EPI == EPI_SWIGLU;
     static_assert(ROWS <= 64 * NW, "one gain per thread");
 
     for (int unit = blockIdx.x; unit < a.n_units; unit += gridDim.x) {
@@ -629,8 +631,6 @@ __global__ __launch_bounds__(64 * NW) void k_proj(GemmArgs a)
         f32x4 rs[Q8 ? RB : 1];  // int8: this lane's four row scales per block
         float sx[EPI == EPI_RESID ? SXN : 1], sgain = 0.f;
         float sv[NEED_RINV ? NJP : 1];
-        float rcs[EPI == EPI_QKV ? RB / 2 : 1][EPI == EPI_QKV ? EPT : 1];
-        float rsn[EPI == EPI_QKV ? RB / 2 : 1][EPI == EPI_QKV ? EPT : 1];
         const bool load_rinv = NEED_RINV && !have_rinv;
         if constexpr (EPI == EPI_RESID) {
 #pragma unroll
@@ -640,39 +640,9 @@ __global__ __launch_bounds__(64 * NW) void k_proj(GemmArgs a)
             }
             if (tid < ROWS) sgain = Elem<uint16_t>::load(reinterpret_cast<const uint16_t *>(a.gain), g * ROWS + tid);
         }
-        if constexpr (NEED_RINV) {
+        if constexpr (NEED_RINV && !RINV_FIRST) {
             if (load_rinv) rinv_load<NJP>(a, sv);
         }
-        // QKV: the positions of the (m, r) entries qkv_epilogue gives this
-        // thread; the rotary factors themselves are loaded once the first
-        // weight steps are requested (their addresses wait for the positions)
-        int posv[EPI == EPI_QKV ? EPT : 1];
-        if constexpr (EPI == EPI_QKV) {
-#pragma unroll
-            for (int c = 0; c < EPT; ++c) {
-                const int e = tid + 64 * NW * c;
-                posv[c] = e < a.M * 16 ? a.pos[e / 16] : 0;
-            }
-        }
-        auto load_rotary = [&]() {
-            if constexpr (EPI == EPI_QKV) {
-                const int per_seg = a.N / DV_GEMM_TILE, per_head = a.hd / DV_GEMM_TILE, half = a.hd / 2;
-#pragma unroll
-                for (int p = 0; p < RB / 2; ++p) {
-                    const int t = g * (RB / 2) + p, seg = t / per_seg, tt = t - seg * per_seg;
-                    const int j0 = (tt - (tt / per_head) * per_head) * 16;
-#pragma unroll
-                    for (int c = 0; c < EPT; ++c) {
-                        const int e = tid + 64 * NW * c, j = j0 + (e % 16);
-                        const bool ok = seg < 2 && e < a.M * 16;
-                        const size_t ti = ok ? (size_t)posv[c] * half + j : 0;
-                        rcs[p][c] = ok ? a.rope_cos[ti] : 0.f;
-                        rsn[p][c] = ok ? a.rope_sin[ti] : 0.f;
-                    }
-                }
-            }
-        };
-        if (n <= 0) load_rotary();
         if (n > 0) {
             u32x4 wb[U][RB], xb[U][MT][XP];
             auto fetch = [&](int j, int i) {
@@ -716,25 +686,23 @@ __global__ __launch_bounds__(64 * NW) void k_proj(GemmArgs a)
                 for (int b = 0; b < RB; ++b)
                     rs[b] = *reinterpret_cast<const f32x4 *>(a.scale + (g * RB + b) * 16 + 4 * (lane >> 4));
             }
-            int i = 0;
-            if (U < n) {
-                // first round; the rotary loads go out once step 0 is in,
-                // when the positions (loaded before it) are in as well
-#pragma unroll
-                for (int j = 0; j < U; ++j) {
-                    mfma(j);
-                    if (j == 0) load_rotary();
-                    fetch(j, min(j + U, n - 1));
+            if constexpr (RINV_FIRST) {
+                // the first unit's weight steps are in flight
+                if (!have_rinv) {
+                    input_rinv(a, rinv);
+                    have_rinv = true;
                 }
-                i = U;
-            } else {
-                load_rotary();
             }
+            int i = 0;
             for (; i + U < n; i += U) {
 #pragma unroll
                 for (int j = 0; j < U; ++j) {
                     mfma(j);
                     fetch(j, min(i + j + U, n - 1));
+                    // keep step j's loads ahead of step j + 1's MFMAs: the
+                    // scheduler would otherwise move every load of the round
+                    // behind the last MFMA, emptying the pipeline each round
+                    __builtin_amdgcn_sched_barrier(0);
                 }
             }
 #pragma unroll
@@ -757,9 +725,15 @@ __global__ __launch_bounds__(64 * NW) void k_proj(GemmArgs a)
             }
             if (tid < ROWS) stage_s[tid] = sgain;
         }
-        if constexpr (NEED_RINV) {
+        if constexpr (NEED_RINV && !RINV_FIRST) {
             if (load_rinv) {
                 rinv_finish<NJP>(a, sv, rinv);
+                have_rinv = true;
+            }
+        }
+        if constexpr (RINV_FIRST) {
+            if (!have_rinv) {  // a unit without k-steps for this workgroup's waves
+                input_rinv(a, rinv);
                 have_rinv = true;
             }
         }
@@ -889,8 +863,7 @@ __global__ __launch_bounds__(64 * NW) void k_proj(GemmArgs a)
                 swiglu_epilogue(a, Y, LD, g * (RB / 2), RB / 2, rinv);
             } else {
 #pragma unroll
-                for (int p = 0; p < RB / 2; ++p)
-                    qkv_epilogue<KV, EPT>(a, Y + 32 * p, LD, g * (RB / 2) + p, rinv, rcs[p], rsn[p]);
+                for (int p = 0; p < RB / 2; ++p) qkv_epilogue<KV>(a, Y + 32 * p, LD, g * (RB / 2) + p, rinv);
             }
         }
         __syncthreads();
@@ -2453,8 +2426,11 @@ static const void *gemm_kernel(int wkind, int use_mfma, int mt, int rb)
     } else {
         if (wkind != W_F32 && use_mfma) {
             const bool q8 = wkind == W_I8;
-            if constexpr (EPI == EPI_SWIGLU || EPI == EPI_LOGITS) {
+            if constexpr (EPI == EPI_SWIGLU) {
                 if (rb == 8) return q8 ? proj_kernel_mt<EPI, uint16_t, 8, true>(mt) : proj_kernel_mt<EPI, uint16_t, 8, false>(mt);
+            }
+            if constexpr (EPI == EPI_LOGITS) {  // bf16 lm_head measured slower in 8-block groups
+                if (rb == 8 && q8) return proj_kernel_mt<EPI, uint16_t, 8, true>(mt);
             }
             if (rb == 8) return nullptr;
             if (rb == 4) return q8 ? proj_kernel_mt<EPI, uint16_t, 4, true>(mt) : proj_kernel_mt<EPI, uint16_t, 4, false>(mt);
