@@ -306,7 +306,7 @@ __device__ void resid_epilogue_split(const GemmArgs &a, const float *Y, int ld, 
                                      const float *gain_s)
 {
     const int tid = threadIdx.x, nt = blockDim.x;
-    const int MT = split_mt(a.Mpad, a.half), nc = nrows >> 3;  // nc = 8 chunks per token (64 rows)
+    const int MT = split_mt(a.Mpad, a.half), nc = nrows >> 3;  // chunks per token: 8 (64 rows) or 4 (32)
     const int total = split_rows(a.Mpad, a.half) * nc;
     for (int e0 = 0; e0 < total; e0 += nt) {
         const int e = e0 + tid;
@@ -333,11 +333,11 @@ __device__ void resid_epilogue_split(const GemmArgs &a, const float *Y, int ld, 
             *reinterpret_cast<bf16x8 *>(a.us + i) = hi;
             *reinterpret_cast<bf16x8 *>(a.us + i + split_lo(MT)) = lo;
         }
-        // the nc = 8 threads of a token are 8 aligned consecutive lanes
+        // the nc threads of a token are nc aligned consecutive lanes
         s += __shfl_xor(s, 1);
         s += __shfl_xor(s, 2);
-        s += __shfl_xor(s, 4);
-        if (e < total && (e & 7) == 0) a.ssq_out[(size_t)(e >> 3) * a.n_groups + group] = s;
+        if (nc == 8) s += __shfl_xor(s, 4);
+        if (e < total && (e & (nc - 1)) == 0) a.ssq_out[(size_t)(e / nc) * a.n_groups + group] = s;
     }
 }
 

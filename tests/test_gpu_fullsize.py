@@ -167,6 +167,20 @@ def test_llama13b_int8_m16_ctx1024():
     torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("m", [16, 11])
+def test_llama7b_width_two_layers(m):
+    """Two layers at the 7B widths with one full or ragged 16-token tile (the
+    8-node workload below runs the half-layout tile): 8-block gate/up groups
+    (172 of them, fewer than the CUs) and 4-block QKV groups (192)."""
+    mc = synth.shrink(synth.LLAMA7B, n_layers=2)
+    wl = synth.Workload("llama7b-2l-bf16-ctx512", mc, context=512, n_tree=m, depth=6, seed_base=250,
+                        weight_seed=251)
+    model = _Model(wl.model, wl.seeds["weights"])
+    model.run(wl)
+    del model
+    torch.cuda.empty_cache()
+
+
 def test_llama7b_m8_ctx512():
     wl = synth.WORKLOADS["llama7b-bf16-m8-ctx512"]
     model = _Model(wl.model, wl.seeds["weights"])
