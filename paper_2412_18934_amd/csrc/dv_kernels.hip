@@ -1848,20 +1848,24 @@ __global__ __launch_bounds__(PF_THREADS) void k_pf_embed(const int32_t *tokens, 
 // The prefill GEMM.  Workgroup = NWR x NWT waves over 64 NWR rows (4 blocks
 // per wave) x 16 TT NWT tokens (TT token tiles per wave).  Per k-step each
 // wave loads its 4 weight blocks into registers, the workgroup stages the
-// activation slab of its token tiles (hi + lo) in LDS (two buffers), and
-// each wave runs 8 TT MFMAs (16x16x32 bf16, hi and lo into the same
-// accumulator).  A wave's loads return in
-// order, so weights and activations share one lead of PF_LEAD k-steps.
-constexpr int PF_LEAD = 4;
-
-
-template <int EPI, int NWR, int NWT, int TT>
+// activation slab of its token tiles (hi + lo) in LDS, and each wave runs
+// 8 TT MFMAs (16x16x32 bf16, hi and lo into the same accumulator).  A
+// wave's loads return in order, so weights and activations share one lead
+// of LEAD k-steps (activations first in each step's loads).  With BPRE the
+// slab is stashed two k-steps ahead into three LDS buffers and each wave
+// reads its B operands one k-step ahead into registers; without it the slab
+// is stashed one k-step ahead into two buffers and read just before use.
+template <int EPI, int NWR, int NWT, int TT, int LEAD, bool BPRE>
 __global__ __launch_bounds__(64 * NWR * NWT) void k_pf_gemm(PfArgs a)
 {
-    constexpr int NW = NWR * NWT, NT = 64 * NW, BW = 4, XT = NWT * TT;
+    constexpr int NW = NWR * NWT, NT = 64 * NW, BW = 4, XT = NWT * TT, NBUF = BPRE ? 3 : 2;
     constexpr int XL = XT * 2 * 64 / NT;  // activation u32x4 each thread stages per k-step
     static_assert(XT * 2 * 64 % NT == 0, "activation slab must split evenly");
-    __shared__ u32x4 xsm[2][XT * 2 * 64];
+    static_assert(LEAD >= (BPRE ? 3 : 2), "the stash needs its loads a k-step earlier");
+    // k-steps per unrolled round: register slots (st % LEAD) and B register
+    // sets (st % 2) are compile-time in it
+    constexpr int UR = (BPRE && LEAD % 2) ? 2 * LEAD : LEAD;
+    __shared__ u32x4 xsm[NBUF][XT * 2 * 64];
     __shared__ float rinv_s[16 * XT];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, tid = threadIdx.x;
     const int wr = wave % NWR, wt = wave / NWR;
@@ -1894,13 +1898,14 @@ __global__ __launch_bounds__(64 * NWR * NWT) void k_pf_gemm(PfArgs a)
 #pragma unroll
     for (int i = 0; i < XL; ++i) xofs[i] = (uint32_t)((tt0 * 128 + tid + NT * i) * 16);
     const uint32_t wstep = (uint32_t)a.NB * 1024u, xstep = (uint32_t)a.MT * 2048u;
-    u32x4 wb[PF_LEAD][BW], stg[PF_LEAD][XL];
+    u32x4 wb[LEAD][BW], stg[LEAD][XL];
     auto fetch = [&](int j, int st) {
+#pragma unroll
+        for (int i = 0; i < XL; ++i)
+            stg[j][i] = __builtin_amdgcn_raw_buffer_load_b128(rx, xofs[i], (uint32_t)st * xstep, 0);
 #pragma unroll
         for (int b = 0; b < BW; ++b)
             wb[j][b] = __builtin_amdgcn_raw_buffer_load_b128(rw, wofs[b], (uint32_t)st * wstep, DV_NT);
-#pragma unroll
-        for (int i = 0; i < XL; ++i) stg[j][i] = __builtin_amdgcn_raw_buffer_load_b128(rx, xofs[i], (uint32_t)st * xstep, 0);
     };
     auto stash = [&](int j, int buf) {
 #pragma unroll
@@ -1911,36 +1916,71 @@ __global__ __launch_bounds__(64 * NWR * NWT) void k_pf_gemm(PfArgs a)
     for (int b = 0; b < BW; ++b)
 #pragma unroll
         for (int t = 0; t < TT; ++t) acc[b][t] = (f32x4){0.f, 0.f, 0.f, 0.f};
-    auto mfma = [&](int j, int buf) {
+    auto mma = [&](int j, int t, const u32x4 &hv, const u32x4 &lv) {
+        const bf16x8 hi = __builtin_bit_cast(bf16x8, hv), lo = __builtin_bit_cast(bf16x8, lv);
 #pragma unroll
-        for (int t = 0; t < TT; ++t) {
-            const bf16x8 hi = __builtin_bit_cast(bf16x8, xsm[buf][((wt * TT + t) * 2 + 0) * 64 + lane]);
-            const bf16x8 lo = __builtin_bit_cast(bf16x8, xsm[buf][((wt * TT + t) * 2 + 1) * 64 + lane]);
-#pragma unroll
-            for (int b = 0; b < BW; ++b) {
-                const bf16x8 w = __builtin_bit_cast(bf16x8, wb[j][b]);
-                acc[b][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, hi, acc[b][t], 0, 0, 0);
-                acc[b][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, lo, acc[b][t], 0, 0, 0);
-            }
+        for (int b = 0; b < BW; ++b) {
+            const bf16x8 w = __builtin_bit_cast(bf16x8, wb[j][b]);
+            acc[b][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, hi, acc[b][t], 0, 0, 0);
+            acc[b][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, lo, acc[b][t], 0, 0, 0);
         }
     };
+    auto xat = [&](int buf, int t, int q) -> u32x4 { return xsm[buf][((wt * TT + t) * 2 + q) * 64 + lane]; };
     // Loads and stashes are issued unconditionally (k-steps past the end
     // re-read the last one and are never used), so the number of loads in
     // flight behind each one is the same on every path and every wait is the
-    // one the pipeline needs.
+    // one the pipeline needs.  K-step st: weights in register slot st % LEAD.
 #pragma unroll
-    for (int j = 0; j < PF_LEAD; ++j) fetch(j, min(j, S - 1));
-    stash(0, 0);
-    __syncthreads();
-    // k-step st uses register slot st % PF_LEAD and LDS buffer st % 2
-    for (int s0 = 0; s0 < S; s0 += PF_LEAD) {
+    for (int j = 0; j < LEAD; ++j) fetch(j, min(j, S - 1));
+    if constexpr (BPRE) {
+        // activations in LDS buffer st % 3, stashed two k-steps ahead; B
+        // operands in register set st % 2, read one k-step ahead.  The
+        // barrier after step st makes step st + 2's stash visible, and every
+        // read of buffer (st + 3) % 3 (step st's operands, read in step
+        // st - 1) is done before step st + 1 overwrites it.
+        u32x4 xb[2][TT][2];
+        auto bread = [&](int r, int buf) {
 #pragma unroll
-        for (int j = 0; j < PF_LEAD; ++j) {
-            const int st = s0 + j;
-            if (st < S) mfma(j, st & 1);
-            stash((j + 1) % PF_LEAD, (st + 1) & 1);
-            fetch(j, min(st + PF_LEAD, S - 1));
-            __syncthreads();
+            for (int t = 0; t < TT; ++t)
+#pragma unroll
+                for (int q = 0; q < 2; ++q) xb[r][t][q] = xat(buf, t, q);
+        };
+        stash(0, 0);
+        stash(1, 1);
+        __syncthreads();
+        bread(0, 0);
+        for (int s0 = 0; s0 < S; s0 += UR) {
+#pragma unroll
+            for (int u = 0; u < UR; ++u) {
+                const int st = s0 + u, j = u % LEAD;
+                if (st < S) {
+#pragma unroll
+                    for (int t = 0; t < TT; ++t) mma(j, t, xb[u & 1][t][0], xb[u & 1][t][1]);
+                }
+                bread((u + 1) & 1, (st + 1) % 3);
+                stash((u + 2) % LEAD, (st + 2) % 3);
+                fetch(j, min(st + LEAD, S - 1));
+                __syncthreads();
+            }
+        }
+    } else {
+        // activations in LDS buffer st % 2, stashed one k-step ahead; the
+        // barrier after step st makes step st + 1's stash visible, and every
+        // read of buffer st % 2 is done before step st + 1 overwrites it
+        stash(0, 0);
+        __syncthreads();
+        for (int s0 = 0; s0 < S; s0 += UR) {
+#pragma unroll
+            for (int u = 0; u < UR; ++u) {
+                const int st = s0 + u, j = u % LEAD;
+                if (st < S) {
+#pragma unroll
+                    for (int t = 0; t < TT; ++t) mma(j, t, xat(st & 1, t, 0), xat(st & 1, t, 1));
+                }
+                stash((u + 1) % LEAD, (st + 1) & 1);
+                fetch(j, min(st + LEAD, S - 1));
+                __syncthreads();
+            }
         }
     }
 
@@ -2636,24 +2676,35 @@ hipError_t launch_pf_embed(const int32_t *tokens, const void *embed, int M, int 
     return hipGetLastError();
 }
 
+#ifndef PF_CFG_MAIN
+#define PF_CFG_MAIN 8, 1, 8, 4, false
+#endif
+#ifndef PF_CFG_RESID
+#define PF_CFG_RESID 4, 2, 4, 4, true
+#endif
+
+template <int EPI, int NWR, int NWT, int TT, int LEAD, bool BPRE>
+static hipError_t pf_launch(const PfArgs &a, hipStream_t s)
+{
+    constexpr int ROWS = 64 * NWR, XT = NWT * TT;
+    if (a.MT % XT) return hipErrorInvalidValue;
+    // 1-D grid of (token groups) x (row tiles rounded up to a multiple of 8)
+    const int n_rt = (a.NB * 16 + ROWS - 1) / ROWS;
+    const dim3 grid((a.MT / XT) * ((n_rt + 7) / 8 * 8));
+    hipLaunchKernelGGL((k_pf_gemm<EPI, NWR, NWT, TT, LEAD, BPRE>), grid, dim3(64 * NWR * NWT), 0, s, a);
+    return hipGetLastError();
+}
+
 hipError_t launch_pf_gemm(const PfArgs &a, int epi, hipStream_t s)
 {
     if (a.K % 32 || a.NB < 1 || a.MT % 8 || a.d % 64 || a.M < 1 || a.M > 16 * a.MT) return hipErrorInvalidValue;
-    // 8 waves of 64 rows x 64 tokens: 256 rows x 128 tokens per workgroup;
-    // 1-D grid of (token tiles) x (row tiles rounded up to a multiple of 8)
-    const int n_rt = (a.NB + 15) / 16;
-    const dim3 grid((a.MT / 8) * ((n_rt + 7) / 8 * 8));
-    if (epi == EPI_RESID) {
-        hipLaunchKernelGGL((k_pf_gemm<EPI_RESID, 4, 2, 4>), grid, dim3(512), 0, s, a);
-    } else if (epi == EPI_QKV) {
+    if (epi == EPI_RESID) return pf_launch<EPI_RESID, PF_CFG_RESID>(a, s);
+    if (epi == EPI_QKV) {
         if (a.hd != 64 && a.hd != 128) return hipErrorInvalidValue;
-        hipLaunchKernelGGL((k_pf_gemm<EPI_QKV, 4, 2, 4>), grid, dim3(512), 0, s, a);
-    } else if (epi == EPI_SWIGLU) {
-        hipLaunchKernelGGL((k_pf_gemm<EPI_SWIGLU, 4, 2, 4>), grid, dim3(512), 0, s, a);
-    } else {
-        return hipErrorInvalidValue;
+        return pf_launch<EPI_QKV, PF_CFG_MAIN>(a, s);
     }
-    return hipGetLastError();
+    if (epi == EPI_SWIGLU) return pf_launch<EPI_SWIGLU, PF_CFG_MAIN>(a, s);
+    return hipErrorInvalidValue;
 }
 
 hipError_t launch_attn_causal(const float *q, const void *kc, const void *vc, int M, int P0, int H, int hd, int cap,
