@@ -1859,8 +1859,9 @@ template <int EPI, int NWR, int NWT, int TT, int LEAD, bool BPRE>
 __global__ __launch_bounds__(64 * NWR * NWT) void k_pf_gemm(PfArgs a)
 {
     constexpr int NW = NWR * NWT, NT = 64 * NW, BW = 4, XT = NWT * TT, NBUF = BPRE ? 3 : 2;
-    constexpr int XL = XT * 2 * 64 / NT;  // activation u32x4 each thread stages per k-step
-    static_assert(XT * 2 * 64 % NT == 0, "activation slab must split evenly");
+    // the activation slab of a k-step: XE u32x4 (hi + lo of XT token
+    // tiles), XL of them staged per thread (whole waves idle past XE)
+    constexpr int XE = XT * 2 * 64, XL = (XE + NT - 1) / NT;
     static_assert(LEAD >= (BPRE ? 3 : 2), "the stash needs its loads a k-step earlier");
     // k-steps per unrolled round: register slots (st % LEAD) and B register
     // sets (st % 2) are compile-time in it
@@ -1870,17 +1871,22 @@ __global__ __launch_bounds__(64 * NWR * NWT) void k_pf_gemm(PfArgs a)
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, tid = threadIdx.x;
     const int wr = wave % NWR, wt = wave / NWR;
     // 1-D grid, XCD-aware: workgroups are dispatched to the 8 XCDs round
-    // robin, so the token tiles of one row tile get the same blockIdx % 8 and
-    // share that XCD's L2 for the row tile's weights
-    const int n_tt = a.MT / XT, n_rt = (a.NB + NWR * BW - 1) / (NWR * BW);
-    const int xcd = blockIdx.x & 7, qq = blockIdx.x >> 3;
-    const int rtile = (qq / n_tt) * 8 + xcd;
-    if (rtile >= n_rt) return;  // padding of the row tiles to a multiple of 8
-    const int tt0 = (qq % n_tt) * XT;                        // first token tile of the workgroup
+    // robin (workgroup b to XCD b % 8, 32 CUs each), so XCD x takes tiles
+    // [x per, (x + 1) per) of the row-tile-major order: every XCD gets the
+    // same count, and the token groups of a row tile share one XCD's L2 for
+    // the row tile's weights (at most two XCDs at a chunk boundary).  Token
+    // groups of XT tiles; the last one may be short (its missing tiles
+    // re-read the last token tile and are never stored).
+    const int n_tt = (a.MT + XT - 1) / XT, n_rt = (a.NB + NWR * BW - 1) / (NWR * BW);
+    const int n_tiles = n_rt * n_tt, per = (n_tiles + 7) / 8;
+    const int L = (blockIdx.x & 7) * per + (blockIdx.x >> 3);
+    if (L >= n_tiles) return;  // padding of the grid to 8 x per
+    const int rtile = L / n_tt;
+    const int tt0 = (L - rtile * n_tt) * XT;                 // first token tile of the workgroup
     const int gb0 = (rtile * NWR + wr) * BW;                 // first block of this wave
     const int S = a.K / 32;
     if (EPI != EPI_RESID) {
-        for (int m = tid; m < 16 * XT; m += NT) {
+        for (int m = tid; m < 16 * min(XT, a.MT - tt0); m += NT) {
             const float *p = a.ssq_in + (size_t)(tt0 * 16 + m) * a.nsq_in;
             float sum = 0.f;
             for (int c = 0; c < a.nsq_in; ++c) sum += p[c];
@@ -1896,7 +1902,10 @@ __global__ __launch_bounds__(64 * NWR * NWT) void k_pf_gemm(PfArgs a)
 #pragma unroll
     for (int b = 0; b < BW; ++b) wofs[b] = (uint32_t)(min(gb0 + b, a.NB - 1) * 1024 + lane * 16);
 #pragma unroll
-    for (int i = 0; i < XL; ++i) xofs[i] = (uint32_t)((tt0 * 128 + tid + NT * i) * 16);
+    for (int i = 0; i < XL; ++i) {
+        const int e = min(tid + NT * i, XE - 1), tile = min(tt0 + e / 128, a.MT - 1);
+        xofs[i] = (uint32_t)((tile * 128 + e % 128) * 16);
+    }
     const uint32_t wstep = (uint32_t)a.NB * 1024u, xstep = (uint32_t)a.MT * 2048u;
     u32x4 wb[LEAD][BW], stg[LEAD][XL];
     auto fetch = [&](int j, int st) {
@@ -1909,7 +1918,8 @@ __global__ __launch_bounds__(64 * NWR * NWT) void k_pf_gemm(PfArgs a)
     };
     auto stash = [&](int j, int buf) {
 #pragma unroll
-        for (int i = 0; i < XL; ++i) xsm[buf][tid + NT * i] = stg[j][i];
+        for (int i = 0; i < XL; ++i)
+            if (XE % NT == 0 || tid + NT * i < XE) xsm[buf][tid + NT * i] = stg[j][i];
     };
     f32x4 acc[BW][TT];
 #pragma unroll
@@ -2046,6 +2056,7 @@ __global__ __launch_bounds__(64 * NWR * NWT) void k_pf_gemm(PfArgs a)
             const int f0 = 16 * (gb >> 1) + r4;
 #pragma unroll
             for (int t = 0; t < TT; ++t) {
+                if (tt0 + wt * TT + t >= a.MT) break;  // a short last token group
                 const int ml = (wt * TT + t) * 16 + n16, m = tt0 * 16 + ml;
                 float hv[4] = {0.f, 0.f, 0.f, 0.f};
                 if (m < a.M) {
@@ -2061,6 +2072,7 @@ __global__ __launch_bounds__(64 * NWR * NWT) void k_pf_gemm(PfArgs a)
             const int nsq = a.d / 64;
 #pragma unroll
             for (int t = 0; t < TT; ++t) {
+                if (tt0 + wt * TT + t >= a.MT) break;  // a short last token group (wave-uniform)
                 const int ml = (wt * TT + t) * 16 + n16, m = tt0 * 16 + ml;
                 float ss = 0.f;
 #pragma unroll
@@ -2680,17 +2692,16 @@ hipError_t launch_pf_embed(const int32_t *tokens, const void *embed, int M, int 
 #define PF_CFG_MAIN 8, 1, 8, 4, false
 #endif
 #ifndef PF_CFG_RESID
-#define PF_CFG_RESID 4, 2, 4, 4, true
+#define PF_CFG_RESID 8, 1, 3, 4, true
 #endif
 
 template <int EPI, int NWR, int NWT, int TT, int LEAD, bool BPRE>
 static hipError_t pf_launch(const PfArgs &a, hipStream_t s)
 {
     constexpr int ROWS = 64 * NWR, XT = NWT * TT;
-    if (a.MT % XT) return hipErrorInvalidValue;
-    // 1-D grid of (token groups) x (row tiles rounded up to a multiple of 8)
-    const int n_rt = (a.NB * 16 + ROWS - 1) / ROWS;
-    const dim3 grid((a.MT / XT) * ((n_rt + 7) / 8 * 8));
+    // 1-D grid: 8 chunks of ceil(tiles / 8) (token groups x row tiles)
+    const int n_rt = (a.NB * 16 + ROWS - 1) / ROWS, n_tiles = (a.MT + XT - 1) / XT * n_rt;
+    const dim3 grid(8 * ((n_tiles + 7) / 8));
     hipLaunchKernelGGL((k_pf_gemm<EPI, NWR, NWT, TT, LEAD, BPRE>), grid, dim3(64 * NWR * NWT), 0, s, a);
     return hipGetLastError();
 }
