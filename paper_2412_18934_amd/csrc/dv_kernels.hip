@@ -2593,11 +2593,12 @@ hipError_t launch_attention(const AttnArgs &a, int kv_bf16, hipStream_t s)
 {
     const dim3 grid(a.n_split, a.H), block(256);
     // up to 8 key tiles per split: 8 waves holding one tile each; longer
-    // splits: 4 waves with two tiles in flight each
+    // splits: 4 waves with two tiles in flight each (one query tile) or one
+    // each (more)
     const bool short_split = a.keys_per_split <= 8 * DV_ATTN_TILE;
     const dim3 b8(512), b4(256);
-    // more than 16 nodes: every key tile serves all query tiles (4 waves, one
-    // tile in flight each, so that the per-tile outputs fit the registers)
+    // more than 16 nodes: every key tile serves all query tiles, with the
+    // per-tile outputs in registers
     const int qt = a.tm.Mpad / 16;
     if (qt < 1 || qt > 4) return hipErrorInvalidValue;
     if (!kv_bf16) {
@@ -2607,14 +2608,22 @@ hipError_t launch_attention(const AttnArgs &a, int kv_bf16, hipStream_t s)
         return hipGetLastError();
     }
     if (a.hd == 128) {
-        if (qt == 1 && short_split) hipLaunchKernelGGL((k_attn_mfma<128, 8, false, 1>), grid, b8, 0, s, a);
-        else if (qt == 1) hipLaunchKernelGGL((k_attn_mfma<128, 4, true, 1>), grid, b4, 0, s, a);
+        if (short_split) {
+            if (qt == 1) hipLaunchKernelGGL((k_attn_mfma<128, 8, false, 1>), grid, b8, 0, s, a);
+            else if (qt == 2) hipLaunchKernelGGL((k_attn_mfma<128, 8, false, 2>), grid, b8, 0, s, a);
+            else if (qt == 3) hipLaunchKernelGGL((k_attn_mfma<128, 8, false, 3>), grid, b8, 0, s, a);
+            else hipLaunchKernelGGL((k_attn_mfma<128, 8, false, 4>), grid, b8, 0, s, a);
+        } else if (qt == 1) hipLaunchKernelGGL((k_attn_mfma<128, 4, true, 1>), grid, b4, 0, s, a);
         else if (qt == 2) hipLaunchKernelGGL((k_attn_mfma<128, 4, false, 2>), grid, b4, 0, s, a);
         else if (qt == 3) hipLaunchKernelGGL((k_attn_mfma<128, 4, false, 3>), grid, b4, 0, s, a);
         else hipLaunchKernelGGL((k_attn_mfma<128, 4, false, 4>), grid, b4, 0, s, a);
     } else if (a.hd == 64) {
-        if (qt == 1 && short_split) hipLaunchKernelGGL((k_attn_mfma<64, 8, false, 1>), grid, b8, 0, s, a);
-        else if (qt == 1) hipLaunchKernelGGL((k_attn_mfma<64, 4, true, 1>), grid, b4, 0, s, a);
+        if (short_split) {
+            if (qt == 1) hipLaunchKernelGGL((k_attn_mfma<64, 8, false, 1>), grid, b8, 0, s, a);
+            else if (qt == 2) hipLaunchKernelGGL((k_attn_mfma<64, 8, false, 2>), grid, b8, 0, s, a);
+            else if (qt == 3) hipLaunchKernelGGL((k_attn_mfma<64, 8, false, 3>), grid, b8, 0, s, a);
+            else hipLaunchKernelGGL((k_attn_mfma<64, 8, false, 4>), grid, b8, 0, s, a);
+        } else if (qt == 1) hipLaunchKernelGGL((k_attn_mfma<64, 4, true, 1>), grid, b4, 0, s, a);
         else if (qt == 2) hipLaunchKernelGGL((k_attn_mfma<64, 4, false, 2>), grid, b4, 0, s, a);
         else if (qt == 3) hipLaunchKernelGGL((k_attn_mfma<64, 4, false, 3>), grid, b4, 0, s, a);
         else hipLaunchKernelGGL((k_attn_mfma<64, 4, false, 4>), grid, b4, 0, s, a);
