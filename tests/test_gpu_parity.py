@@ -124,7 +124,10 @@ def test_bf16_empty_context_and_planted_acceptance(bf16_case):
     assert acc.accept_len >= 5
 
 
-def test_bf16_head_dim_64_parity():
+@pytest.mark.parametrize("m", [20, 40, 64])
+def test_bf16_head_dim_64_parity(m):
+    """Head size 64 with 2, 3 and 4 query tiles (the attention's multi-tile
+    variants for that head size)."""
     cfg = small_cfg(n_layers=2, d_model=256, n_heads=4, head_dim=64, d_ffn=528, vocab=1056,
                     weight_dtype="bf16", init_std=0.09)
     case = GpuCase(cfg, seed=81, capacity=224)
@@ -132,7 +135,7 @@ def test_bf16_head_dim_64_parity():
         om = case.w.oracle()
         kv = case.new_kv()
         kv_o = case.synthetic_context(kv, 82, 45)
-        toks, par = synth.random_tree(83, 20, 6, cfg.vocab)
+        toks, par = synth.random_tree(83 + m, m, 6, cfg.vocab)
         ref = _ref(om, kv_o, toks, par)
         acc, lg = case.step(kv, toks, par)
         compare_step(acc, lg, ref, 2e-2)
